@@ -1,0 +1,174 @@
+"""CPU oracle for ParallelMLPs training (fp64, plain C + OpenMP).
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and
+the benchmark's CPU-baseline leg, never by the product package.  The oracle
+trains every MLP on its own with ordinary matrix products, which is the
+result the packed method of Section 3 is constructed to reproduce exactly.
+
+`build()` compiles `pmlp_oracle.c` with gcc into `liboracle.so` next to
+this file; the wrappers below only marshal numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pmlp_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle (plain -O2, no target-specific tuning)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+               "-ffp-contract=off", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = C.CDLL(_LIB)
+        P = C.c_void_p
+        i32, i64, u64, dbl = C.c_int32, C.c_int64, C.c_uint64, C.c_double
+        lib.orc_splitmix64.restype = u64
+        lib.orc_splitmix64.argtypes = [u64]
+        lib.orc_act.restype = dbl
+        lib.orc_act.argtypes = [C.c_int, dbl]
+        lib.orc_act_deriv.restype = dbl
+        lib.orc_act_deriv.argtypes = [C.c_int, dbl]
+        lib.orc_max_threads.restype = C.c_int
+        lib.orc_init_params.restype = C.c_int
+        lib.orc_init_params.argtypes = [i32, i32, i32, P, u64, P, P]
+        lib.orc_forward.restype = C.c_int
+        lib.orc_forward.argtypes = [i32, i32, i32, P, P, P, P, P, i32, P, C.c_int]
+        lib.orc_gradients.restype = C.c_int
+        lib.orc_gradients.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32,
+                                      P, P, P, P, dbl, C.c_int]
+        lib.orc_train.restype = C.c_int
+        lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32, P, P,
+                                  dbl, P, P, P, P, i32, C.c_int]
+        lib.orc_dataset_loss.restype = C.c_int
+        lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, i64,
+                                         i32, P, C.c_int]
+        _lib = lib
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def _c(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=dtype))
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise RuntimeError("oracle %s failed with code %d" % (what, rc))
+
+
+def splitmix64(state: int) -> int:
+    return int(_load().orc_splitmix64(C.c_uint64(state & 0xFFFFFFFFFFFFFFFF)))
+
+
+def act(act_id: int, z: float) -> float:
+    return float(_load().orc_act(act_id, z))
+
+
+def act_deriv(act_id: int, z: float) -> float:
+    return float(_load().orc_act_deriv(act_id, z))
+
+
+def max_threads() -> int:
+    return int(_load().orc_max_threads())
+
+
+def init_params(F: int, O: int, hidden_sizes, seed: int) -> Tuple[np.ndarray, np.ndarray]:
+    hs = _c(hidden_sizes, np.int32)
+    N = int(hs.sum())
+    W1 = np.empty((N, F), np.float32)
+    W2 = np.empty((O, N), np.float32)
+    _check(_load().orc_init_params(F, O, len(hs), _p(hs), C.c_uint64(seed), _p(W1), _p(W2)),
+           "init_params")
+    return W1, W2
+
+
+def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0) -> np.ndarray:
+    """logits [B, M, O] in fp64."""
+    hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
+    W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
+    B, F = Xf.shape
+    O = W2d.shape[0]
+    out = np.empty((B, len(hs), O), np.float64)
+    _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf), B,
+                               _p(out), nthreads), "forward")
+    return out
+
+
+def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
+              with_allowance: bool = True, nthreads: int = 0):
+    """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
+
+    The gradient is that of sum_m L_m, so each model's slice is the gradient
+    of its own mean cross-entropy."""
+    hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
+    W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
+    B, F = Xf.shape
+    O, N = W2d.shape
+    dW1 = np.empty((N, F), np.float64)
+    dW2 = np.empty((O, N), np.float64)
+    loss = np.empty(len(hs), np.float64)
+    allow = np.empty((N, F), np.float64) if with_allowance else None
+    _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
+                                 _p(yi), B, _p(dW1), _p(dW2), _p(loss), _p(allow),
+                                 float(kink_rel), nthreads), "gradients")
+    return dW1, dW2, loss, allow
+
+
+def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
+          lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0):
+    """SGD over the given (offset, length) batches.
+
+    Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
+    subset, entries of the other models are NaN."""
+    hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
+    W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
+    F = Xf.shape[1]
+    O, N = W2d.shape
+    off = np.asarray([b[0] for b in batches], np.int64)
+    ln = np.asarray([b[1] for b in batches], np.int32)
+    if len(batches) and (off.min() < 0 or (off + ln).max() > Xf.shape[0]):
+        raise ValueError("batch outside the sample arrays")
+    W1o = np.full((N, F), np.nan)
+    W2o = np.full((O, N), np.nan)
+    loss = np.full(len(hs), np.nan)
+    sel = None if models is None else _c(models, np.int32)
+    _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf), _p(yi),
+                             len(batches), _p(off), _p(ln), float(lr), _p(W1o), _p(W2o),
+                             _p(loss), _p(sel), 0 if sel is None else len(sel), nthreads),
+           "train")
+    return W1o, W2o, loss
+
+
+def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,
+                 nthreads: int = 0) -> np.ndarray:
+    hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
+    W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
+    S, F = Xf.shape
+    O = W2d.shape[0]
+    loss = np.empty(len(hs), np.float64)
+    _check(_load().orc_dataset_loss(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
+                                    _p(yi), S, chunk, _p(loss), nthreads), "dataset_loss")
+    return loss

@@ -1,0 +1,529 @@
+/*
+ * pmlp_oracle.c -- plain, slow, fp64 CPU oracle for ParallelMLPs training.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
+ * includes this file; only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load it.  It shares no code, header, table or
+ * constant with the HIP implementation.
+ *
+ * What it computes (Farias, Ludermir, Bastos-Filho, "Embarrassingly Parallel
+ * Independent Training of Multi-Layer Perceptrons with Heterogeneous
+ * Architectures", 2022):
+ *
+ *   The packed method (Section 3, the four-step summary after the Scatter Add
+ *   example) is built so that the per-model gradient paths never mix and every
+ *   internal MLP trains exactly as it would alone (Section 3, the paragraph on
+ *   the Scatter Add keeping gradients separate).  The plain definition of the
+ *   result is therefore "train each MLP separately with ordinary matrix
+ *   products", and that is what this file does: for every model m it slices
+ *   its rows of the packed W1 [N,F] and its columns of the packed W2 [O,N],
+ *   runs the three-step forward of Section 3 (input-to-hidden product, hidden
+ *   activation, hidden-to-output product; no biases, as Section 3 drops them),
+ *   a softmax cross-entropy loss, back-propagation (Section 2.3, Section 3)
+ *   and a plain SGD update, batch after batch, in fp64.
+ *
+ *   Readings of points the paper leaves open (loss, optimizer, activation
+ *   kink conventions, initialisation) are listed in the design notes and
+ *   restated at each function below.
+ *
+ * Inputs are fp32 (as the GPU path receives them); all arithmetic and all
+ * weight state are fp64.  Models are processed in parallel with OpenMP; each
+ * model's arithmetic is sequential and independent of the thread count, so
+ * results are bitwise reproducible.
+ *
+ * Parity pins (see tests/test_oracle_*.py): the Scatter Add worked example of
+ * Section 3, the 4-1-2 + 4-2-2 packing example of Section 3, closed forms for
+ * W2 = 0, reductions to textbook matrix products (M = 1 identity; all h = 1),
+ * central finite differences of the loss, the independence invariant, the
+ * pack-equals-alone invariant, activation values against library special
+ * functions, and published splitmix64 output values.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)
+#define ORC_ENOMEM (-2)
+
+/* ------------------------------------------------------------------------ */
+/* Activations.  Ids: 0 identity, 1 ReLU, 2 tanh, 3 sigmoid, 4 ELU(alpha=1), */
+/* 5 LeakyReLU(0.01), 6 GELU (exact: z * normal CDF), 7 SiLU, 8 softplus  */
+/* (beta=1, linear above 20), 9 Swish with beta=2.                          */
+/* Section 3 (last paragraph) applies a different activation to each       */
+/* contiguous portion of the hidden layer; which functions is a workload   */
+/* choice.  Kinks follow the usual autograd conventions: ReLU'(0)=0,        */
+/* LeakyReLU'(0)=0.01, ELU'(0)=1.                                            */
+/* ------------------------------------------------------------------------ */
+
+static double orc_logistic(double x) {
+  /* 1/(1+e^-x) written so that exp never overflows */
+  if (x >= 0.0) {
+    double e = exp(-x);
+    return 1.0 / (1.0 + e);
+  } else {
+    double e = exp(x);
+    return e / (1.0 + e);
+  }
+}
+
+double orc_act(int id, double z) {
+  switch (id) {
+    case 0: return z;
+    case 1: return z > 0.0 ? z : 0.0;
+    case 2: return tanh(z);
+    case 3: return orc_logistic(z);
+    case 4: return z > 0.0 ? z : expm1(z);
+    case 5: return z > 0.0 ? z : 0.01 * z;
+    case 6: return z * (0.5 * erfc(-z / sqrt(2.0))); /* z * Phi(z), erfc keeps Phi accurate for z << 0 */
+    case 7: return z * orc_logistic(z);
+    case 8: return z > 20.0 ? z : (z > 0.0 ? z : 0.0) + log1p(exp(-fabs(z)));
+    case 9: return z * orc_logistic(2.0 * z);
+    default: return NAN;
+  }
+}
+
+double orc_act_deriv(int id, double z) {
+  switch (id) {
+    case 0: return 1.0;
+    case 1: return z > 0.0 ? 1.0 : 0.0;
+    case 2: { double t = tanh(z); return 1.0 - t * t; }
+    case 3: { double s = orc_logistic(z); return s * (1.0 - s); }
+    case 4: return z > 0.0 ? 1.0 : exp(z);
+    case 5: return z > 0.0 ? 1.0 : 0.01;
+    case 6: {
+      double cdf = 0.5 * erfc(-z / sqrt(2.0));
+      double pdf = exp(-0.5 * z * z) / sqrt(2.0 * 3.14159265358979323846);
+      return cdf + z * pdf;
+    }
+    case 7: { double s = orc_logistic(z); return s + z * s * (1.0 - s); }
+    case 8: return z > 20.0 ? 1.0 : orc_logistic(z);
+    case 9: { double s = orc_logistic(2.0 * z); return s + 2.0 * z * s * (1.0 - s); }
+    default: return NAN;
+  }
+}
+
+/* Slope jump across the kink at z = 0 for piecewise-linear activations
+ * (right slope minus left slope); 0 for activations differentiable at 0. */
+static double orc_kink_jump(int id) {
+  switch (id) {
+    case 1: return 1.0;
+    case 5: return 0.99;
+    default: return 0.0;
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Initialisation: U(-1/sqrt(fan_in), +1/sqrt(fan_in)), fan_in = F for W1   */
+/* and h_m for model m's W2.  The paper does not say how weights start; the */
+/* draws come from splitmix64 (Steele, Lea, Flood, OOPSLA 2014) used as a   */
+/* counter-based generator so the value of each weight depends only on      */
+/* (seed, tensor, index):                                                    */
+/*   key = sm(seed);  r = sm(key ^ (tag << 60) ^ idx)                        */
+/*   tag 1: W1, idx = n*F + f;  tag 2: W2, idx = o*N + n                     */
+/*   u = (r >> 40) * 2^-24;  w = (float)(2u - 1) * (float)(1/sqrt(fan_in))  */
+/* where sm(x) is the splitmix64 output for generator state x.               */
+/* ------------------------------------------------------------------------ */
+
+uint64_t orc_splitmix64(uint64_t state) {
+  uint64_t z = state + 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+static float orc_uniform_weight(uint64_t key, uint64_t tag, uint64_t idx, float bound) {
+  uint64_t r = orc_splitmix64(key ^ (tag << 60) ^ idx);
+  double u = (double)(r >> 40) * (1.0 / 16777216.0);
+  float centred = (float)(2.0 * u - 1.0); /* exact: a multiple of 2^-23 in [-1,1) */
+  volatile float w = centred * bound;     /* one fp32 rounding */
+  return w;
+}
+
+int orc_init_params(int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes,
+                    uint64_t seed, float* W1, float* W2) {
+  if (F < 1 || O < 1 || M < 1 || !hidden_sizes || !W1 || !W2) return ORC_EINVAL;
+  int64_t N = 0;
+  for (int m = 0; m < M; ++m) {
+    if (hidden_sizes[m] < 1) return ORC_EINVAL;
+    N += hidden_sizes[m];
+  }
+  uint64_t key = orc_splitmix64(seed);
+  float b1 = (float)(1.0 / sqrt((double)F));
+  for (int64_t n = 0; n < N; ++n)
+    for (int64_t f = 0; f < F; ++f)
+      W1[n * F + f] = orc_uniform_weight(key, 1, (uint64_t)(n * F + f), b1);
+  int64_t n0 = 0;
+  for (int m = 0; m < M; ++m) {
+    int64_t h = hidden_sizes[m];
+    float b2 = (float)(1.0 / sqrt((double)h));
+    for (int64_t o = 0; o < O; ++o)
+      for (int64_t n = n0; n < n0 + h; ++n)
+        W2[o * N + n] = orc_uniform_weight(key, 2, (uint64_t)(o * N + n), b2);
+    n0 += h;
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* One model's forward / backward on one batch, Section 3 and Section 2.3.  */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int F, O, h, act;
+  double* Z;  /* [B,h]  pre-activation */
+  double* H;  /* [B,h]  activation */
+  double* L;  /* [B,O]  logits */
+  double* G;  /* [B,O]  dLoss/dlogits */
+  double* dH; /* [B,h] */
+  double* dZ; /* [B,h] */
+} orc_scratch;
+
+static int orc_scratch_alloc(orc_scratch* s, int B, int h, int F, int O, int act) {
+  s->F = F; s->O = O; s->h = h; s->act = act;
+  s->Z = (double*)malloc(sizeof(double) * (size_t)B * h);
+  s->H = (double*)malloc(sizeof(double) * (size_t)B * h);
+  s->L = (double*)malloc(sizeof(double) * (size_t)B * O);
+  s->G = (double*)malloc(sizeof(double) * (size_t)B * O);
+  s->dH = (double*)malloc(sizeof(double) * (size_t)B * h);
+  s->dZ = (double*)malloc(sizeof(double) * (size_t)B * h);
+  return (s->Z && s->H && s->L && s->G && s->dH && s->dZ) ? ORC_OK : ORC_ENOMEM;
+}
+
+static void orc_scratch_free(orc_scratch* s) {
+  free(s->Z); free(s->H); free(s->L); free(s->G); free(s->dH); free(s->dZ);
+}
+
+/* Forward of one standalone MLP (Section 3, three-step procedure):
+ *   Z = X W1^T   [B,h]      (input-to-hidden product)
+ *   H = act(Z)              (hidden activation)
+ *   L = H W2^T   [B,O]      (hidden-to-output product)
+ * w1 is the model's [h,F] block, w2 its [O,h] block. */
+static void orc_model_forward(const orc_scratch* s, int B, const float* X,
+                              const double* w1, const double* w2) {
+  const int F = s->F, O = s->O, h = s->h;
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < h; ++j) {
+      double acc = 0.0;
+      for (int f = 0; f < F; ++f) acc += (double)X[(int64_t)b * F + f] * w1[(int64_t)j * F + f];
+      s->Z[(int64_t)b * h + j] = acc;
+      s->H[(int64_t)b * h + j] = orc_act(s->act, acc);
+    }
+  for (int b = 0; b < B; ++b)
+    for (int o = 0; o < O; ++o) {
+      double acc = 0.0;
+      for (int j = 0; j < h; ++j) acc += s->H[(int64_t)b * h + j] * w2[(int64_t)o * h + j];
+      s->L[(int64_t)b * O + o] = acc;
+    }
+}
+
+/* Softmax cross-entropy, mean over the batch.  Returns the loss and fills
+ * G = dLoss/dL = (softmax(L) - onehot(y)) / B.  Labels outside [0,O) -> NaN. */
+static double orc_model_ce(const orc_scratch* s, int B, const int32_t* y) {
+  const int O = s->O;
+  double total = 0.0;
+  for (int b = 0; b < B; ++b) {
+    const double* l = s->L + (int64_t)b * O;
+    double* g = s->G + (int64_t)b * O;
+    int yb = y[b];
+    if (yb < 0 || yb >= O) return NAN;
+    double mx = l[0];
+    for (int o = 1; o < O; ++o) mx = l[o] > mx ? l[o] : mx;
+    double se = 0.0;
+    for (int o = 0; o < O; ++o) se += exp(l[o] - mx);
+    double lse = mx + log(se);
+    total += lse - l[yb];
+    for (int o = 0; o < O; ++o) g[o] = (exp(l[o] - lse) - (o == yb ? 1.0 : 0.0)) / (double)B;
+  }
+  return total / (double)B;
+}
+
+/* Back-propagation of the loss through one model (chain rule of the three
+ * forward steps):
+ *   dW2 = G^T H        [O,h]
+ *   dH  = G W2         [B,h]   (W2 before this step's update)
+ *   dZ  = dH * act'(Z)
+ *   dW1 = dZ^T X       [h,F]                                              */
+static void orc_model_backward(const orc_scratch* s, int B, const float* X,
+                               const double* w2, double* dw1, double* dw2) {
+  const int F = s->F, O = s->O, h = s->h;
+  for (int o = 0; o < O; ++o)
+    for (int j = 0; j < h; ++j) {
+      double acc = 0.0;
+      for (int b = 0; b < B; ++b) acc += s->G[(int64_t)b * O + o] * s->H[(int64_t)b * h + j];
+      dw2[(int64_t)o * h + j] = acc;
+    }
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < h; ++j) {
+      double acc = 0.0;
+      for (int o = 0; o < O; ++o) acc += s->G[(int64_t)b * O + o] * w2[(int64_t)o * h + j];
+      s->dH[(int64_t)b * h + j] = acc;
+      s->dZ[(int64_t)b * h + j] = acc * orc_act_deriv(s->act, s->Z[(int64_t)b * h + j]);
+    }
+  for (int j = 0; j < h; ++j)
+    for (int f = 0; f < F; ++f) {
+      double acc = 0.0;
+      for (int b = 0; b < B; ++b) acc += s->dZ[(int64_t)b * h + j] * (double)X[(int64_t)b * F + f];
+      dw1[(int64_t)j * F + f] = acc;
+    }
+}
+
+/* Kink allowance for piecewise-linear activations.  When |Z| lies within
+ * rounding distance of the kink at 0 (|Z| <= kink_rel * sum_f |x_f w_f|), a
+ * correct fp32 evaluation may take either derivative branch; dW1 can then
+ * move by at most
+ *   allow[j,f] = sum over such b of |dH[b,j]| * slope_jump * |X[b,f]|.     */
+static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
+                                 const double* w1, double* allow, double kink_rel) {
+  const int F = s->F, h = s->h;
+  double jump = orc_kink_jump(s->act);
+  for (int64_t i = 0; i < (int64_t)h * F; ++i) allow[i] = 0.0;
+  if (jump == 0.0) return;
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < h; ++j) {
+      double mag = 0.0;
+      for (int f = 0; f < F; ++f) mag += fabs((double)X[(int64_t)b * F + f] * w1[(int64_t)j * F + f]);
+      double z = s->Z[(int64_t)b * h + j];
+      if (fabs(z) <= kink_rel * mag) {
+        double d = fabs(s->dH[(int64_t)b * h + j]) * jump;
+        for (int f = 0; f < F; ++f) allow[(int64_t)j * F + f] += d * fabs((double)X[(int64_t)b * F + f]);
+      }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Packed-layout helpers: model m owns rows [off_m, off_m+h_m) of W1 [N,F]  */
+/* and columns [off_m, off_m+h_m) of W2 [O,N] (Section 3, Figure 2 layout). */
+/* ------------------------------------------------------------------------ */
+
+static int orc_offsets(int M, const int32_t* hs, int64_t* off) {
+  off[0] = 0;
+  for (int m = 0; m < M; ++m) {
+    if (hs[m] < 1) return ORC_EINVAL;
+    off[m + 1] = off[m] + hs[m];
+  }
+  return ORC_OK;
+}
+
+static void orc_take(int64_t N, int F, int O, int64_t off, int h, const double* W1,
+                     const double* W2, double* w1, double* w2) {
+  memcpy(w1, W1 + off * F, sizeof(double) * (size_t)h * F);
+  for (int o = 0; o < O; ++o)
+    for (int j = 0; j < h; ++j) w2[(int64_t)o * h + j] = W2[(int64_t)o * N + off + j];
+}
+
+static void orc_put(int64_t N, int F, int O, int64_t off, int h, const double* w1,
+                    const double* w2, double* W1, double* W2) {
+  if (W1) memcpy(W1 + off * F, w1, sizeof(double) * (size_t)h * F);
+  if (W2)
+    for (int o = 0; o < O; ++o)
+      for (int j = 0; j < h; ++j) W2[(int64_t)o * N + off + j] = w2[(int64_t)o * h + j];
+}
+
+static int orc_check(int F, int O, int M, const int32_t* hs, const int32_t* acts) {
+  if (F < 1 || O < 2 || M < 1 || !hs || !acts) return ORC_EINVAL;
+  for (int m = 0; m < M; ++m)
+    if (hs[m] < 1 || acts[m] < 0 || acts[m] > 9) return ORC_EINVAL;
+  return ORC_OK;
+}
+
+static void orc_set_threads(int nthreads) {
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+}
+
+int orc_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* Forward only: logits [B,M,O] (model-major inside each sample row), the
+ * layout of the Scatter Add result Y[batch, model, out] of Section 3. */
+int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
+                const double* W1, const double* W2, const float* X, int32_t B,
+                double* logits, int nthreads) {
+  if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !logits) return ORC_EINVAL;
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
+  if (!off) return ORC_ENOMEM;
+  orc_offsets(M, hs, off);
+  const int64_t N = off[M];
+  int err = ORC_OK;
+  orc_set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = 0; m < M; ++m) {
+    const int h = hs[m];
+    orc_scratch s;
+    double* w1 = (double*)malloc(sizeof(double) * (size_t)h * F);
+    double* w2 = (double*)malloc(sizeof(double) * (size_t)h * O);
+    if (!w1 || !w2 || orc_scratch_alloc(&s, B, h, F, O, acts[m])) {
+      err = ORC_ENOMEM;
+    } else {
+      orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
+      orc_model_forward(&s, B, X, w1, w2);
+      for (int b = 0; b < B; ++b)
+        for (int o = 0; o < O; ++o)
+          logits[((int64_t)b * M + m) * O + o] = s.L[(int64_t)b * O + o];
+    }
+    orc_scratch_free(&s);
+    free(w1); free(w2);
+  }
+  free(off);
+  return err;
+}
+
+/* Gradients of L = sum_m L_m on one batch, without an update.  dW1 [N,F],
+ * dW2 [O,N], loss [M] (per-model mean cross-entropy).  allow_dW1 [N,F]
+ * (may be NULL) receives the kink allowance described above, with
+ * kink_rel the relative distance to the kink treated as undetermined. */
+int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
+                  const double* W1, const double* W2, const float* X, const int32_t* y,
+                  int32_t B, double* dW1, double* dW2, double* loss, double* allow_dW1,
+                  double kink_rel, int nthreads) {
+  if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !y || !dW1 || !dW2 || !loss)
+    return ORC_EINVAL;
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
+  if (!off) return ORC_ENOMEM;
+  orc_offsets(M, hs, off);
+  const int64_t N = off[M];
+  int err = ORC_OK;
+  orc_set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = 0; m < M; ++m) {
+    const int h = hs[m];
+    orc_scratch s;
+    double* w1 = (double*)malloc(sizeof(double) * (size_t)h * F);
+    double* w2 = (double*)malloc(sizeof(double) * (size_t)h * O);
+    double* g1 = (double*)malloc(sizeof(double) * (size_t)h * F);
+    double* g2 = (double*)malloc(sizeof(double) * (size_t)h * O);
+    double* al = allow_dW1 ? (double*)malloc(sizeof(double) * (size_t)h * F) : NULL;
+    if (!w1 || !w2 || !g1 || !g2 || (allow_dW1 && !al) ||
+        orc_scratch_alloc(&s, B, h, F, O, acts[m])) {
+      err = ORC_ENOMEM;
+    } else {
+      orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
+      orc_model_forward(&s, B, X, w1, w2);
+      loss[m] = orc_model_ce(&s, B, y);
+      orc_model_backward(&s, B, X, w2, g1, g2);
+      orc_put(N, F, O, off[m], h, g1, g2, dW1, dW2);
+      if (al) {
+        orc_model_kink_allow(&s, B, X, w1, al, kink_rel);
+        memcpy(allow_dW1 + off[m] * F, al, sizeof(double) * (size_t)h * F);
+      }
+    }
+    orc_scratch_free(&s);
+    free(w1); free(w2); free(g1); free(g2); free(al);
+  }
+  free(off);
+  return err;
+}
+
+/* SGD training.  Batches are given explicitly as (offset, length) pairs into
+ * the sample arrays X [S,F], y [S]; each batch performs, for every model
+ * independently, forward, loss, backward and the simultaneous update
+ *   W1 -= lr dW1;  W2 -= lr dW2
+ * (dH uses W2 before the update).  W1_out/W2_out receive the final fp64
+ * weights (only the chosen models' entries are written); loss_last [M]
+ * receives each model's loss on the last batch, before that batch's
+ * update.  models/nmodels select a subset of the models (NULL: all).      */
+int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
+              const double* W1, const double* W2, const float* X, const int32_t* y,
+              int32_t nbatches, const int64_t* batch_off, const int32_t* batch_len,
+              double lr, double* W1_out, double* W2_out, double* loss_last,
+              const int32_t* models, int32_t nmodels, int nthreads) {
+  if (orc_check(F, O, M, hs, acts) || nbatches < 0 || !W1 || !W2 || !X || !y ||
+      (nbatches > 0 && (!batch_off || !batch_len)) || !W1_out || !W2_out)
+    return ORC_EINVAL;
+  int Bmax = 1;
+  for (int k = 0; k < nbatches; ++k) {
+    if (batch_len[k] < 1 || batch_off[k] < 0) return ORC_EINVAL;
+    if (batch_len[k] > Bmax) Bmax = batch_len[k];
+  }
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
+  if (!off) return ORC_ENOMEM;
+  orc_offsets(M, hs, off);
+  const int64_t N = off[M];
+  const int count = models ? nmodels : M;
+  int err = ORC_OK;
+  orc_set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < count; ++i) {
+    const int m = models ? models[i] : i;
+    if (m < 0 || m >= M) { err = ORC_EINVAL; continue; }
+    const int h = hs[m];
+    orc_scratch s;
+    double* w1 = (double*)malloc(sizeof(double) * (size_t)h * F);
+    double* w2 = (double*)malloc(sizeof(double) * (size_t)h * O);
+    double* g1 = (double*)malloc(sizeof(double) * (size_t)h * F);
+    double* g2 = (double*)malloc(sizeof(double) * (size_t)h * O);
+    if (!w1 || !w2 || !g1 || !g2 || orc_scratch_alloc(&s, Bmax, h, F, O, acts[m])) {
+      err = ORC_ENOMEM;
+    } else {
+      orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
+      double last = NAN;
+      for (int k = 0; k < nbatches; ++k) {
+        const float* Xb = X + batch_off[k] * F;
+        const int32_t* yb = y + batch_off[k];
+        const int B = batch_len[k];
+        orc_model_forward(&s, B, Xb, w1, w2);
+        last = orc_model_ce(&s, B, yb);
+        orc_model_backward(&s, B, Xb, w2, g1, g2);
+        for (int64_t t = 0; t < (int64_t)h * F; ++t) w1[t] -= lr * g1[t];
+        for (int64_t t = 0; t < (int64_t)h * O; ++t) w2[t] -= lr * g2[t];
+      }
+      if (loss_last) loss_last[m] = last;
+      orc_put(N, F, O, off[m], h, w1, w2, W1_out, W2_out);
+    }
+    orc_scratch_free(&s);
+    free(w1); free(w2); free(g1); free(g2);
+  }
+  free(off);
+  return err;
+}
+
+/* Mean cross-entropy of every model over a whole sample set (no update),
+ * evaluated in chunks of at most chunk samples. */
+int orc_dataset_loss(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
+                     const double* W1, const double* W2, const float* X, const int32_t* y,
+                     int64_t S, int32_t chunk, double* loss, int nthreads) {
+  if (orc_check(F, O, M, hs, acts) || S < 1 || chunk < 1 || !W1 || !W2 || !X || !y || !loss)
+    return ORC_EINVAL;
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
+  if (!off) return ORC_ENOMEM;
+  orc_offsets(M, hs, off);
+  const int64_t N = off[M];
+  int err = ORC_OK;
+  orc_set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = 0; m < M; ++m) {
+    const int h = hs[m];
+    orc_scratch s;
+    double* w1 = (double*)malloc(sizeof(double) * (size_t)h * F);
+    double* w2 = (double*)malloc(sizeof(double) * (size_t)h * O);
+    if (!w1 || !w2 || orc_scratch_alloc(&s, chunk, h, F, O, acts[m])) {
+      err = ORC_ENOMEM;
+    } else {
+      orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
+      double total = 0.0;
+      for (int64_t s0 = 0; s0 < S; s0 += chunk) {
+        int B = (int)((S - s0) < chunk ? (S - s0) : chunk);
+        orc_model_forward(&s, B, X + s0 * F, w1, w2);
+        total += orc_model_ce(&s, B, y + s0) * B;
+      }
+      loss[m] = total / (double)S;
+    }
+    orc_scratch_free(&s);
+    free(w1); free(w2);
+  }
+  free(off);
+  return err;
+}
