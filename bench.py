@@ -1,0 +1,207 @@
+"""Benchmark: packed ParallelMLPs SGD training steps on one MI355X.
+
+One step = one batch through the whole hot path (batch packing, the
+input-layer GEMM, fused activation + M3 forward, per-model softmax
+cross-entropy, M3 backward with the W2 update, and the dW1 GEMM with the
+W1 update).  Inputs are seeded synthetic data shaped like the paper's
+simulated workloads, resident in GPU memory before timing; weights start
+from the library's seeded initialisation.
+
+Prints ONE JSON line with the throughput in model-samples trained per
+second, the roofline position of the dominant kernel (per-kernel times
+from HIP events recorded on the library's stream inside the timed region)
+and the CPU oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import pmlp_workloads as wl  # noqa: E402
+
+METRIC = "model-samples trained/sec (fwd+bwd+SGD) + % MFMA/HBM roofline, 10k MLPs"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
+PEAK_FP32_MFMA = 157.3         # TFLOP/s, dense fp32 matrix
+PEAK_BF16_MFMA = 2500.0        # TFLOP/s, dense bf16 matrix
+
+
+def kernel_work(name, B, F, N, M, O):
+    """(bound, algorithmic bytes, algorithmic flops) of one launch.
+
+    Bytes count each tensor the kernel must read or write once (fp32);
+    flops count multiply-adds as two operations."""
+    f4 = 4.0
+    if name == "gemm_fwd":      # Z = X W1^T: read W1, X; write Z
+        return "mfma", f4 * (N * F + B * F + N * B), 2.0 * B * F * N
+    if name == "gemm_bwd":      # W1 -= lr dZ^T X: read dZ, X; read+write W1
+        return "mfma", f4 * (N * B + B * F + 2 * N * F), 2.0 * B * F * N
+    if name == "m3_fwd":        # read Z, W2; write logits
+        return "hbm", f4 * (N * B + O * N + B * M * O), 2.0 * B * O * N
+    if name == "m3_bwd":        # read Z, G, W2; write dZ, W2
+        return "hbm", f4 * (2 * N * B + 2 * O * N + B * M * O), 4.0 * B * O * N
+    if name == "ce":            # read logits, y; write G, loss
+        return "hbm", f4 * (2 * B * M * O + B + M), 0.0
+    if name == "pack_x":        # read X; write two padded copies
+        return "hbm", f4 * 3 * B * F, 0.0
+    return "hbm", 0.0, 0.0
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if
+    they were taken on the current kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        table = json.load(open(path))
+    except ValueError:
+        return None
+    src = os.path.join(ROOT, "paper_2206_08369_amd", "csrc", "kernels.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    ent = table.get("%s/%s" % (kernel, workload))
+    if not ent or ent.get("kernels_sha") != digest:
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(w, hs, acts, X, y, seconds_hint: float):
+    """Oracle (every MLP trained alone, fp64, OpenMP over models) on a
+    strided subset of the models for one batch; the rate is extrapolated to
+    the whole pack by total hidden units (the oracle's cost is linear in
+    each model's width)."""
+    import oracle
+    oracle.build(force=False)
+    cores = len(os.sched_getaffinity(0))
+    if os.environ.get("OMP_NUM_THREADS", "").isdigit():
+        cores = max(1, min(cores, int(os.environ["OMP_NUM_THREADS"])))
+    N = int(hs.sum())
+    # choose the stride so that the sample costs roughly seconds_hint
+    flop_all = (4.0 * w.F + 6.0 * w.O) * N * w.B
+    est_rate = 1.0e9 * cores                    # ~1 GFLOP/s per core, plain loops
+    stride = int(max(1, round(flop_all / (est_rate * seconds_hint))))
+    models = np.arange(0, w.M, stride)
+    W1, W2 = oracle.init_params(w.F, w.O, hs[models], 1)   # any weights: cost is data-independent
+    t0 = time.perf_counter()
+    oracle.train(hs[models], acts[models], W1, W2, X[:w.B], y[:w.B], [(0, w.B)], w.lr,
+                 nthreads=cores)
+    dt = time.perf_counter() - t0
+    sub_h = float(hs[models].sum())
+    rate = w.M * w.B / (dt * N / sub_h)
+    return {
+        "value": rate, "unit": "model-samples/s", "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": "every %d-th model (%d of %d models, %d of %d hidden units), one batch of %d "
+                  "samples, fp64, %.1f s; rate scaled to the full pack by total hidden units"
+                  % (stride, len(models), w.M, int(sub_h), N, w.B, dt),
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="w10k_f100", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time of the oracle baseline sample (0 = skip)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the packed models are independent, so "
+              "a multi-GPU run would shard the model list with no per-step exchange; "
+              "that path is not built here.", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2206_08369_amd as pm
+
+    torch.cuda.set_device(0)
+    w = wl.WORKLOADS[args.workload]
+    hs, acts = w.model_grid()
+    X, y = wl.workload_dataset(w)
+    N, M = int(hs.sum()), w.M
+    Xd = torch.from_numpy(X).cuda()
+    yd = torch.from_numpy(y).cuda()
+    nfull = w.S // w.B
+    net = pm.PackedMLP(w.F, w.O, hs, acts, seed=w.init_seed,
+                       precision=pm.PMLP_BF16_GEMM if args.precision == "bf16" else pm.PMLP_FP32)
+
+    def step(k):
+        s = (k % nfull) * w.B
+        net.train_step(Xd[s:s + w.B], yd[s:s + w.B], w.lr)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    net.profile_reset()
+    net.set_profiling(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(args.warmup + k)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    times = net.kernel_times()
+    net.set_profiling(False)
+    losses = net.losses()
+    if not np.all(np.isfinite(losses)):
+        print("non-finite losses after the timed steps", file=sys.stderr)
+        return 1
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = M * w.B * args.steps / elapsed
+    kernels = {}
+    for name, (ms, n) in times.items():
+        if n == 0:
+            continue
+        bound, nbytes, flops = kernel_work(name, w.B, w.F, N, M, w.O)
+        avg = ms / n
+        kernels[name] = {"avg_ms": avg, "launches": n,
+                         "gbs": nbytes / (avg * 1e-3) / 1e9 if nbytes else None,
+                         "tflops": flops / (avg * 1e-3) / 1e12 if flops else None}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    bound, nbytes, flops = kernel_work(dom, w.B, w.F, N, M, w.O)
+    avg_s = kernels[dom]["avg_ms"] * 1e-3
+    if bound == "mfma":
+        peak = PEAK_BF16_MFMA if args.precision == "bf16" else PEAK_FP32_MFMA
+        achieved, unit = flops / avg_s / 1e12, "TFLOP/s"
+    else:
+        peak, achieved, unit = PEAK_HBM_GBS, nbytes / avg_s / 1e9, "GB/s"
+    roofline = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                "frac": achieved / peak, "traffic": load_traffic(dom, w.name),
+                "kernel": dom}
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(w, hs, acts, X, y, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "model-samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if args.precision == "fp32" else "bf16-gemm/f32",
+        "data": "synthetic (seeded X ~ N(0,1), linear-teacher labels; seeded weight init)",
+        "config": {"workload": w.name, "models": M, "hidden_units": N, "F": w.F, "O": w.O,
+                   "batch": w.B, "samples": w.S, "hidden_sizes": "%d..%d" % w.sizes,
+                   "activations": len(w.acts)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

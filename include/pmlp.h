@@ -1,0 +1,167 @@
+/*
+ * pmlp.h -- C ABI of libpmlp: packed training of many independent
+ * one-hidden-layer MLPs ("ParallelMLPs", Farias, Ludermir and Bastos-Filho,
+ * 2022) on one AMD Instinct MI355X (gfx950).
+ *
+ * The problem (Section 3): M independent MLPs share the input features and
+ * are trained on the same batches.  Model m has h_m hidden units, its own
+ * activation function and no biases (Section 3 drops them).  The hidden
+ * units of all models are concatenated into one wide layer of
+ * N = sum_m h_m units (Section 3, Figure 2); model m owns the contiguous
+ * units [off_m, off_m + h_m).  The hidden-to-output product is replaced by
+ * the paper's Modified Matrix Multiplication: an elementwise product of the
+ * hidden activations with the output weights followed by a scatter-add
+ * keyed by model id (Section 3, Scatter Add definition and the four-step
+ * procedure after it), so the per-model gradient paths never mix.
+ *
+ * Parameter layout (what pmlp_get_params / pmlp_set_params exchange):
+ *   W1 [N, F] row-major  -- row n holds the input weights of hidden unit n
+ *                           (the paper's W_{hid,in}).
+ *   W2 [O, N] row-major  -- column n holds the output weights of hidden
+ *                           unit n towards its own model's O outputs.
+ * Per-model outputs are laid out as [B, M, O] (o fastest), the paper's
+ * Y[batch, model, out].
+ *
+ * Each training step does, for every model independently: forward,
+ * softmax cross-entropy averaged over the batch, back-propagation and a
+ * plain SGD update with one learning rate (W1 -= lr dW1, W2 -= lr dW2,
+ * both gradients taken at the pre-update weights).
+ *
+ * Activation ids: 0 identity, 1 ReLU, 2 tanh, 3 logistic sigmoid,
+ * 4 ELU (alpha 1), 5 LeakyReLU (slope 0.01), 6 GELU (exact, z * normal
+ * CDF), 7 SiLU, 8 softplus (beta 1, identity above 20), 9 Swish with
+ * beta 2 (z * sigmoid(2z)).  Derivatives at the kinks: ReLU'(0) = 0,
+ * LeakyReLU'(0) = 0.01, ELU'(0) = 1.
+ *
+ * Conventions for every call:
+ *   - Return value: PMLP_OK (0) or a negative PMLP_E* code; a message for
+ *     the last failure on the calling thread is in pmlp_last_error().
+ *   - "_dev" pointers are device memory on the handle's device; "_host"
+ *     pointers are ordinary host memory.  The caller owns every buffer it
+ *     passes and must keep it alive until the handle's stream has reached
+ *     the call (enqueueing calls return before the GPU work is done).
+ *   - Enqueueing calls (pmlp_forward, pmlp_train_step, pmlp_gradients,
+ *     pmlp_hidden) never synchronise.  Device-side problems such as labels
+ *     outside [0, O) are recorded on the device and reported by the next
+ *     synchronising call (pmlp_losses).
+ *   - A handle is not thread-safe; use one handle per thread or serialise.
+ *   - Sizes: B >= 1 samples per batch; rows of X_dev are F contiguous
+ *     floats (row stride F).  Batches of any size up to 2^20 are accepted;
+ *     internal workspaces grow to the largest batch seen.
+ */
+#ifndef PMLP_H
+#define PMLP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PMLP_OK 0
+#define PMLP_EINVAL (-1)  /* bad argument (null pointer, size, id, lr) */
+#define PMLP_ENOMEM (-2)  /* device or host allocation failed; state unchanged */
+#define PMLP_EDEVICE (-3) /* HIP runtime error; see pmlp_last_error() */
+#define PMLP_ESTATE (-4)  /* call not valid in the current state */
+
+#define PMLP_FP32 0       /* fp32 operands, fp32 accumulation (default) */
+#define PMLP_BF16_GEMM 1  /* the two input-layer GEMMs take bf16-rounded
+                             operands with fp32 accumulation */
+
+#define PMLP_NUM_ACTS 10
+
+typedef struct pmlp* pmlp_t;
+
+/* Create a packed model of M MLPs with F inputs and O outputs each.
+ * hidden_sizes[M] (each >= 1) and act_ids[M] (each in [0, 9]) are copied;
+ * models are packed in the given order.  Weights start uniform in
+ * (-1/sqrt(fan_in), +1/sqrt(fan_in)) with fan_in = F for W1 and h_m for
+ * model m's W2, drawn from a counter-based splitmix64 stream:
+ *   key = sm(seed); r = sm(key ^ (tag << 60) ^ idx), tag 1 for W1
+ *   (idx = n*F + f), tag 2 for W2 (idx = o*N + n); u = (r >> 40) * 2^-24;
+ *   w = (float)(2u - 1) * (float)(1/sqrt(fan_in))
+ * where sm(x) is the splitmix64 output for state x (Steele, Lea and
+ * Flood, OOPSLA 2014).  Requires F >= 1, O >= 2, M >= 1.  Uses the
+ * current HIP device; the stream defaults to the null stream.
+ * On success *out receives a handle the caller frees with pmlp_destroy. */
+int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M,
+                const int32_t* hidden_sizes, const int32_t* act_ids,
+                uint64_t seed);
+
+/* Free the handle and every device buffer it owns (synchronises its
+ * stream first).  A null handle is accepted. */
+int pmlp_destroy(pmlp_t h);
+
+/* Launch all later work on `stream` (a hipStream_t, passed as void*;
+ * null selects the null stream).  The stream must belong to the device
+ * the handle was created on. */
+int pmlp_set_stream(pmlp_t h, void* stream);
+
+/* PMLP_FP32 (default) or PMLP_BF16_GEMM. */
+int pmlp_set_precision(pmlp_t h, int32_t mode);
+
+/* Forward pass only (Section 3: input-to-hidden product, per-model
+ * activation, Modified Matrix Multiplication):
+ *   logits[b, m, o] = sum_{n in model m} act_m(sum_f X[b,f] W1[n,f]) W2[o,n]
+ * X_dev [B, F] fp32, logits_dev [B, M, O] fp32 (written).  No state
+ * changes. */
+int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev);
+
+/* One SGD step on the batch (X_dev [B, F], y_dev [B] int32 labels in
+ * [0, O)): forward, per-model mean softmax cross-entropy, back-propagation
+ * and the update W -= lr * dW for every model at once.  lr must be
+ * finite.  The per-model losses of this batch (at the pre-update weights)
+ * are kept for pmlp_losses. */
+int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev,
+                    int32_t B, float lr);
+
+/* Copy the per-model mean cross-entropy of the last pmlp_train_step or
+ * pmlp_gradients batch into out_host [M] (fp32).  Synchronises the
+ * stream.  PMLP_ESTATE before any step; PMLP_EINVAL if that batch held a
+ * label outside [0, O) (the flag is cleared by the call). */
+int pmlp_losses(pmlp_t h, float* out_host);
+
+/* Gradients of sum_m L_m on one batch without updating the weights
+ * (L_m is model m's mean cross-entropy, so each model's slice is the
+ * gradient of its own loss): dW1_dev [N, F], dW2_dev [O, N], fp32,
+ * written.  Uses the same kernels as pmlp_train_step with the update
+ * replaced by a store.  Also records the batch losses for pmlp_losses. */
+int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev,
+                   int32_t B, float* dW1_dev, float* dW2_dev);
+
+/* Hidden layer of the packed network: Z_dev [B, N] = X W1^T and
+ * H_dev [B, N] = act_{model of n}(Z) (either pointer may be null).  A
+ * view of the first two forward steps for inspection and testing. */
+int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev,
+                float* H_dev);
+
+/* Copy the parameters to / from host memory in the layout above
+ * (W1_host [N, F], W2_host [O, N], fp32).  Synchronous.  Either pointer
+ * may be null to skip that tensor. */
+int pmlp_get_params(pmlp_t h, float* W1_host, float* W2_host);
+int pmlp_set_params(pmlp_t h, const float* W1_host, const float* W2_host);
+
+/* Sizes of the packed model; any output pointer may be null. */
+int pmlp_info(pmlp_t h, int64_t* N, int32_t* M, int32_t* F, int32_t* O);
+
+/* Per-kernel timing with HIP events on the handle's stream.  While
+ * enabled, every kernel launch is bracketed by two events.
+ * pmlp_kernel_time synchronises and returns, for kernel id k (0 ..
+ * PMLP_NUM_KERNELS-1, names from pmlp_kernel_name), the summed duration
+ * in milliseconds and the number of launches since the last reset;
+ * pmlp_profile_reset clears the totals. */
+#define PMLP_NUM_KERNELS 8
+int pmlp_set_profiling(pmlp_t h, int32_t enable);
+int pmlp_kernel_time(pmlp_t h, int32_t k, double* total_ms, int64_t* launches);
+int pmlp_profile_reset(pmlp_t h);
+const char* pmlp_kernel_name(int32_t k);
+
+/* Message describing the last failure on the calling thread (a
+ * library-owned string, valid until the next failing call on it). */
+const char* pmlp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PMLP_H */

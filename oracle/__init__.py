@@ -59,6 +59,8 @@ def _load():
         lib.orc_train.restype = C.c_int
         lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32, P, P,
                                   dbl, P, P, P, P, i32, C.c_int]
+        lib.orc_hidden.restype = C.c_int
+        lib.orc_hidden.argtypes = [i32, i32, P, P, P, P, i32, P, P]
         lib.orc_dataset_loss.restype = C.c_int
         lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, i64,
                                          i32, P, C.c_int]
@@ -160,6 +162,19 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
                              _p(loss), _p(sel), 0 if sel is None else len(sel), nthreads),
            "train")
     return W1o, W2o, loss
+
+
+def hidden(hidden_sizes, act_ids, W1, X) -> Tuple[np.ndarray, np.ndarray]:
+    """Z = X W1^T and H = act(Z), both [B, N] fp64."""
+    hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
+    W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
+    B, F = Xf.shape
+    N = int(hs.sum())
+    Z = np.empty((B, N), np.float64)
+    H = np.empty((B, N), np.float64)
+    _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B, _p(Z), _p(H)),
+           "hidden")
+    return Z, H
 
 
 def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,

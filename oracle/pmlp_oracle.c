@@ -490,6 +490,32 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
   return err;
 }
 
+/* Hidden layer of the packed network (Section 3, steps 1 and 2 of the
+ * packed procedure, with each contiguous portion of the hidden layer taking
+ * its own model's activation): Z [B,N] = X W1^T and H [B,N] = act(Z),
+ * both fp64, sample-major. */
+int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
+               const double* W1, const float* X, int32_t B, double* Z, double* H) {
+  if (F < 1 || M < 1 || !hs || !acts || !W1 || !X || B < 1 || !Z || !H) return ORC_EINVAL;
+  int64_t N = 0;
+  for (int m = 0; m < M; ++m) {
+    if (hs[m] < 1 || acts[m] < 0 || acts[m] > 9) return ORC_EINVAL;
+    N += hs[m];
+  }
+  int64_t n = 0;
+  for (int m = 0; m < M; ++m) {
+    for (int j = 0; j < hs[m]; ++j, ++n) {
+      for (int b = 0; b < B; ++b) {
+        double acc = 0.0;
+        for (int f = 0; f < F; ++f) acc += (double)X[(int64_t)b * F + f] * W1[n * F + f];
+        Z[(int64_t)b * N + n] = acc;
+        H[(int64_t)b * N + n] = orc_act(acts[m], acc);
+      }
+    }
+  }
+  return ORC_OK;
+}
+
 /* Mean cross-entropy of every model over a whole sample set (no update),
  * evaluated in chunks of at most chunk samples. */
 int orc_dataset_loss(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,

@@ -1,0 +1,562 @@
+// libpmlp host side: argument checking, the packing plan, parameter and
+// workspace ownership, and step sequencing on one HIP stream.  The C ABI is
+// declared and documented in include/pmlp.h.
+
+#include "pmlp.h"
+#include "pmlp_internal.h"
+
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace pmlpk;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define PMLP_HIP(expr)                                                                    \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return fail(PMLP_EDEVICE, std::string(#expr) + " failed: " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int64_t kTile3 = 512;      // M3 forward tile width (hidden units)
+constexpr int32_t kMaxBatch = 1 << 20;
+constexpr int32_t kMaxO = 16;
+
+static_assert(KID_COUNT == PMLP_NUM_KERNELS, "kernel id table");
+
+const char* const kKernelNames[KID_COUNT] = {
+    "pack_x", "gemm_fwd", "act", "m3_fwd", "ce", "m3_bwd", "gemm_bwd", "aux"};
+
+uint64_t splitmix64_host(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+template <class T>
+void dfree(T*& p) {
+  if (p) (void)hipFree(p);
+  p = nullptr;
+}
+
+}  // namespace
+
+struct pmlp {
+  int dev = 0;
+  hipStream_t stream = nullptr;
+  int32_t F = 0, F4 = 0, O = 0, M = 0;
+  int64_t N = 0;
+  int32_t precision = PMLP_FP32;
+  std::vector<int32_t> hs, acts;
+  std::vector<int64_t> seg_off;
+
+  float* W1 = nullptr;  // [N][F4]
+  float* W2 = nullptr;  // [O][N]
+  int64_t* d_seg_off = nullptr;
+  int32_t* d_act = nullptr;
+  int32_t* d_mid = nullptr;
+  Tile3* d_tiles = nullptr;
+  int32_t ntiles = 0;
+  bool has_split = false;
+  float* loss = nullptr;   // [M]
+  int32_t* flag = nullptr; // label-range flag
+
+  int32_t capBp = 0;
+  float* Xp = nullptr;
+  float* Xt = nullptr;
+  float* Zt = nullptr;
+  float* LG = nullptr;
+  bool have_loss = false;
+
+  bool prof = false;
+  struct Pending {
+    int k;
+    hipEvent_t a, b;
+  };
+  std::vector<hipEvent_t> ev_free;
+  std::vector<Pending> pending;
+  double tot_ms[KID_COUNT] = {};
+  int64_t launches[KID_COUNT] = {};
+};
+
+namespace {
+
+void release(pmlp* h) {
+  dfree(h->W1);
+  dfree(h->W2);
+  dfree(h->d_seg_off);
+  dfree(h->d_act);
+  dfree(h->d_mid);
+  dfree(h->d_tiles);
+  dfree(h->loss);
+  dfree(h->flag);
+  dfree(h->Xp);
+  dfree(h->Xt);
+  dfree(h->Zt);
+  dfree(h->LG);
+  h->capBp = 0;
+  for (auto& p : h->pending) {
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  h->pending.clear();
+  for (auto e : h->ev_free) (void)hipEventDestroy(e);
+  h->ev_free.clear();
+}
+
+int take_event(pmlp* h, hipEvent_t* e) {
+  if (!h->ev_free.empty()) {
+    *e = h->ev_free.back();
+    h->ev_free.pop_back();
+    return PMLP_OK;
+  }
+  PMLP_HIP(hipEventCreate(e));
+  return PMLP_OK;
+}
+
+// Launch `fn` (returning hipError_t) as kernel `kid`, bracketed by events
+// when profiling is on.
+template <class Fn>
+int run(pmlp* h, int kid, Fn fn) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (h->prof) {
+    int rc = take_event(h, &a);
+    if (rc) return rc;
+    rc = take_event(h, &b);
+    if (rc) return rc;
+    PMLP_HIP(hipEventRecord(a, h->stream));
+  }
+  hipError_t e = fn();
+  if (e != hipSuccess)
+    return fail(PMLP_EDEVICE, std::string("launch of ") + kKernelNames[kid] +
+                                  " failed: " + hipGetErrorString(e));
+  if (h->prof) {
+    PMLP_HIP(hipEventRecord(b, h->stream));
+    h->pending.push_back({kid, a, b});
+  }
+  return PMLP_OK;
+}
+
+int use_device(pmlp* h) {
+  int cur = -1;
+  PMLP_HIP(hipGetDevice(&cur));
+  if (cur != h->dev) PMLP_HIP(hipSetDevice(h->dev));
+  return PMLP_OK;
+}
+
+int ensure_workspace(pmlp* h, int32_t Bp) {
+  if (Bp <= h->capBp) return PMLP_OK;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  dfree(h->Xp);
+  dfree(h->Xt);
+  dfree(h->Zt);
+  dfree(h->LG);
+  h->capBp = 0;
+  const size_t nx = (size_t)Bp * h->F4 * sizeof(float);
+  const size_t nz = (size_t)h->N * Bp * sizeof(float);
+  const size_t nl = (size_t)h->M * Bp * h->O * sizeof(float);
+  if (hipMalloc(&h->Xp, nx) != hipSuccess || hipMalloc(&h->Xt, nx) != hipSuccess ||
+      hipMalloc(&h->Zt, nz) != hipSuccess || hipMalloc(&h->LG, nl) != hipSuccess) {
+    (void)hipGetLastError();
+    dfree(h->Xp);
+    dfree(h->Xt);
+    dfree(h->Zt);
+    dfree(h->LG);
+    return fail(PMLP_ENOMEM, "workspace allocation failed for batch " + std::to_string(Bp) +
+                                 " (" + std::to_string((nz + 2 * nx + nl) >> 20) + " MiB)");
+  }
+  h->capBp = Bp;
+  return PMLP_OK;
+}
+
+int check_handle(pmlp* h) {
+  if (!h) return fail(PMLP_EINVAL, "null handle");
+  return PMLP_OK;
+}
+
+int check_batch(pmlp* h, const void* X, int32_t B) {
+  if (int rc = check_handle(h)) return rc;
+  if (!X) return fail(PMLP_EINVAL, "null X");
+  if (B < 1 || B > kMaxBatch) return fail(PMLP_EINVAL, "batch size out of range [1, 2^20]");
+  return PMLP_OK;
+}
+
+int32_t pad_batch(int32_t B) { return (B + 15) & ~15; }
+
+// Batch copy and the input-to-hidden product (Section 3, step 1).
+int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
+  if (int rc = run(h, KID_PACK_X, [&] {
+        return launch_pack_x(X, B, h->F, Bp, h->F4, h->Xp, h->Xt, h->stream);
+      }))
+    return rc;
+  GemmArgs g{};
+  g.P = h->W1;
+  g.ldp = h->F4;
+  g.NP = h->N;
+  g.Q = h->Xp;
+  g.ldq = h->F4;
+  g.NQ = Bp;
+  g.K = h->F4;
+  g.out = h->Zt;
+  g.ldo = Bp;
+  g.ncols = Bp;
+  g.lr = 0.f;
+  g.bf16 = h->precision == PMLP_BF16_GEMM;
+  return run(h, KID_GEMM_FWD, [&] { return launch_gemm(g, EPI_STORE, h->stream); });
+}
+
+// Full step: forward, loss, backward and either the SGD update (dW1 and
+// dW2 null) or gradient stores.
+int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* dW1,
+         float* dW2) {
+  const int32_t Bp = pad_batch(B);
+  if (int rc = use_device(h)) return rc;
+  if (int rc = ensure_workspace(h, Bp)) return rc;
+  if (int rc = forward_hidden(h, X, B, Bp)) return rc;
+  if (h->has_split) {
+    if (int rc = run(h, KID_AUX, [&] {
+          return launch_fill(h->LG, (int64_t)h->M * Bp * h->O, 0.f, h->stream);
+        }))
+      return rc;
+  }
+  if (int rc = run(h, KID_M3_FWD, [&] {
+        return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->N, h->O, h->d_seg_off, h->d_act,
+                             h->d_tiles, h->ntiles, h->LG, (int64_t)Bp * h->O, h->O,
+                             h->stream);
+      }))
+    return rc;
+  if (int rc = run(h, KID_CE, [&] {
+        return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, h->stream);
+      }))
+    return rc;
+  if (int rc = run(h, KID_M3_BWD, [&] {
+        return launch_m3_bwd(h->Zt, Bp, h->W2, h->N, h->O, h->d_mid, h->d_act, h->LG, lr, dW2,
+                             h->stream);
+      }))
+    return rc;
+  GemmArgs g{};
+  g.P = h->Zt;
+  g.ldp = Bp;
+  g.NP = h->N;
+  g.Q = h->Xt;
+  g.ldq = Bp;
+  g.NQ = h->F4;
+  g.K = Bp;
+  g.out = dW1 ? dW1 : h->W1;
+  g.ldo = dW1 ? h->F : h->F4;
+  g.ncols = h->F;
+  g.lr = lr;
+  g.bf16 = h->precision == PMLP_BF16_GEMM;
+  if (int rc = run(h, KID_GEMM_BWD, [&] {
+        return launch_gemm(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
+      }))
+    return rc;
+  h->have_loss = true;
+  return PMLP_OK;
+}
+
+// Tiles of the M3 forward: runs of whole segments up to kTile3 units wide;
+// a wider segment becomes pieces of kTile3 units added with atomics.
+void build_tiles(const std::vector<int32_t>& hs, std::vector<Tile3>& tiles, bool& has_split) {
+  tiles.clear();
+  has_split = false;
+  Tile3 cur{0, 0, 0, 0, 0};
+  int64_t n = 0;
+  for (size_t m = 0; m < hs.size(); ++m) {
+    const int64_t w = hs[m];
+    if (w > kTile3) {
+      if (cur.len > 0) tiles.push_back(cur);
+      cur.len = 0;
+      for (int64_t s = 0; s < w; s += kTile3) {
+        const int64_t len = w - s < kTile3 ? w - s : kTile3;
+        tiles.push_back(Tile3{n + s, (int32_t)len, (int32_t)m, 1, 0});
+      }
+      has_split = true;
+    } else {
+      if (cur.len > 0 && cur.len + w > kTile3) {
+        tiles.push_back(cur);
+        cur.len = 0;
+      }
+      if (cur.len == 0) cur = Tile3{n, 0, (int32_t)m, 0, 0};
+      cur.len += (int32_t)w;
+    }
+    n += w;
+  }
+  if (cur.len > 0) tiles.push_back(cur);
+}
+
+}  // namespace
+
+extern "C" {
+
+int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes,
+                const int32_t* act_ids, uint64_t seed) {
+  if (!out) return fail(PMLP_EINVAL, "null output handle pointer");
+  *out = nullptr;
+  if (F < 1) return fail(PMLP_EINVAL, "F must be >= 1");
+  if (O < 2 || O > kMaxO) return fail(PMLP_EINVAL, "O must be in [2, 16]");
+  if (M < 1) return fail(PMLP_EINVAL, "M must be >= 1");
+  if (!hidden_sizes || !act_ids) return fail(PMLP_EINVAL, "null hidden_sizes or act_ids");
+  int64_t N = 0;
+  for (int32_t m = 0; m < M; ++m) {
+    if (hidden_sizes[m] < 1) return fail(PMLP_EINVAL, "hidden size < 1 at model " + std::to_string(m));
+    if (act_ids[m] < 0 || act_ids[m] >= PMLP_NUM_ACTS)
+      return fail(PMLP_EINVAL, "activation id out of range at model " + std::to_string(m));
+    N += hidden_sizes[m];
+  }
+  if (N > ((int64_t)1 << 31) - 1) return fail(PMLP_EINVAL, "total hidden units exceed 2^31-1");
+  const int32_t F4 = (F + 3) & ~3;
+
+  pmlp* h = new (std::nothrow) pmlp();
+  if (!h) return fail(PMLP_ENOMEM, "host allocation failed");
+  h->F = F;
+  h->F4 = F4;
+  h->O = O;
+  h->M = M;
+  h->N = N;
+  h->hs.assign(hidden_sizes, hidden_sizes + M);
+  h->acts.assign(act_ids, act_ids + M);
+  h->seg_off.resize((size_t)M + 1);
+  h->seg_off[0] = 0;
+  for (int32_t m = 0; m < M; ++m) h->seg_off[m + 1] = h->seg_off[m] + hidden_sizes[m];
+  std::vector<int32_t> mid((size_t)N);
+  for (int32_t m = 0; m < M; ++m)
+    for (int64_t n = h->seg_off[m]; n < h->seg_off[m + 1]; ++n) mid[n] = m;
+  std::vector<Tile3> tiles;
+  build_tiles(h->hs, tiles, h->has_split);
+  h->ntiles = (int32_t)tiles.size();
+  std::vector<float> bound2((size_t)M);
+  for (int32_t m = 0; m < M; ++m) bound2[m] = (float)(1.0 / std::sqrt((double)hidden_sizes[m]));
+  const float bound1 = (float)(1.0 / std::sqrt((double)F));
+
+  auto bail = [&](int rc) {
+    release(h);
+    delete h;
+    return rc;
+  };
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(fail(PMLP_EDEVICE, "no HIP device available"));
+  }
+  h->dev = dev;
+  float* d_bound2 = nullptr;
+  if (hipMalloc(&h->W1, (size_t)N * F4 * sizeof(float)) != hipSuccess ||
+      hipMalloc(&h->W2, (size_t)O * N * sizeof(float)) != hipSuccess ||
+      hipMalloc(&h->d_seg_off, ((size_t)M + 1) * sizeof(int64_t)) != hipSuccess ||
+      hipMalloc(&h->d_act, (size_t)M * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&h->d_mid, (size_t)N * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&h->d_tiles, tiles.size() * sizeof(Tile3)) != hipSuccess ||
+      hipMalloc(&h->loss, (size_t)M * sizeof(float)) != hipSuccess ||
+      hipMalloc(&h->flag, sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&d_bound2, (size_t)M * sizeof(float)) != hipSuccess) {
+    (void)hipGetLastError();
+    dfree(d_bound2);
+    return bail(fail(PMLP_ENOMEM, "device allocation failed for the packed parameters"));
+  }
+  auto setup = [&]() -> int {
+    PMLP_HIP(hipMemcpy(h->d_seg_off, h->seg_off.data(), ((size_t)M + 1) * sizeof(int64_t),
+                       hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(h->d_act, act_ids, (size_t)M * sizeof(int32_t), hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(h->d_mid, mid.data(), (size_t)N * sizeof(int32_t), hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(h->d_tiles, tiles.data(), tiles.size() * sizeof(Tile3),
+                       hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(d_bound2, bound2.data(), (size_t)M * sizeof(float), hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemset(h->flag, 0, sizeof(int32_t)));
+    PMLP_HIP(launch_init_params(h->W1, N, F, F4, bound1, h->W2, O, h->d_mid, d_bound2,
+                                splitmix64_host(seed), nullptr));
+    PMLP_HIP(hipStreamSynchronize(nullptr));
+    return PMLP_OK;
+  };
+  int rc = setup();
+  dfree(d_bound2);
+  if (rc) return bail(rc);
+  *out = h;
+  return PMLP_OK;
+}
+
+int pmlp_destroy(pmlp_t h) {
+  if (!h) return PMLP_OK;
+  (void)hipSetDevice(h->dev);
+  (void)hipStreamSynchronize(h->stream);
+  release(h);
+  delete h;
+  return PMLP_OK;
+}
+
+int pmlp_set_stream(pmlp_t h, void* stream) {
+  if (int rc = check_handle(h)) return rc;
+  h->stream = (hipStream_t)stream;
+  return PMLP_OK;
+}
+
+int pmlp_set_precision(pmlp_t h, int32_t mode) {
+  if (int rc = check_handle(h)) return rc;
+  if (mode != PMLP_FP32 && mode != PMLP_BF16_GEMM) return fail(PMLP_EINVAL, "unknown precision mode");
+  if (mode == PMLP_BF16_GEMM) return fail(PMLP_EINVAL, "the bf16 GEMM variant is not available in this build");
+  h->precision = mode;
+  return PMLP_OK;
+}
+
+int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!logits_dev) return fail(PMLP_EINVAL, "null logits");
+  const int32_t Bp = pad_batch(B);
+  if (int rc = use_device(h)) return rc;
+  if (int rc = ensure_workspace(h, Bp)) return rc;
+  if (int rc = forward_hidden(h, X_dev, B, Bp)) return rc;
+  if (h->has_split) {
+    if (int rc = run(h, KID_AUX, [&] {
+          return launch_fill(logits_dev, (int64_t)B * h->M * h->O, 0.f, h->stream);
+        }))
+      return rc;
+  }
+  return run(h, KID_M3_FWD, [&] {
+    return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->N, h->O, h->d_seg_off, h->d_act, h->d_tiles,
+                         h->ntiles, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
+  });
+}
+
+int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B, float lr) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!y_dev) return fail(PMLP_EINVAL, "null labels");
+  if (!std::isfinite(lr)) return fail(PMLP_EINVAL, "learning rate is not finite");
+  return step(h, X_dev, y_dev, B, lr, nullptr, nullptr);
+}
+
+int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
+                   float* dW1_dev, float* dW2_dev) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null labels or gradient buffer");
+  return step(h, X_dev, y_dev, B, 0.f, dW1_dev, dW2_dev);
+}
+
+int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev, float* H_dev) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  const int32_t Bp = pad_batch(B);
+  if (int rc = use_device(h)) return rc;
+  if (int rc = ensure_workspace(h, Bp)) return rc;
+  if (int rc = forward_hidden(h, X_dev, B, Bp)) return rc;
+  if (!Z_dev && !H_dev) return PMLP_OK;
+  return run(h, KID_ACT, [&] {
+    return launch_hidden_out(h->Zt, Bp, B, h->N, h->d_mid, h->d_act, Z_dev, H_dev, h->stream);
+  });
+}
+
+int pmlp_losses(pmlp_t h, float* out_host) {
+  if (int rc = check_handle(h)) return rc;
+  if (!out_host) return fail(PMLP_EINVAL, "null output");
+  if (!h->have_loss) return fail(PMLP_ESTATE, "no training step has run yet");
+  if (int rc = use_device(h)) return rc;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  PMLP_HIP(hipMemcpy(out_host, h->loss, (size_t)h->M * sizeof(float), hipMemcpyDeviceToHost));
+  int32_t flag = 0;
+  PMLP_HIP(hipMemcpy(&flag, h->flag, sizeof(int32_t), hipMemcpyDeviceToHost));
+  if (flag) {
+    PMLP_HIP(hipMemset(h->flag, 0, sizeof(int32_t)));
+    return fail(PMLP_EINVAL, "a label outside [0, O) was seen since the last pmlp_losses call");
+  }
+  return PMLP_OK;
+}
+
+int pmlp_get_params(pmlp_t h, float* W1_host, float* W2_host) {
+  if (int rc = check_handle(h)) return rc;
+  if (int rc = use_device(h)) return rc;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  if (W1_host)
+    PMLP_HIP(hipMemcpy2D(W1_host, (size_t)h->F * sizeof(float), h->W1,
+                         (size_t)h->F4 * sizeof(float), (size_t)h->F * sizeof(float),
+                         (size_t)h->N, hipMemcpyDeviceToHost));
+  if (W2_host)
+    PMLP_HIP(hipMemcpy(W2_host, h->W2, (size_t)h->O * h->N * sizeof(float),
+                       hipMemcpyDeviceToHost));
+  return PMLP_OK;
+}
+
+int pmlp_set_params(pmlp_t h, const float* W1_host, const float* W2_host) {
+  if (int rc = check_handle(h)) return rc;
+  if (int rc = use_device(h)) return rc;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  if (W1_host)
+    PMLP_HIP(hipMemcpy2D(h->W1, (size_t)h->F4 * sizeof(float), W1_host,
+                         (size_t)h->F * sizeof(float), (size_t)h->F * sizeof(float),
+                         (size_t)h->N, hipMemcpyHostToDevice));
+  if (W2_host)
+    PMLP_HIP(hipMemcpy(h->W2, W2_host, (size_t)h->O * h->N * sizeof(float),
+                       hipMemcpyHostToDevice));
+  return PMLP_OK;
+}
+
+int pmlp_info(pmlp_t h, int64_t* N, int32_t* M, int32_t* F, int32_t* O) {
+  if (int rc = check_handle(h)) return rc;
+  if (N) *N = h->N;
+  if (M) *M = h->M;
+  if (F) *F = h->F;
+  if (O) *O = h->O;
+  return PMLP_OK;
+}
+
+int pmlp_set_profiling(pmlp_t h, int32_t enable) {
+  if (int rc = check_handle(h)) return rc;
+  h->prof = enable != 0;
+  return PMLP_OK;
+}
+
+int pmlp_kernel_time(pmlp_t h, int32_t k, double* total_ms, int64_t* launches) {
+  if (int rc = check_handle(h)) return rc;
+  if (k < 0 || k >= KID_COUNT) return fail(PMLP_EINVAL, "kernel id out of range");
+  if (!h->pending.empty()) {
+    if (int rc = use_device(h)) return rc;
+    PMLP_HIP(hipStreamSynchronize(h->stream));
+    for (auto& p : h->pending) {
+      float ms = 0.f;
+      PMLP_HIP(hipEventElapsedTime(&ms, p.a, p.b));
+      h->tot_ms[p.k] += ms;
+      h->launches[p.k] += 1;
+      h->ev_free.push_back(p.a);
+      h->ev_free.push_back(p.b);
+    }
+    h->pending.clear();
+  }
+  if (total_ms) *total_ms = h->tot_ms[k];
+  if (launches) *launches = h->launches[k];
+  return PMLP_OK;
+}
+
+int pmlp_profile_reset(pmlp_t h) {
+  if (int rc = check_handle(h)) return rc;
+  if (!h->pending.empty()) {
+    if (int rc = use_device(h)) return rc;
+    PMLP_HIP(hipStreamSynchronize(h->stream));
+    for (auto& p : h->pending) {
+      h->ev_free.push_back(p.a);
+      h->ev_free.push_back(p.b);
+    }
+    h->pending.clear();
+  }
+  for (int k = 0; k < KID_COUNT; ++k) {
+    h->tot_ms[k] = 0.0;
+    h->launches[k] = 0;
+  }
+  return PMLP_OK;
+}
+
+const char* pmlp_kernel_name(int32_t k) {
+  if (k < 0 || k >= KID_COUNT) return "";
+  return kKernelNames[k];
+}
+
+const char* pmlp_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

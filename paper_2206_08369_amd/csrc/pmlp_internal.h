@@ -1,0 +1,84 @@
+// Internal declarations shared by the host library and the kernel launchers.
+// Not part of the public C ABI (include/pmlp.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pmlpk {
+
+// One unit of work of the M3 forward kernel: either a run of whole
+// segments (models) whose total width is at most the tile limit, or one
+// piece of a segment wider than that limit.  Pieces are summed into the
+// logits with atomics; whole segments are written with plain stores.
+struct Tile3 {
+  int64_t n0;      // first hidden unit
+  int32_t len;     // number of hidden units
+  int32_t m0;      // model owning hidden unit n0
+  int32_t atomic;  // 1: a piece of a split segment
+  int32_t reserved;
+};
+static_assert(sizeof(Tile3) == 24, "Tile3 layout");
+
+enum KernelId {
+  KID_PACK_X = 0,
+  KID_GEMM_FWD = 1,
+  KID_ACT = 2,
+  KID_M3_FWD = 3,
+  KID_CE = 4,
+  KID_M3_BWD = 5,
+  KID_GEMM_BWD = 6,
+  KID_AUX = 7,
+  KID_COUNT = 8
+};
+
+// GEMM epilogues: C[p][q] = sum_k P[p][k] Q[q][k]
+enum GemmEpi {
+  EPI_STORE = 0,  // out[p*ldo + q] = C        (float4 over q)
+  EPI_SGD = 1,    // out[p*ldo + q] -= lr * C  (float4 over q)
+  EPI_GRAD = 2    // out[p*ldo + q] = C for q < ncols (scalar stores)
+};
+
+struct GemmArgs {
+  const float* P;  // big operand [NP][K], row stride ldp
+  int64_t ldp;
+  int64_t NP;
+  const float* Q;  // small operand [NQ][K], row stride ldq
+  int64_t ldq;
+  int32_t NQ;      // multiple of 4
+  int32_t K;       // multiple of 4
+  float* out;
+  int64_t ldo;
+  int32_t ncols;   // EPI_GRAD: number of valid q columns
+  float lr;
+  int32_t bf16;    // round both operands to bf16 before the products
+};
+
+hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
+
+hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float bound1,
+                              float* W2, int32_t O, const int32_t* mid, const float* bound2,
+                              uint64_t key, hipStream_t s);
+
+hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
+                         float* Xp, float* Xt, hipStream_t s);
+
+hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t N,
+                         int32_t O, const int64_t* seg_off, const int32_t* act,
+                         const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
+                         int64_t sb, hipStream_t s);
+
+hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
+                     float* loss, int32_t* flag, hipStream_t s);
+
+hipError_t launch_m3_bwd(float* Zt, int32_t Bp, float* W2, int64_t N, int32_t O,
+                         const int32_t* mid, const int32_t* act, const float* G, float lr,
+                         float* dW2, hipStream_t s);
+
+hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
+                             const int32_t* mid, const int32_t* act, float* Z, float* H,
+                             hipStream_t s);
+
+hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
+
+}  // namespace pmlpk

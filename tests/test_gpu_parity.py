@@ -1,0 +1,360 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 CPU oracle.
+
+Every test is marked `gpu`.  Tolerances (per-model normwise, see
+tests/parity.py): 1e-5 for one forward/backward step in fp32, 1e-3 for
+per-model losses after one epoch.  Inputs are seeded and synthetic
+(pmlp_workloads); nothing here is produced by the HIP path and then
+reused as an expected value.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import pmlp_workloads as wl
+from conftest import load_golden
+from parity import (cross_entropy, err_cols, err_logits, err_losses, err_rows, offsets,
+                    submodel)
+
+pytestmark = pytest.mark.gpu
+
+TOL_STEP = 1e-5
+TOL_EPOCH = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    torch.cuda.set_device(0)
+    return torch
+
+
+@pytest.fixture(scope="module")
+def pm(torch):
+    import paper_2206_08369_amd as pm
+    pm.load_library()
+    return pm
+
+
+def dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def make_net(pm, F, O, hs, acts, seed=0, W1=None, W2=None):
+    net = pm.PackedMLP(F, O, hs, acts, seed=seed)
+    if W1 is not None or W2 is not None:
+        net.set_params(W1, W2)
+    return net
+
+
+# Shapes spanning the kernels' tiling: B = 1 and ragged batches, a batch
+# wider than 256 (two passes in the backward kernel) and wider than 1024,
+# F not a multiple of 4 or 16, O up to 16, widths 1 and segments wider than
+# the M3 tile (split into two and three pieces).
+CASES = {
+    "tiny_b1": dict(hs=[1, 2, 3, 1], F=3, O=2, B=1),
+    "ragged": dict(M=37, hmax=40, F=13, O=3, B=7),
+    "tile_spanning": dict(hs=[1300, 513, 512, 1, 700, 3, 1024], F=10, O=2, B=33),
+    "o10_b32": dict(M=20, hmax=30, F=32, O=10, B=32),
+    "o16": dict(M=10, hmax=20, F=5, O=16, B=48),
+    "b300_f100": dict(M=12, hmax=50, F=100, O=2, B=300),
+    "f1": dict(M=8, hmax=9, F=1, O=2, B=17),
+    "b1100": dict(M=6, hmax=20, F=20, O=2, B=1100),
+    "all_width_one": dict(hs=[1] * 70, F=7, O=4, B=20),
+}
+
+
+def case_inputs(name, seed=0):
+    c = CASES[name]
+    rng = np.random.default_rng(zlib.crc32(name.encode()) + seed)
+    if "hs" in c:
+        hs = np.asarray(c["hs"], np.int32)
+        acts = rng.integers(0, 10, len(hs)).astype(np.int32)
+    else:
+        hs, acts = wl.random_models(rng, c["M"], c["hmax"])
+    X, y = wl.make_dataset(c["F"], c["O"], c["B"], seed=int(rng.integers(1 << 30)))
+    return hs, acts, c["F"], c["O"], c["B"], X, y
+
+
+# --------------------------------------------------------------------------
+# Initialisation and the paper's worked examples
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("F,O,hs,seed", [
+    (10, 2, None, 3000),           # the 60-model grid (h = 1..10 x 6 activations)
+    (13, 3, [5, 1, 700, 2], 99),
+    (1, 16, [1, 1, 1], 7),
+])
+def test_init_is_bit_exact(pm, orc, F, O, hs, seed):
+    if hs is None:
+        hs, acts = wl.WORKLOADS["w60_f10"].model_grid()
+    else:
+        hs = np.asarray(hs, np.int32)
+        acts = np.zeros(len(hs), np.int32)
+    net = make_net(pm, F, O, hs, acts, seed=seed)
+    W1, W2 = net.get_params()
+    R1, R2 = orc.init_params(F, O, hs, seed)
+    assert np.array_equal(W1, R1) and np.array_equal(W2, R2)
+    net.close()
+
+
+@pytest.mark.parametrize("O", [2, 3])
+def test_scatter_add_worked_example(pm, torch, O):
+    """Section 3 Scatter Add example: [1..6] keyed by [0,1,1,2,2,2] gives
+    [1, 5, 15]; reproduced with W1 = I, identity activation and W2 = 1."""
+    g = load_golden("scatter_example.json")
+    S = np.asarray(g["S"], np.float32)
+    hs = np.bincount(np.asarray(g["I"][0])).astype(np.int32)
+    F = S.shape[1]
+    net = make_net(pm, F, O, hs, np.zeros(len(hs), np.int32),
+                   W1=np.eye(F, dtype=np.float32), W2=np.ones((O, F), np.float32))
+    out = net.forward(dev(torch, S)).cpu().numpy()
+    for o in range(O):
+        assert np.array_equal(out[0, :, o], np.asarray(g["R"][0], np.float32))
+    net.close()
+
+
+def test_packing_example_4_3_4(pm, orc, torch):
+    """Section 3 / Figure 2: a 4-1-2 and a 4-2-2 MLP packed as 4-3-4."""
+    g = load_golden("packing_example.json")
+    hs = np.asarray(g["hidden_sizes"], np.int32)
+    rng = np.random.default_rng(7)
+    X = rng.standard_normal((5, g["F"])).astype(np.float32)
+    W1 = rng.uniform(-1, 1, (3, g["F"])).astype(np.float32)
+    W2 = rng.uniform(-1, 1, (g["O"], 3)).astype(np.float32)
+    for act in range(10):
+        acts = np.full(2, act, np.int32)
+        net = make_net(pm, g["F"], g["O"], hs, acts, W1=W1, W2=W2)
+        got = net.forward(dev(torch, X)).cpu().numpy()
+        want = orc.forward(hs, acts, W1, W2, X)
+        assert err_logits(got, want).max() <= TOL_STEP, act
+        net.close()
+
+
+# --------------------------------------------------------------------------
+# One step, element by element, on shapes spanning the tiling
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_hidden_layer(pm, orc, torch, name):
+    hs, acts, F, O, B, X, y = case_inputs(name)
+    net = make_net(pm, F, O, hs, acts, seed=11)
+    W1, W2 = net.get_params()
+    Z, H = net.hidden(dev(torch, X))
+    RZ, RH = orc.hidden(hs, acts, W1, X)
+    assert err_cols(Z.cpu().numpy(), RZ, hs).max() <= TOL_STEP
+    assert err_cols(H.cpu().numpy(), RH, hs).max() <= TOL_STEP
+    net.close()
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_forward_logits(pm, orc, torch, name):
+    hs, acts, F, O, B, X, y = case_inputs(name)
+    net = make_net(pm, F, O, hs, acts, seed=12)
+    W1, W2 = net.get_params()
+    got = net.forward(dev(torch, X)).cpu().numpy()
+    want = orc.forward(hs, acts, W1, W2, X)
+    assert got.shape == (B, len(hs), O)
+    assert err_logits(got, want).max() <= TOL_STEP
+    net.close()
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_gradients_and_losses(pm, orc, torch, name):
+    hs, acts, F, O, B, X, y = case_inputs(name)
+    net = make_net(pm, F, O, hs, acts, seed=13)
+    W1, W2 = net.get_params()
+    dW1, dW2 = net.gradients(dev(torch, X), dev(torch, y))
+    loss = net.losses()
+    r1, r2, rl, allow = orc.gradients(hs, acts, W1, W2, X, y)
+    assert err_rows(dW1.cpu().numpy(), r1, hs, allow).max() <= TOL_STEP
+    assert err_cols(dW2.cpu().numpy(), r2, hs).max() <= TOL_STEP
+    assert err_losses(loss, rl).max() <= TOL_STEP
+    net.close()
+
+
+@pytest.mark.parametrize("name", ["ragged", "tile_spanning", "o10_b32", "b300_f100"])
+def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name):
+    """The fused update equals W - lr * dW with dW from the gradient mode
+    (to fp32 rounding of W), and the step's losses match the oracle."""
+    hs, acts, F, O, B, X, y = case_inputs(name)
+    lr = 0.05
+    net = make_net(pm, F, O, hs, acts, seed=14)
+    W1, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    dW1, dW2 = net.gradients(Xd, yd)
+    dW1, dW2 = dW1.cpu().numpy(), dW2.cpu().numpy()
+    net.train_step(Xd, yd, lr)
+    loss = net.losses()
+    T1, T2 = net.get_params()
+    ulp1 = np.spacing(np.maximum(np.abs(W1), np.abs(T1))) * 2
+    ulp2 = np.spacing(np.maximum(np.abs(W2), np.abs(T2))) * 2
+    assert np.all(np.abs(T1 - (W1 - lr * dW1)) <= ulp1)
+    assert np.all(np.abs(T2 - (W2 - lr * dW2)) <= ulp2)
+    O1, O2, ol = orc.train(hs, acts, W1, W2, X, y, [(0, B)], lr)
+    assert err_losses(loss, ol).max() <= TOL_STEP
+    assert err_rows(T1, O1, hs).max() <= TOL_STEP
+    assert err_cols(T2, O2, hs).max() <= TOL_STEP
+    net.close()
+
+
+# --------------------------------------------------------------------------
+# Gradient isolation (Section 3) on the GPU
+# --------------------------------------------------------------------------
+
+def test_perturbing_one_model_leaves_the_others_bitwise(pm, torch):
+    rng = np.random.default_rng(5)
+    hs, acts = wl.random_models(rng, 40, 900)
+    F, O, B = 9, 3, 40
+    X, y = wl.make_dataset(F, O, B, seed=8)
+    net = make_net(pm, F, O, hs, acts, seed=15)
+    W1, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    la = net.forward(Xd).cpu().numpy()
+    ga = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+    lossa = net.losses()
+    off = offsets(hs)
+    j = 17
+    P1, P2 = W1.copy(), W2.copy()
+    P1[off[j]:off[j + 1]] += 0.25
+    P2[:, off[j]:off[j + 1]] -= 0.5
+    net.set_params(P1, P2)
+    lb = net.forward(Xd).cpu().numpy()
+    gb = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+    lossb = net.losses()
+    keep = np.ones(len(hs), bool)
+    keep[j] = False
+    rows = np.repeat(keep, hs)
+    assert np.array_equal(la[:, keep], lb[:, keep])
+    assert np.array_equal(lossa[keep], lossb[keep])
+    assert np.array_equal(ga[0][rows], gb[0][rows])
+    assert np.array_equal(ga[1][:, rows], gb[1][:, rows])
+    assert not np.array_equal(la[:, j], lb[:, j])
+    net.close()
+
+
+def test_packed_model_equals_model_alone(pm, torch):
+    rng = np.random.default_rng(6)
+    hs, acts = wl.random_models(rng, 30, 1000)
+    F, O, B = 20, 2, 64
+    X, y = wl.make_dataset(F, O, B, seed=9)
+    net = make_net(pm, F, O, hs, acts, seed=16)
+    W1, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    logits = net.forward(Xd).cpu().numpy()
+    g1, g2 = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+    off = offsets(hs)
+    for m in (0, 7, 29):
+        s = slice(off[m], off[m + 1])
+        one = make_net(pm, F, O, hs[m:m + 1], acts[m:m + 1], W1=W1[s], W2=W2[:, s])
+        lo = one.forward(Xd).cpu().numpy()
+        a1, a2 = [t.cpu().numpy() for t in one.gradients(Xd, yd)]
+        assert err_logits(lo, logits[:, m:m + 1]).max() <= 1e-6
+        assert err_rows(a1, g1[s], hs[m:m + 1]).max() <= 1e-6
+        assert err_cols(a2, g2[:, s], hs[m:m + 1]).max() <= 1e-6
+        one.close()
+    net.close()
+
+
+# --------------------------------------------------------------------------
+# Whole epochs (per-model losses within 1e-3 after one epoch)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wname", ["w60_f10", "w1k_f50"])
+def test_one_epoch(pm, orc, torch, wname):
+    w = wl.WORKLOADS[wname]
+    hs, acts = w.model_grid()
+    X, y = wl.workload_dataset(w)
+    net = make_net(pm, w.F, w.O, hs, acts, seed=w.init_seed)
+    W1, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    batches = w.batches()
+    for s, n in batches:
+        net.train_step(Xd[s:s + n], yd[s:s + n], w.lr)
+    last = net.losses()
+    T1, T2 = net.get_params()
+    R1, R2, rl = orc.train(hs, acts, W1, W2, X, y, batches, w.lr)
+    assert err_losses(last, rl).max() <= TOL_EPOCH
+    # full-train-set loss with the post-epoch weights: GPU forward + fp64 CE
+    logits = np.concatenate([net.forward(Xd[s:s + 1024]).cpu().numpy()
+                             for s in range(0, w.S, 1024)])
+    got = cross_entropy(logits, y)
+    want = orc.dataset_loss(hs, acts, R1, R2, X, y)
+    assert err_losses(got, want).max() <= TOL_EPOCH
+    assert err_rows(T1, R1, hs).max() <= TOL_EPOCH
+    net.close()
+
+
+# --------------------------------------------------------------------------
+# Full-size 10,000-model workloads: one step in the launch configuration the
+# benchmark times, checked on a strided sample of models (exact, since the
+# models are independent).
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wname", ["w10k_f100", "w10k_f32_o10", "w10k_f1000"])
+def test_full_size_step_on_sampled_models(pm, orc, torch, wname):
+    w = wl.WORKLOADS[wname]
+    hs, acts = w.model_grid()
+    X, y = wl.make_dataset(w.F, w.O, w.B, w.data_seed)
+    net = make_net(pm, w.F, w.O, hs, acts, seed=w.init_seed)
+    W1, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    dW1, dW2 = net.gradients(Xd, yd)
+    loss = net.losses()
+    models = np.arange(7, w.M, w.M // 12)
+    models = np.unique(np.concatenate([models, [0, 999, w.M - 1]]))
+    shs, sacts, sW1, sW2, rows = submodel(hs, acts, W1, W2, models)
+    rows_t = torch.from_numpy(rows).cuda()
+    g1 = dW1.index_select(0, rows_t).cpu().numpy()
+    g2 = dW2.index_select(1, rows_t).cpu().numpy()
+    del dW1, dW2
+    r1, r2, rl, allow = orc.gradients(shs, sacts, sW1, sW2, X, y)
+    assert err_rows(g1, r1, shs, allow).max() <= TOL_STEP
+    assert err_cols(g2, r2, shs).max() <= TOL_STEP
+    assert err_losses(loss[models], rl).max() <= TOL_STEP
+    # the fused update path on the same batch
+    net.train_step(Xd, yd, w.lr)
+    assert err_losses(net.losses()[models], rl).max() <= TOL_STEP
+    T1, T2 = net.get_params()
+    O1, O2, _ = orc.train(shs, sacts, sW1, sW2, X, y, [(0, w.B)], w.lr)
+    assert err_rows(T1[rows], O1, shs).max() <= TOL_STEP
+    assert err_cols(T2[:, rows], O2, shs).max() <= TOL_STEP
+    net.close()
+
+
+# --------------------------------------------------------------------------
+# Error paths
+# --------------------------------------------------------------------------
+
+def test_losses_before_any_step_is_a_state_error(pm):
+    net = make_net(pm, 3, 2, [2, 3], [0, 1])
+    with pytest.raises(pm.PmlpError) as e:
+        net.losses()
+    assert e.value.code == pm.PMLP_ESTATE
+    net.close()
+
+
+def test_label_out_of_range_is_reported(pm, torch):
+    net = make_net(pm, 3, 2, [2, 3], [0, 1])
+    X = dev(torch, np.ones((4, 3), np.float32))
+    net.train_step(X, dev(torch, np.array([0, 1, 2, 0], np.int32)), 0.1)
+    with pytest.raises(pm.PmlpError) as e:
+        net.losses()
+    assert e.value.code == pm.PMLP_EINVAL
+    net.train_step(X, dev(torch, np.array([0, 1, 1, 0], np.int32)), 0.1)
+    assert np.all(np.isfinite(net.losses()))
+    net.close()
+
+
+def test_bad_batch_arguments(pm, torch):
+    net = make_net(pm, 3, 2, [2, 3], [0, 1])
+    X = dev(torch, np.ones((4, 3), np.float32))
+    y = dev(torch, np.zeros(4, np.int32))
+    for B in (0, -1, (1 << 20) + 1):
+        with pytest.raises(pm.PmlpError) as e:
+            pm.pmlp_train_step(net.handle, X, y, B, 0.1)
+        assert e.value.code == pm.PMLP_EINVAL
+    with pytest.raises(pm.PmlpError):
+        pm.pmlp_train_step(net.handle, X, y, 4, float("nan"))
+    net.close()

@@ -405,3 +405,19 @@ def test_workload_shapes():
     assert X.dtype == np.float32 and y.dtype == np.int32
     assert np.array_equal(X, X2) and np.array_equal(y, y2)
     assert set(np.unique(y)) <= {0, 1, 2}
+
+
+def test_hidden_layer_is_matmul_then_activation(orc):
+    """Steps 1-2 of the packed procedure: Z is one plain matrix product over
+    all concatenated hidden units; H applies each portion's activation."""
+    rng = np.random.default_rng(21)
+    hs, acts = wl.random_models(rng, 15, 7)
+    N, F, B = int(hs.sum()), 6, 5
+    X = rng.standard_normal((B, F)).astype(np.float32)
+    W1 = rng.standard_normal((N, F))
+    Z, H = orc.hidden(hs, acts, W1, X)
+    np.testing.assert_allclose(Z, X.astype(np.float64) @ W1.T, rtol=1e-13, atol=1e-13)
+    mid = np.repeat(np.arange(len(hs)), hs)
+    for n in range(N):
+        np.testing.assert_allclose(H[:, n], _reference_act(acts[mid[n]], Z[:, n]),
+                                   rtol=1e-12, atol=1e-300)
