@@ -267,7 +267,9 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
 }
 
 // Tiles of the M3 forward: runs of whole segments up to kTile3 units wide;
-// a wider segment becomes pieces of kTile3 units added with atomics.
+// a wider segment becomes two halves added with atomics onto zeroed logits.
+// Two additions onto zero give the same sum in either order, so the
+// forward is deterministic for every segment width.
 void build_tiles(const std::vector<int32_t>& hs, std::vector<Tile3>& tiles, bool& has_split) {
   tiles.clear();
   has_split = false;
@@ -278,10 +280,9 @@ void build_tiles(const std::vector<int32_t>& hs, std::vector<Tile3>& tiles, bool
     if (w > kTile3) {
       if (cur.len > 0) tiles.push_back(cur);
       cur.len = 0;
-      for (int64_t s = 0; s < w; s += kTile3) {
-        const int64_t len = w - s < kTile3 ? w - s : kTile3;
-        tiles.push_back(Tile3{n + s, (int32_t)len, (int32_t)m, 1, 0});
-      }
+      const int64_t half = (w + 1) / 2;
+      tiles.push_back(Tile3{n, (int32_t)half, (int32_t)m, 1, 0});
+      tiles.push_back(Tile3{n + half, (int32_t)(w - half), (int32_t)m, 1, 0});
       has_split = true;
     } else {
       if (cur.len > 0 && cur.len + w > kTile3) {

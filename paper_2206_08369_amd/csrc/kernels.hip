@@ -340,9 +340,9 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s) {
 // inside one segment at a time, so the activation id is wave-uniform and
 // the running sums never mix models.  At the end of a segment the NG
 // groups' partial sums are combined with lane shuffles and written once
-// (plain store); pieces of a segment wider than the tile limit are added
-// with atomics instead (at most two pieces per segment for widths up to
-// twice the limit, and two additions onto zero are order-independent).
+// (plain store); the two halves of a segment wider than the tile limit are
+// added with atomics onto zeroed logits instead (two additions onto zero
+// are order-independent, so the result is still deterministic).
 // ---------------------------------------------------------------------------
 
 template <int OM>

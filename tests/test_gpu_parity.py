@@ -51,7 +51,7 @@ def make_net(pm, F, O, hs, acts, seed=0, W1=None, W2=None):
 # Shapes spanning the kernels' tiling: B = 1 and ragged batches, a batch
 # wider than 256 (two passes in the backward kernel) and wider than 1024,
 # F not a multiple of 4 or 16, O up to 16, widths 1 and segments wider than
-# the M3 tile (split into two and three pieces).
+# the M3 tile (split into two halves).
 CASES = {
     "tiny_b1": dict(hs=[1, 2, 3, 1], F=3, O=2, B=1),
     "ragged": dict(M=37, hmax=40, F=13, O=3, B=7),
