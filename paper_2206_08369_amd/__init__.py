@@ -33,7 +33,7 @@ PMLP_EDEVICE = -3
 PMLP_ESTATE = -4
 PMLP_FP32 = 0
 PMLP_BF16_GEMM = 1
-PMLP_NUM_KERNELS = 8
+PMLP_NUM_KERNELS = 9
 
 ACT_IDS = {
     "identity": 0, "relu": 1, "tanh": 2, "sigmoid": 3, "elu": 4, "leaky_relu": 5,

@@ -15,13 +15,17 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpmlp.so")
-SOURCES = ("kernels.hip", "api.hip")
+SOURCES = ("k_misc.hip", "k_gemm.hip", "k_m3.hip", "k_lds.hip", "api.hip")
 
 HIPCC_FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-munsafe-fp-atomics", "-Wall",
 ]
+
+# hipcc's host pass does not know the packed-fp32 feature name; that warning
+# is expected and harmless.
+_NOISE = "is not a recognized feature for this target"
 
 
 def hipcc() -> str:
@@ -30,24 +34,47 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libpmlp.so next to this file."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE, "-I", CSRC]
-    cmd += [os.path.join(CSRC, s) for s in SOURCES] + ["-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     out = (res.stdout or "") + (res.stderr or "")
-    # hipcc's host pass does not know the packed-fp32 feature name; that
-    # warning is expected and harmless.
-    noise = "is not a recognized feature for this target"
-    lines = [ln for ln in out.splitlines() if noise not in ln]
-    if res.returncode != 0:
-        sys.stderr.write("\n".join(lines) + "\n")
-        raise RuntimeError("hipcc failed with code %d" % res.returncode)
-    if verbose and lines:
-        print("\n".join(lines))
+    lines = [ln for ln in out.splitlines() if _NOISE not in ln]
+    return res.returncode, "\n".join(lines)
+
+
+def build(verbose: bool = False, jobs: int = 0) -> str:
+    """Compile every HIP translation unit (in parallel) and link libpmlp.so."""
+    from concurrent.futures import ThreadPoolExecutor
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    tag = "%d" % os.getpid()
+    objs, cmds = [], []
+    for src in SOURCES:
+        obj = os.path.join(objdir, src.replace(".hip", ".%s.o" % tag))
+        objs.append(obj)
+        cmds.append([hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE, "-I", CSRC, "-c",
+                                               os.path.join(CSRC, src), "-o", obj])
+    jobs = jobs or min(len(cmds), max(1, os.cpu_count() or 1))
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        results = list(ex.map(lambda c: _run(c, verbose), cmds))
+    failed = [(c, out) for c, (rc, out) in zip(cmds, results) if rc != 0]
+    for c, out in failed:
+        sys.stderr.write(out + "\n")
+    if failed:
+        raise RuntimeError("hipcc failed for %s" % ", ".join(os.path.basename(c[-3]) for c, _ in failed))
+    if verbose:
+        for rc, out in results:
+            if out:
+                print(out)
+    tmp = LIB + ".tmp" + tag
+    rc, out = _run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + ["-o", tmp],
+                   verbose)
+    for o in objs:
+        os.remove(o)
+    if rc != 0:
+        sys.stderr.write(out + "\n")
+        raise RuntimeError("linking libpmlp.so failed")
     os.replace(tmp, LIB)
     return LIB
 

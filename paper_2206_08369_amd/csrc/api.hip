@@ -6,6 +6,7 @@
 #include "pmlp_internal.h"
 
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -35,7 +36,7 @@ constexpr int32_t kMaxO = 16;
 static_assert(KID_COUNT == PMLP_NUM_KERNELS, "kernel id table");
 
 const char* const kKernelNames[KID_COUNT] = {
-    "pack_x", "gemm_fwd", "act", "m3_fwd", "ce", "m3_bwd", "gemm_bwd", "aux"};
+    "pack_x", "gemm_fwd", "act", "m3_fwd", "ce", "m3_bwd", "gemm_bwd", "aux", "bwd_fused"};
 
 uint64_t splitmix64_host(uint64_t x) {
   uint64_t z = x + 0x9E3779B97F4A7C15ull;
@@ -57,12 +58,13 @@ struct pmlp {
   hipStream_t stream = nullptr;
   int32_t F = 0, F4 = 0, O = 0, M = 0;
   int64_t N = 0;
+  int64_t Npad = 0;  // rows of W1/Zt/mid and the row stride of W2
   int32_t precision = PMLP_FP32;
   std::vector<int32_t> hs, acts;
   std::vector<int64_t> seg_off;
 
-  float* W1 = nullptr;  // [N][F4]
-  float* W2 = nullptr;  // [O][N]
+  float* W1 = nullptr;  // [Npad][F4] (+ slack)
+  float* W2 = nullptr;  // [O][Npad]
   int64_t* d_seg_off = nullptr;
   int32_t* d_act = nullptr;
   int32_t* d_mid = nullptr;
@@ -78,6 +80,7 @@ struct pmlp {
   float* Zt = nullptr;
   float* LG = nullptr;
   bool have_loss = false;
+  bool lds_kernels = true;  // persistent LDS-resident GEMMs where they apply
 
   bool prof = false;
   struct Pending {
@@ -164,7 +167,7 @@ int ensure_workspace(pmlp* h, int32_t Bp) {
   dfree(h->LG);
   h->capBp = 0;
   const size_t nx = (size_t)Bp * h->F4 * sizeof(float);
-  const size_t nz = (size_t)h->N * Bp * sizeof(float);
+  const size_t nz = (size_t)h->Npad * Bp * sizeof(float);
   const size_t nl = (size_t)h->M * Bp * h->O * sizeof(float);
   if (hipMalloc(&h->Xp, nx) != hipSuccess || hipMalloc(&h->Xt, nx) != hipSuccess ||
       hipMalloc(&h->Zt, nz) != hipSuccess || hipMalloc(&h->LG, nl) != hipSuccess) {
@@ -192,7 +195,17 @@ int check_batch(pmlp* h, const void* X, int32_t B) {
   return PMLP_OK;
 }
 
-int32_t pad_batch(int32_t B) { return (B + 15) & ~15; }
+// Batch padding: a multiple of 16, and a power of two up to 256 so that the
+// LDS-resident forward GEMM has an instance for it.
+int32_t pad_batch(int32_t B) {
+  int32_t Bp = (B + 15) & ~15;
+  if (Bp <= 256) {
+    int32_t p = 16;
+    while (p < Bp) p <<= 1;
+    Bp = p;
+  }
+  return Bp;
+}
 
 // Batch copy and the input-to-hidden product (Section 3, step 1).
 int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
@@ -200,6 +213,16 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
         return launch_pack_x(X, B, h->F, Bp, h->F4, h->Xp, h->Xt, h->stream);
       }))
     return rc;
+  if (h->lds_kernels && fwd_lds_supported(Bp, h->F4)) {
+    FwdLdsArgs f{};
+    f.W1 = h->W1;
+    f.Xp = h->Xp;
+    f.Zt = h->Zt;
+    f.N = h->N;
+    f.Bp = Bp;
+    f.K = h->F4;
+    return run(h, KID_GEMM_FWD, [&] { return launch_fwd_lds(f, h->stream); });
+  }
   GemmArgs g{};
   g.P = h->W1;
   g.ldp = h->F4;
@@ -231,7 +254,7 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
       return rc;
   }
   if (int rc = run(h, KID_M3_FWD, [&] {
-        return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->N, h->O, h->d_seg_off, h->d_act,
+        return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act,
                              h->d_tiles, h->ntiles, h->LG, (int64_t)Bp * h->O, h->O,
                              h->stream);
       }))
@@ -240,9 +263,31 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
         return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, h->stream);
       }))
     return rc;
+  if (h->lds_kernels && bwd_lds_supported(Bp, h->F4, h->O)) {
+    BwdArgs b{};
+    b.Zt = h->Zt;
+    b.G = h->LG;
+    b.Xt = h->Xt;
+    b.mid = h->d_mid;
+    b.act = h->d_act;
+    b.W1 = h->W1;
+    b.W2 = h->W2;
+    b.dW1 = dW1;
+    b.dW2 = dW2;
+    b.N = h->N;
+    b.ldw = h->Npad;
+    b.Bp = Bp;
+    b.F = h->F;
+    b.F4 = h->F4;
+    b.O = h->O;
+    b.lr = lr;
+    if (int rc = run(h, KID_BWD_FUSED, [&] { return launch_bwd_lds(b, h->stream); })) return rc;
+    h->have_loss = true;
+    return PMLP_OK;
+  }
   if (int rc = run(h, KID_M3_BWD, [&] {
-        return launch_m3_bwd(h->Zt, Bp, h->W2, h->N, h->O, h->d_mid, h->d_act, h->LG, lr, dW2,
-                             h->stream);
+        return launch_m3_bwd(h->Zt, Bp, h->W2, h->N, h->Npad, h->O, h->d_mid, h->d_seg_off,
+                             h->d_act, h->LG, lr, dW2, h->stream);
       }))
     return rc;
   GemmArgs g{};
@@ -326,12 +371,14 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
   h->O = O;
   h->M = M;
   h->N = N;
+  h->Npad = (N + 63) / 64 * 64;
+  if (const char* env = getenv("PMLP_GENERIC_KERNELS")) h->lds_kernels = env[0] == '0';
   h->hs.assign(hidden_sizes, hidden_sizes + M);
   h->acts.assign(act_ids, act_ids + M);
   h->seg_off.resize((size_t)M + 1);
   h->seg_off[0] = 0;
   for (int32_t m = 0; m < M; ++m) h->seg_off[m + 1] = h->seg_off[m] + hidden_sizes[m];
-  std::vector<int32_t> mid((size_t)N);
+  std::vector<int32_t> mid((size_t)h->Npad, M - 1);  // padding rows map to the last model
   for (int32_t m = 0; m < M; ++m)
     for (int64_t n = h->seg_off[m]; n < h->seg_off[m + 1]; ++n) mid[n] = m;
   std::vector<Tile3> tiles;
@@ -353,11 +400,13 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
   }
   h->dev = dev;
   float* d_bound2 = nullptr;
-  if (hipMalloc(&h->W1, (size_t)N * F4 * sizeof(float)) != hipSuccess ||
-      hipMalloc(&h->W2, (size_t)O * N * sizeof(float)) != hipSuccess ||
+  const int64_t Npad = h->Npad;
+  const size_t w1_bytes = ((size_t)Npad * F4 + 64) * sizeof(float);  // slack for clamped loads
+  if (hipMalloc(&h->W1, w1_bytes) != hipSuccess ||
+      hipMalloc(&h->W2, (size_t)O * Npad * sizeof(float)) != hipSuccess ||
       hipMalloc(&h->d_seg_off, ((size_t)M + 1) * sizeof(int64_t)) != hipSuccess ||
       hipMalloc(&h->d_act, (size_t)M * sizeof(int32_t)) != hipSuccess ||
-      hipMalloc(&h->d_mid, (size_t)N * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&h->d_mid, (size_t)Npad * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->d_tiles, tiles.size() * sizeof(Tile3)) != hipSuccess ||
       hipMalloc(&h->loss, (size_t)M * sizeof(float)) != hipSuccess ||
       hipMalloc(&h->flag, sizeof(int32_t)) != hipSuccess ||
@@ -370,12 +419,15 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
     PMLP_HIP(hipMemcpy(h->d_seg_off, h->seg_off.data(), ((size_t)M + 1) * sizeof(int64_t),
                        hipMemcpyHostToDevice));
     PMLP_HIP(hipMemcpy(h->d_act, act_ids, (size_t)M * sizeof(int32_t), hipMemcpyHostToDevice));
-    PMLP_HIP(hipMemcpy(h->d_mid, mid.data(), (size_t)N * sizeof(int32_t), hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(h->d_mid, mid.data(), (size_t)Npad * sizeof(int32_t),
+                       hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemset(h->W1, 0, w1_bytes));
+    PMLP_HIP(hipMemset(h->W2, 0, (size_t)O * Npad * sizeof(float)));
     PMLP_HIP(hipMemcpy(h->d_tiles, tiles.data(), tiles.size() * sizeof(Tile3),
                        hipMemcpyHostToDevice));
     PMLP_HIP(hipMemcpy(d_bound2, bound2.data(), (size_t)M * sizeof(float), hipMemcpyHostToDevice));
     PMLP_HIP(hipMemset(h->flag, 0, sizeof(int32_t)));
-    PMLP_HIP(launch_init_params(h->W1, N, F, F4, bound1, h->W2, O, h->d_mid, d_bound2,
+    PMLP_HIP(launch_init_params(h->W1, N, F, F4, bound1, h->W2, Npad, O, h->d_mid, d_bound2,
                                 splitmix64_host(seed), nullptr));
     PMLP_HIP(hipStreamSynchronize(nullptr));
     return PMLP_OK;
@@ -424,7 +476,7 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
       return rc;
   }
   return run(h, KID_M3_FWD, [&] {
-    return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->N, h->O, h->d_seg_off, h->d_act, h->d_tiles,
+    return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act, h->d_tiles,
                          h->ntiles, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
   });
 }
@@ -480,8 +532,9 @@ int pmlp_get_params(pmlp_t h, float* W1_host, float* W2_host) {
                          (size_t)h->F4 * sizeof(float), (size_t)h->F * sizeof(float),
                          (size_t)h->N, hipMemcpyDeviceToHost));
   if (W2_host)
-    PMLP_HIP(hipMemcpy(W2_host, h->W2, (size_t)h->O * h->N * sizeof(float),
-                       hipMemcpyDeviceToHost));
+    PMLP_HIP(hipMemcpy2D(W2_host, (size_t)h->N * sizeof(float), h->W2,
+                         (size_t)h->Npad * sizeof(float), (size_t)h->N * sizeof(float),
+                         (size_t)h->O, hipMemcpyDeviceToHost));
   return PMLP_OK;
 }
 
@@ -494,8 +547,9 @@ int pmlp_set_params(pmlp_t h, const float* W1_host, const float* W2_host) {
                          (size_t)h->F * sizeof(float), (size_t)h->F * sizeof(float),
                          (size_t)h->N, hipMemcpyHostToDevice));
   if (W2_host)
-    PMLP_HIP(hipMemcpy(h->W2, W2_host, (size_t)h->O * h->N * sizeof(float),
-                       hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy2D(h->W2, (size_t)h->Npad * sizeof(float), W2_host,
+                         (size_t)h->N * sizeof(float), (size_t)h->N * sizeof(float),
+                         (size_t)h->O, hipMemcpyHostToDevice));
   return PMLP_OK;
 }
 

@@ -1,0 +1,122 @@
+// Device-side definitions shared by the HIP kernels of libpmlp (gfx950).
+//
+// Notation: N hidden units in total, M models, F inputs, O outputs, B
+// samples in the batch, Bp = B rounded up to a multiple of 16.  Model m
+// owns the contiguous hidden units [seg_off[m], seg_off[m+1]) and mid[n]
+// is the model of hidden unit n (the Scatter Add index of Section 3,
+// collapsed to one row).
+//
+// Device layouts (Npad = N rounded up to a multiple of 64; rows n >= N are
+// padding that kernels may write but never read back into a result):
+//   W1  [Npad][F4] fp32, F4 = F rounded up to 4, pad columns held at 0
+//   W2  [O][Npad]  fp32 (row stride ldw = Npad)
+//   Xp  [Bp][F4]   batch copy, zero padded          (operand of Z = X W1^T)
+//   Xt  [F4][Bp]   transposed batch copy, zero padded (operand of dW1)
+//   Zt  [Npad][Bp] hidden pre-activations, batch-minor: the Bp values of one
+//                  hidden unit are contiguous.
+//   LG  [M][Bp][O] per-model logits, overwritten in place by dLoss/dlogits.
+// Zero padding of the batch (rows b >= B of Xp, columns b >= B of Xt, and
+// G = 0 for b >= B) makes every padded lane contribute exactly nothing to
+// the gradients, so no kernel needs the true B except the loss.
+
+#pragma once
+
+#include "pmlp_internal.h"
+
+#include <math.h>
+
+namespace pmlpk {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kBlock = 256;  // 4 waves of 64 lanes
+
+inline int ceil_div_i(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+inline unsigned grid_for(int64_t n) {
+  int64_t g = (n + kBlock - 1) / kBlock;
+  if (g > 1048576) g = 1048576;
+  if (g < 1) g = 1;
+  return (unsigned)g;
+}
+
+// ---------------------------------------------------------------------------
+// Activations (Section 3, last paragraph: one activation per contiguous
+// portion of the hidden layer).  Ids as in include/pmlp.h.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
+
+__device__ __forceinline__ float act_fwd(int a, float z) {
+  switch (a) {
+    case 0: return z;
+    case 1: return z > 0.f ? z : 0.f;
+    case 2: return tanhf(z);
+    case 3: return logistic(z);
+    case 4: return z > 0.f ? z : expm1f(z);
+    case 5: return z > 0.f ? z : 0.01f * z;
+    case 6: return z * (0.5f * erfcf(-z * 0.70710678118654752f));
+    case 7: return z * logistic(z);
+    case 8: return z > 20.f ? z : fmaxf(z, 0.f) + log1pf(expf(-fabsf(z)));
+    case 9: return z * logistic(2.f * z);
+    default: return 0.f;
+  }
+}
+
+// Value and derivative together.
+__device__ __forceinline__ float act_fwd_bwd(int a, float z, float* d) {
+  switch (a) {
+    case 0: *d = 1.f; return z;
+    case 1: *d = z > 0.f ? 1.f : 0.f; return z > 0.f ? z : 0.f;
+    case 2: { float t = tanhf(z); *d = 1.f - t * t; return t; }
+    case 3: { float s = logistic(z); *d = s * (1.f - s); return s; }
+    case 4: {
+      if (z > 0.f) { *d = 1.f; return z; }
+      *d = expf(z);
+      return expm1f(z);
+    }
+    case 5: *d = z > 0.f ? 1.f : 0.01f; return z > 0.f ? z : 0.01f * z;
+    case 6: {
+      float cdf = 0.5f * erfcf(-z * 0.70710678118654752f);
+      float pdf = 0.39894228040143268f * expf(-0.5f * z * z);
+      *d = cdf + z * pdf;
+      return z * cdf;
+    }
+    case 7: { float s = logistic(z); *d = s + z * s * (1.f - s); return z * s; }
+    case 8: {
+      if (z > 20.f) { *d = 1.f; return z; }
+      *d = logistic(z);
+      return fmaxf(z, 0.f) + log1pf(expf(-fabsf(z)));
+    }
+    case 9: { float s = logistic(2.f * z); *d = s + 2.f * z * s * (1.f - s); return z * s; }
+    default: *d = 0.f; return 0.f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Lane-group sums with DPP (register-only cross-lane moves).  A Hillis-Steele
+// scan with row shifts 1, 2, 4, 8 (zero fill outside the 16-lane row) and
+// the row broadcasts 15 and 31 leaves in the last lane of every aligned
+// group of LG lanes (LG a power of two up to 64) the sum over that group.
+// Each step only reads lanes inside the window that ends at a group's last
+// lane, so groups that are inactive do not affect active ones.
+// ---------------------------------------------------------------------------
+
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ float dpp_add(float v) {
+  const int moved = __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWMASK, 0xf, true);
+  return v + __int_as_float(moved);
+}
+
+__device__ __forceinline__ float group_sum_to_last(float v, int LG) {
+  if (LG > 1) v = dpp_add<0x111, 0xf>(v);   // row_shr:1
+  if (LG > 2) v = dpp_add<0x112, 0xf>(v);   // row_shr:2
+  if (LG > 4) v = dpp_add<0x114, 0xf>(v);   // row_shr:4
+  if (LG > 8) v = dpp_add<0x118, 0xf>(v);   // row_shr:8
+  if (LG > 16) v = dpp_add<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  if (LG > 32) v = dpp_add<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3
+  return v;
+}
+
+}  // namespace pmlpk

@@ -1,0 +1,325 @@
+// Modified Matrix Multiplication kernels: fused forward and backward (generic path).
+
+#include "device_common.h"
+
+namespace pmlpk {
+
+// ---------------------------------------------------------------------------
+// M3 forward (Section 3, steps 3-4 of the packed procedure): the product of
+// the hidden activations with W2 followed by the scatter-add over each
+// model's hidden units, fused so that the [B, O, N] product is never
+// stored:
+//   out[m, b, o] = sum_{n in tile, n in model m} act_m(Zt[n][b]) * W2[o][n]
+//
+// One wave per (tile, block of BW samples).  Lane l handles the four
+// samples b = 4*(l % LG) .. +3 (LG = BW/4 lanes per hidden unit) and
+// hidden units n = first + l/LG, stepping by NG = 64/LG; all groups stay
+// inside one segment at a time, so the activation id is wave-uniform (the
+// inner loop is instantiated per activation) and the running sums never
+// mix models.  At the end of a segment the NG groups' partial sums are
+// combined with lane shuffles and written once (plain store); the two
+// halves of a segment wider than the tile limit are added with atomics onto
+// zeroed logits instead (two additions onto zero are order-independent, so
+// the result is still deterministic).
+// ---------------------------------------------------------------------------
+
+static constexpr int kU = 4;  // hidden units per lane group per pass (loads in flight)
+
+template <int OM, int A>
+__device__ __forceinline__ void fwd_segment(const float* __restrict__ Zt, int Bp, int bl,
+                                            const float* __restrict__ W2, int64_t ldw, int O,
+                                            int64_t nbeg, int64_t nend, int g, int NG,
+                                            float (&acc)[4][OM]) {
+  // Four hidden units per group per pass, all loads first; addresses past
+  // the segment end are clamped to its last unit so every load is in bounds
+  // and unconditional.
+  for (int64_t n0 = nbeg + g; n0 < nend; n0 += kU * NG) {
+    f32x4 z[kU];
+    float w[kU][OM];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      int64_t n = n0 + u * NG;
+      if (n >= nend) n = nend - 1;
+      z[u] = *(const f32x4*)(Zt + n * Bp + bl);
+#pragma unroll
+      for (int o = 0; o < OM; ++o) {
+        const float v = W2[(int64_t)(o < O ? o : O - 1) * ldw + n];
+        w[u][o] = o < O ? v : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      if (n0 + u * NG >= nend) break;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float h = act_fwd(A, z[u][i]);
+#pragma unroll
+        for (int o = 0; o < OM; ++o) acc[i][o] = fmaf(h, w[u][o], acc[i][o]);
+      }
+    }
+  }
+}
+
+template <int OM>
+__global__ __launch_bounds__(kBlock) void k_m3_fwd(
+    const float* __restrict__ Zt, int Bp, int B, const float* __restrict__ W2, int64_t ldw,
+    int O, const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
+    const Tile3* __restrict__ tiles, int ntiles, int BW, int LG, int nbblk,
+    float* __restrict__ out, int64_t sm, int64_t sb) {
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+  const int tile = wv / nbblk;
+  const int bblk = wv - tile * nbblk;
+  if (tile >= ntiles) return;
+  const int NG = 64 / LG;
+  const int g = lane / LG;
+  const int pp = lane - g * LG;
+  const int b = bblk * BW + 4 * pp;
+  const bool bvalid = b < Bp;
+  const int bl = bvalid ? b : Bp - 4;  // lanes past the batch read a valid row, store nothing
+  const Tile3 t = tiles[tile];
+  const int64_t nend = t.n0 + t.len;
+  int64_t n = t.n0;
+  int m = t.m0;
+  while (n < nend) {
+    int64_t se = seg_off[m + 1];
+    if (se > nend) se = nend;
+    const int a = act[m];
+    float acc[4][OM];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int o = 0; o < OM; ++o) acc[i][o] = 0.f;
+    switch (a) {
+      case 0: fwd_segment<OM, 0>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 1: fwd_segment<OM, 1>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 2: fwd_segment<OM, 2>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 3: fwd_segment<OM, 3>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 4: fwd_segment<OM, 4>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 5: fwd_segment<OM, 5>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 6: fwd_segment<OM, 6>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 7: fwd_segment<OM, 7>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 8: fwd_segment<OM, 8>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      default: fwd_segment<OM, 9>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+    }
+    for (int s = LG; s < 64; s <<= 1)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int o = 0; o < OM; ++o) acc[i][o] += __shfl_xor(acc[i][o], s);
+    if (g == 0 && bvalid) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (b + i >= B) continue;
+        float* dst = out + (int64_t)m * sm + (int64_t)(b + i) * sb;
+#pragma unroll
+        for (int o = 0; o < OM; ++o) {
+          if (o >= O) continue;
+          if (t.atomic) unsafeAtomicAdd(dst + o, acc[i][o]);
+          else dst[o] = acc[i][o];
+        }
+      }
+    }
+    n = se;
+    ++m;
+  }
+}
+
+template <int OM>
+static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float* W2,
+                            int64_t ldw, int32_t O, const int64_t* seg_off, const int32_t* act,
+                            const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
+                            int64_t sb, hipStream_t s) {
+  int BW = 64;
+  if (Bp < 64) BW = Bp <= 16 ? 16 : (Bp <= 32 ? 32 : 64);
+  const int LG = BW / 4;
+  const int nbblk = ceil_div_i(Bp, BW);
+  const int64_t waves = (int64_t)ntiles * nbblk;
+  const unsigned blocks = (unsigned)((waves + 3) / 4);
+  k_m3_fwd<OM><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, BW,
+                                         LG, nbblk, out, sm, sb);
+}
+
+hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
+                         int32_t O, const int64_t* seg_off, const int32_t* act,
+                         const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
+                         int64_t sb, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
+  else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
+  else if (O <= 8) m3_fwd_dispatch<8>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
+  else if (O <= 10) m3_fwd_dispatch<10>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
+  else m3_fwd_dispatch<16>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// M3 backward + activation derivative + W2 update.  The gradient of the
+// scatter-add is a gather by model id (each hidden unit only ever sees its
+// own model's output gradient, Section 3):
+//   dH[b][n] = sum_o G[mid[n]][b][o] * W2[o][n]          (W2 before update)
+//   dZ[b][n] = dH[b][n] * act'(Z[b][n])                  (in place over Zt)
+//   dW2[o][n] = sum_b G[mid[n]][b][o] * act(Z[b][n])
+//   W2[o][n] -= lr * dW2[o][n]        (or dW2 stored, gradient mode)
+// One wave per run of kT5 consecutive hidden units and the whole batch.
+// Lanes as in the forward (groups of LG lanes per hidden unit, four samples
+// per lane), with `slots` passes when the batch is wider than 256.  The
+// wave walks the segments of its run, so the model (its G rows, held in
+// registers) and the activation are wave-uniform.  Per-unit dW2 partial
+// sums are reduced over the group with DPP and accumulated in LDS across
+// passes; W2 is updated once at the end.
+// ---------------------------------------------------------------------------
+
+static constexpr int kT5 = 256;
+
+template <int OM, int A>
+__device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, int Bp, int bl, bool bvalid,
+                                            const float* __restrict__ W2, int64_t ldw, int O,
+                                            int64_t nbeg, int64_t nend, int g, int NG, int LG,
+                                            int pp, const float (&gr)[4][OM],
+                                            float* __restrict__ dwl, int64_t r0, bool first) {
+  for (int64_t n0 = nbeg + g; n0 < nend; n0 += kU * NG) {
+    f32x4 z[kU];
+    float w[kU][OM];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      int64_t n = n0 + u * NG;
+      if (n >= nend) n = nend - 1;
+      z[u] = *(const f32x4*)(Zt + n * Bp + bl);
+#pragma unroll
+      for (int o = 0; o < OM; ++o) {
+        const float v = W2[(int64_t)(o < O ? o : O - 1) * ldw + n];
+        w[u][o] = o < O ? v : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t n = n0 + u * NG;
+      if (n >= nend) break;
+      float dw[OM];
+#pragma unroll
+      for (int o = 0; o < OM; ++o) dw[o] = 0.f;
+      f32x4 dz;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float hp;
+        const float h = act_fwd_bwd(A, z[u][i], &hp);
+        float dh = 0.f;
+#pragma unroll
+        for (int o = 0; o < OM; ++o) dh = fmaf(gr[i][o], w[u][o], dh);
+        dz[i] = dh * hp;
+#pragma unroll
+        for (int o = 0; o < OM; ++o) dw[o] = fmaf(gr[i][o], h, dw[o]);
+      }
+      if (bvalid) *(f32x4*)(Zt + n * Bp + bl) = dz;
+#pragma unroll
+      for (int o = 0; o < OM; ++o) dw[o] = group_sum_to_last(dw[o], LG);
+      if (pp == LG - 1) {
+        float* d = dwl + (n - r0) * OM;
+#pragma unroll
+        for (int o = 0; o < OM; ++o)
+          if (o < O) d[o] = first ? dw[o] : d[o] + dw[o];
+      }
+    }
+  }
+}
+
+template <int OM, bool GRAD>
+__global__ __launch_bounds__(kBlock) void k_m3_bwd(
+    float* __restrict__ Zt, int Bp, float* __restrict__ W2, int64_t N, int64_t ldw, int O,
+    const int32_t* __restrict__ mid, const int64_t* __restrict__ seg_off,
+    const int32_t* __restrict__ act, const float* __restrict__ G, int LG, int slots, float lr,
+    float* __restrict__ dW2) {
+  __shared__ float lds[4 * kT5 * OM];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  float* dwl = lds + wave * kT5 * OM;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * kT5;
+  int64_t r1 = r0 + kT5;
+  if (r1 > N) r1 = N;
+  const int NG = 64 / LG;
+  const int g = lane / LG;
+  const int pp = lane - g * LG;
+  if (r0 < N) {
+    const int m_first = mid[r0];
+    for (int slot = 0; slot < slots; ++slot) {
+      const int b = slot * 4 * LG + 4 * pp;
+      const bool bvalid = b < Bp;
+      const int bl = bvalid ? b : Bp - 4;  // lanes past the batch read a valid row, add nothing
+      int64_t n = r0;
+      int m = m_first;
+      while (n < r1) {
+        int64_t se = seg_off[m + 1];
+        if (se > r1) se = r1;
+        const int a = act[m];
+        float gr[4][OM];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int o = 0; o < OM; ++o) {
+            const float v = G[((int64_t)m * Bp + bl + i) * O + (o < O ? o : O - 1)];
+            gr[i][o] = (bvalid && o < O) ? v : 0.f;
+          }
+        const bool first = slot == 0;
+        switch (a) {
+          case 0: bwd_segment<OM, 0>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 1: bwd_segment<OM, 1>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 2: bwd_segment<OM, 2>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 3: bwd_segment<OM, 3>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 4: bwd_segment<OM, 4>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 5: bwd_segment<OM, 5>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 6: bwd_segment<OM, 6>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 7: bwd_segment<OM, 7>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 8: bwd_segment<OM, 8>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          default: bwd_segment<OM, 9>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+        }
+        n = se;
+        ++m;
+      }
+    }
+  }
+  __syncthreads();
+  const int64_t cnt = r1 > r0 ? (r1 - r0) * O : 0;
+  for (int64_t idx = lane; idx < cnt; idx += 64) {
+    const int64_t nl = idx / O;
+    const int o = (int)(idx - nl * O);
+    const int64_t n = r0 + nl;
+    const float d = dwl[nl * OM + o];
+    if (GRAD) dW2[(int64_t)o * N + n] = d;
+    else W2[(int64_t)o * ldw + n] -= lr * d;
+  }
+}
+
+template <int OM>
+static void m3_bwd_dispatch(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t ldw, int32_t O,
+                            const int32_t* mid, const int64_t* seg_off, const int32_t* act,
+                            const float* G, float lr, float* dW2, hipStream_t s) {
+  int LG = 64;
+  const int q = (Bp + 3) / 4;
+  if (q < 64) {
+    LG = 1;
+    while (LG < q) LG <<= 1;
+  }
+  const int slots = ceil_div_i(Bp, 4 * LG);
+  const int64_t waves = (N + kT5 - 1) / kT5;
+  const unsigned blocks = (unsigned)((waves + 3) / 4);
+  if (dW2)
+    k_m3_bwd<OM, true><<<blocks, kBlock, 0, s>>>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, LG,
+                                                 slots, lr, dW2);
+  else
+    k_m3_bwd<OM, false><<<blocks, kBlock, 0, s>>>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, LG,
+                                                  slots, lr, dW2);
+}
+
+hipError_t launch_m3_bwd(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t ldw, int32_t O,
+                         const int32_t* mid, const int64_t* seg_off, const int32_t* act,
+                         const float* G, float lr, float* dW2, hipStream_t s) {
+  if (O <= 2) m3_bwd_dispatch<2>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else if (O <= 4) m3_bwd_dispatch<4>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else if (O <= 8) m3_bwd_dispatch<8>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else if (O <= 10) m3_bwd_dispatch<10>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else m3_bwd_dispatch<16>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  return hipGetLastError();
+}
+
+}  // namespace pmlpk

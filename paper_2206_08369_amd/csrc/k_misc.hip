@@ -1,0 +1,188 @@
+// Initialisation, batch packing, fills, the loss and the hidden-layer view.
+
+#include "device_common.h"
+
+namespace pmlpk {
+
+// ---------------------------------------------------------------------------
+// Initialisation: counter-based splitmix64 draws (Steele, Lea and Flood,
+// OOPSLA 2014), U(-bound, bound) with bound = 1/sqrt(fan_in).
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ float uniform_weight(uint64_t key, uint64_t tag, uint64_t idx,
+                                                float bound) {
+  const uint64_t r = splitmix64(key ^ (tag << 60) ^ idx);
+  const int32_t k = (int32_t)(r >> 40);                             // 24 random bits
+  const float c = (float)(2 * k - 16777216) * 5.9604644775390625e-08f;  // exact: (2u - 1)
+  return c * bound;                                                // one rounding
+}
+
+__global__ __launch_bounds__(kBlock) void k_init_w1(float* __restrict__ W1, int64_t N, int F,
+                                                    int F4, float bound, uint64_t key) {
+  const int64_t total = N * F4;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int64_t n = i / F4;
+    const int f = (int)(i - n * F4);
+    W1[i] = f < F ? uniform_weight(key, 1, (uint64_t)(n * F + f), bound) : 0.f;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_init_w2(float* __restrict__ W2, int64_t N,
+                                                    int64_t ldw, int O,
+                                                    const int32_t* __restrict__ mid,
+                                                    const float* __restrict__ bound2,
+                                                    uint64_t key) {
+  const int64_t total = N * O;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int64_t o = i / N;
+    const int64_t n = i - o * N;
+    W2[o * ldw + n] = uniform_weight(key, 2, (uint64_t)i, bound2[mid[n]]);  // counter o*N + n
+  }
+}
+
+hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float bound1,
+                              float* W2, int64_t ldw, int32_t O, const int32_t* mid,
+                              const float* bound2, uint64_t key, hipStream_t s) {
+  k_init_w1<<<grid_for(N * F4), kBlock, 0, s>>>(W1, N, F, F4, bound1, key);
+  k_init_w2<<<grid_for(N * O), kBlock, 0, s>>>(W2, N, ldw, O, mid, bound2, key);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Batch packing: X [B][F] -> Xp [Bp][F4] and Xt [F4][Bp], zero padded.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void k_pack_x(const float* __restrict__ X, int B, int F,
+                                                   int Bp, int F4, float* __restrict__ Xp,
+                                                   float* __restrict__ Xt) {
+  const int64_t total = (int64_t)Bp * F4;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int b = (int)(i / F4);
+    const int f = (int)(i - (int64_t)b * F4);
+    const float v = (b < B && f < F) ? X[(int64_t)b * F + f] : 0.f;
+    Xp[i] = v;
+    Xt[(int64_t)f * Bp + b] = v;
+  }
+}
+
+hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
+                         float* Xp, float* Xt, hipStream_t s) {
+  k_pack_x<<<grid_for((int64_t)Bp * F4), kBlock, 0, s>>>(X, B, F, Bp, F4, Xp, Xt);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void k_fill(float* __restrict__ p, int64_t n, float v) {
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kBlock)
+    p[i] = v;
+}
+
+hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  k_fill<<<grid_for(n), kBlock, 0, s>>>(p, n, v);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Per-model softmax cross-entropy, mean over the batch (the loss the
+// packed training minimises; its sum over models has per-model gradients
+// equal to each model's own).  One wave per model; in place:
+//   LG[m][b][:] (logits) -> G = (softmax - onehot(y_b)) / B,  G = 0 for b >= B
+//   loss[m] = mean_b (logsumexp - logit_y)
+// A label outside [0, O) raises *flag.
+// ---------------------------------------------------------------------------
+
+template <int OM>
+__global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
+                                               const int32_t* __restrict__ y, int M, int Bp,
+                                               int B, int O, float invB,
+                                               float* __restrict__ loss,
+                                               int32_t* __restrict__ flag) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;
+  float part = 0.f;
+  for (int b = lane; b < Bp; b += 64) {
+    float* row = LG + ((int64_t)m * Bp + b) * O;
+    if (b < B) {
+      float l[OM];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int o = 0; o < OM; ++o) {
+        l[o] = o < O ? row[o] : -INFINITY;
+        mx = fmaxf(mx, l[o]);
+      }
+      float se = 0.f;
+#pragma unroll
+      for (int o = 0; o < OM; ++o)
+        if (o < O) se += expf(l[o] - mx);
+      const float lse = mx + logf(se);
+      const int yb = y[b];
+      if (yb < 0 || yb >= O) flag[0] = 1;
+      float ly = 0.f;
+#pragma unroll
+      for (int o = 0; o < OM; ++o)
+        if (o == yb) ly = l[o];
+      part += lse - ly;
+#pragma unroll
+      for (int o = 0; o < OM; ++o)
+        if (o < O) row[o] = (expf(l[o] - lse) - (o == yb ? 1.f : 0.f)) * invB;
+    } else {
+      for (int o = 0; o < O; ++o) row[o] = 0.f;
+    }
+  }
+#pragma unroll
+  for (int s = 32; s > 0; s >>= 1) part += __shfl_xor(part, s);
+  if (lane == 0) loss[m] = part * invB;
+}
+
+hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
+                     float* loss, int32_t* flag, hipStream_t s) {
+  const unsigned blocks = (unsigned)((M + 3) / 4);
+  const float invB = 1.0f / (float)B;
+  if (O <= 2) k_ce<2><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
+  else if (O <= 4) k_ce<4><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
+  else if (O <= 8) k_ce<8><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
+  else k_ce<16><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Hidden layer in the caller's [B][N] layout (inspection path).
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void k_hidden_out(const float* __restrict__ Zt, int Bp,
+                                                       int B, int64_t N,
+                                                       const int32_t* __restrict__ mid,
+                                                       const int32_t* __restrict__ act,
+                                                       float* __restrict__ Z,
+                                                       float* __restrict__ H) {
+  const int64_t total = (int64_t)B * N;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int64_t b = i / N;
+    const int64_t n = i - b * N;
+    const float z = Zt[n * Bp + b];
+    if (Z) Z[i] = z;
+    if (H) H[i] = act_fwd(act[mid[n]], z);
+  }
+}
+
+hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
+                             const int32_t* mid, const int32_t* act, float* Z, float* H,
+                             hipStream_t s) {
+  k_hidden_out<<<grid_for((int64_t)B * N), kBlock, 0, s>>>(Zt, Bp, B, N, mid, act, Z, H);
+  return hipGetLastError();
+}
+
+}  // namespace pmlpk

@@ -29,7 +29,8 @@ enum KernelId {
   KID_M3_BWD = 5,
   KID_GEMM_BWD = 6,
   KID_AUX = 7,
-  KID_COUNT = 8
+  KID_BWD_FUSED = 8,  // fused backward (M3 backward + dW1 GEMM + updates)
+  KID_COUNT = 9
 };
 
 // GEMM epilogues: C[p][q] = sum_k P[p][k] Q[q][k]
@@ -56,14 +57,49 @@ struct GemmArgs {
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
 
+// Persistent forward GEMM with the batch resident in LDS:
+// Zt[p][q] = sum_k W1[p][k] Xp[q][k], p < N, q < Bp (Bp in {16,...,256}).
+struct FwdLdsArgs {
+  const float* W1;   // [Npad][K]
+  const float* Xp;   // [Bp][K]
+  float* Zt;         // [Npad][Bp]
+  int64_t N;
+  int32_t Bp;
+  int32_t K;         // F4
+  int32_t SQ;        // LDS row stride (set by the launcher)
+};
+bool fwd_lds_supported(int32_t Bp, int32_t F4);
+hipError_t launch_fwd_lds(const FwdLdsArgs& a, hipStream_t s);
+
+// Fused backward (dZ formed in registers, dW1 GEMM, dW2, both updates),
+// persistent, with Xt resident in LDS.
+struct BwdArgs {
+  const float* Zt;   // [Npad][Bp] pre-activations
+  const float* G;    // [M][Bp][O] dLoss/dlogits (0 for padded samples)
+  const float* Xt;   // [F4][Bp]
+  const int32_t* mid;
+  const int32_t* act;
+  float* W1;         // [Npad][F4], updated unless dW1 is set
+  float* W2;         // [O][ldw], updated unless dW2 is set
+  float* dW1;        // gradient mode: [N][F]
+  float* dW2;        // gradient mode: [O][N]
+  int64_t N;
+  int64_t ldw;
+  int32_t Bp, F, F4, O;
+  int32_t SQ;        // LDS row stride (set by the launcher)
+  float lr;
+};
+bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O);
+hipError_t launch_bwd_lds(const BwdArgs& a, hipStream_t s);
+
 hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float bound1,
-                              float* W2, int32_t O, const int32_t* mid, const float* bound2,
-                              uint64_t key, hipStream_t s);
+                              float* W2, int64_t ldw, int32_t O, const int32_t* mid,
+                              const float* bound2, uint64_t key, hipStream_t s);
 
 hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
                          float* Xp, float* Xt, hipStream_t s);
 
-hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t N,
+hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
                          const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
                          int64_t sb, hipStream_t s);
@@ -71,9 +107,9 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
                      float* loss, int32_t* flag, hipStream_t s);
 
-hipError_t launch_m3_bwd(float* Zt, int32_t Bp, float* W2, int64_t N, int32_t O,
-                         const int32_t* mid, const int32_t* act, const float* G, float lr,
-                         float* dW2, hipStream_t s);
+hipError_t launch_m3_bwd(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t ldw, int32_t O,
+                         const int32_t* mid, const int64_t* seg_off, const int32_t* act,
+                         const float* G, float lr, float* dW2, hipStream_t s);
 
 hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              const int32_t* mid, const int32_t* act, float* Z, float* H,

@@ -62,7 +62,28 @@ CASES = {
     "f1": dict(M=8, hmax=9, F=1, O=2, B=17),
     "b1100": dict(M=6, hmax=20, F=20, O=2, B=1100),
     "all_width_one": dict(hs=[1] * 70, F=7, O=4, B=20),
+    # shapes of the LDS-resident kernels: batch padded to 16..256, F giving
+    # 1, 2, 4, 7 and 8 sixteen-wide column tiles, K tails of 0, 4 and 12
+    "f100_b250": dict(M=30, hmax=300, F=100, O=2, B=250),
+    "f52_b128": dict(M=25, hmax=120, F=52, O=2, B=128),
+    "f128_b100_o4": dict(M=15, hmax=90, F=128, O=4, B=100),
+    "f32_b32_o10": dict(M=25, hmax=200, F=32, O=10, B=29),
+    "f140_b64": dict(M=12, hmax=64, F=140, O=2, B=64),
+    "f12_b16": dict(M=40, hmax=30, F=12, O=2, B=16),
 }
+
+# Kernel paths: the persistent LDS-resident kernels (default where a shape
+# allows them) and the generic kernels, selected when the handle is made.
+PATHS = ["default", "generic"]
+
+
+@pytest.fixture(params=PATHS)
+def path(request, monkeypatch):
+    if request.param == "generic":
+        monkeypatch.setenv("PMLP_GENERIC_KERNELS", "1")
+    else:
+        monkeypatch.delenv("PMLP_GENERIC_KERNELS", raising=False)
+    return request.param
 
 
 def case_inputs(name, seed=0):
@@ -149,7 +170,7 @@ def test_hidden_layer(pm, orc, torch, name):
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_forward_logits(pm, orc, torch, name):
+def test_forward_logits(pm, orc, torch, name, path):
     hs, acts, F, O, B, X, y = case_inputs(name)
     net = make_net(pm, F, O, hs, acts, seed=12)
     W1, W2 = net.get_params()
@@ -161,7 +182,7 @@ def test_forward_logits(pm, orc, torch, name):
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_gradients_and_losses(pm, orc, torch, name):
+def test_gradients_and_losses(pm, orc, torch, name, path):
     hs, acts, F, O, B, X, y = case_inputs(name)
     net = make_net(pm, F, O, hs, acts, seed=13)
     W1, W2 = net.get_params()
@@ -174,8 +195,9 @@ def test_gradients_and_losses(pm, orc, torch, name):
     net.close()
 
 
-@pytest.mark.parametrize("name", ["ragged", "tile_spanning", "o10_b32", "b300_f100"])
-def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name):
+@pytest.mark.parametrize("name", ["ragged", "tile_spanning", "o10_b32", "b300_f100",
+                                  "f100_b250", "f128_b100_o4", "f32_b32_o10"])
+def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name, path):
     """The fused update equals W - lr * dW with dW from the gradient mode
     (to fp32 rounding of W), and the step's losses match the oracle."""
     hs, acts, F, O, B, X, y = case_inputs(name)
@@ -262,7 +284,7 @@ def test_packed_model_equals_model_alone(pm, torch):
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("wname", ["w60_f10", "w1k_f50"])
-def test_one_epoch(pm, orc, torch, wname):
+def test_one_epoch(pm, orc, torch, wname, path):
     w = wl.WORKLOADS[wname]
     hs, acts = w.model_grid()
     X, y = wl.workload_dataset(w)
