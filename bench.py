@@ -49,6 +49,9 @@ def kernel_work(name, B, F, N, M, O):
         return "hbm", f4 * (N * B + O * N + B * M * O), 2.0 * B * O * N
     if name == "m3_bwd":        # read Z, G, W2; write dZ, W2
         return "hbm", f4 * (2 * N * B + 2 * O * N + B * M * O), 4.0 * B * O * N
+    if name == "bwd_fused":     # read Z, G, X; read+write W1 and W2 (dZ stays in registers)
+        return ("mfma", f4 * (N * B + B * M * O + B * F + 2 * N * F + 2 * O * N),
+                2.0 * B * F * N + 4.0 * B * O * N)
     if name == "ce":            # read logits, y; write G, loss
         return "hbm", f4 * (2 * B * M * O + B + M), 0.0
     if name == "pack_x":        # read X; write two padded copies

@@ -46,19 +46,34 @@ inline unsigned grid_for(int64_t n) {
 // portion of the hidden layer).  Ids as in include/pmlp.h.
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ float logistic(float z) { return 1.0f / (1.0f + expf(-z)); }
+// The transcendental pieces use the hardware approximations (v_exp_f32 on
+// x*log2(e), v_log_f32, v_rcp_f32; about 1 ulp each), which keeps the
+// per-element cost of the activation far below the memory time of the
+// kernels that apply it.  Absolute errors stay near 1e-7 for the values
+// these networks see, well inside the per-model normwise tolerance.
+
+__device__ __forceinline__ float fexp(float x) { return __expf(x); }
+__device__ __forceinline__ float frcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float flog(float x) { return __logf(x); }
+
+__device__ __forceinline__ float logistic(float z) { return frcp(1.0f + fexp(-z)); }
+
+// Normal CDF Phi(z) = erfc(-z/sqrt 2)/2 (library erfc: accurate in both tails)
+__device__ __forceinline__ float normal_cdf(float z) {
+  return 0.5f * erfcf(-z * 0.70710678118654752f);
+}
 
 __device__ __forceinline__ float act_fwd(int a, float z) {
   switch (a) {
     case 0: return z;
     case 1: return z > 0.f ? z : 0.f;
-    case 2: return tanhf(z);
+    case 2: return 1.f - 2.f * frcp(1.f + fexp(2.f * z));  // tanh
     case 3: return logistic(z);
-    case 4: return z > 0.f ? z : expm1f(z);
+    case 4: return z > 0.f ? z : fexp(z) - 1.f;
     case 5: return z > 0.f ? z : 0.01f * z;
-    case 6: return z * (0.5f * erfcf(-z * 0.70710678118654752f));
+    case 6: return z * normal_cdf(z);
     case 7: return z * logistic(z);
-    case 8: return z > 20.f ? z : fmaxf(z, 0.f) + log1pf(expf(-fabsf(z)));
+    case 8: return z > 20.f ? z : fmaxf(z, 0.f) + flog(1.f + fexp(-fabsf(z)));
     case 9: return z * logistic(2.f * z);
     default: return 0.f;
   }
@@ -69,27 +84,36 @@ __device__ __forceinline__ float act_fwd_bwd(int a, float z, float* d) {
   switch (a) {
     case 0: *d = 1.f; return z;
     case 1: *d = z > 0.f ? 1.f : 0.f; return z > 0.f ? z : 0.f;
-    case 2: { float t = tanhf(z); *d = 1.f - t * t; return t; }
-    case 3: { float s = logistic(z); *d = s * (1.f - s); return s; }
+    case 2: {
+      const float t = 1.f - 2.f * frcp(1.f + fexp(2.f * z));
+      *d = 1.f - t * t;
+      return t;
+    }
+    case 3: { const float s = logistic(z); *d = s * (1.f - s); return s; }
     case 4: {
       if (z > 0.f) { *d = 1.f; return z; }
-      *d = expf(z);
-      return expm1f(z);
+      const float e = fexp(z);
+      *d = e;
+      return e - 1.f;
     }
     case 5: *d = z > 0.f ? 1.f : 0.01f; return z > 0.f ? z : 0.01f * z;
     case 6: {
-      float cdf = 0.5f * erfcf(-z * 0.70710678118654752f);
-      float pdf = 0.39894228040143268f * expf(-0.5f * z * z);
+      const float cdf = normal_cdf(z);
+      const float pdf = 0.39894228040143268f * fexp(-0.5f * z * z);
       *d = cdf + z * pdf;
       return z * cdf;
     }
-    case 7: { float s = logistic(z); *d = s + z * s * (1.f - s); return z * s; }
+    case 7: { const float s = logistic(z); *d = s + z * s * (1.f - s); return z * s; }
     case 8: {
       if (z > 20.f) { *d = 1.f; return z; }
       *d = logistic(z);
-      return fmaxf(z, 0.f) + log1pf(expf(-fabsf(z)));
+      return fmaxf(z, 0.f) + flog(1.f + fexp(-fabsf(z)));
     }
-    case 9: { float s = logistic(2.f * z); *d = s + 2.f * z * s * (1.f - s); return z * s; }
+    case 9: {
+      const float s = logistic(2.f * z);
+      *d = s + 2.f * z * s * (1.f - s);
+      return z * s;
+    }
     default: *d = 0.f; return 0.f;
   }
 }

@@ -150,7 +150,8 @@ template <int TQ, int TP, int OM>
 __device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ][TP], float (&dw)[TP][OM],
                                            const float* qptr, int SQ, const f32x4 (&cz)[TP],
                                            const f32x4 (&cg)[TP][OM],
-                                           const float (&w2)[TP][OM], const int (&arow)[TP]) {
+                                           const float (&w2)[TP][OM], const int (&arow)[TP],
+                                           int auni) {
   f32x4 q[TQ];
 #pragma unroll
   for (int i = 0; i < TQ; ++i) q[i] = *(const f32x4*)(qptr + 16 * i * SQ);
@@ -161,7 +162,10 @@ __device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ][TP], float (&dw)[TP]
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       float hp;
-      const float h = act_fwd_bwd(arow[j], cz[j][s], &hp);
+      // auni >= 0: every row of the tile has this activation (wave-uniform
+      // branch); otherwise each lane dispatches on its own row's id.
+      const float h = auni >= 0 ? act_fwd_bwd(auni, cz[j][s], &hp)
+                                : act_fwd_bwd(arow[j], cz[j][s], &hp);
       float dh = 0.f;
 #pragma unroll
       for (int o = 0; o < OM; ++o) {
@@ -216,6 +220,12 @@ __global__ __launch_bounds__(kLdsBlock) void k_bwd_lds(BwdArgs a) {
 #pragma unroll
       for (int o = 0; o < OM; ++o) w2[j][o] = a.W2[(int64_t)o * a.ldw + p];
     }
+    // one activation for the whole tile (the common case: segments are wide)
+    const int a0 = __builtin_amdgcn_readfirstlane(arow[0]);
+    bool same = true;
+#pragma unroll
+    for (int j = 0; j < TP; ++j) same = same && arow[j] == a0;
+    const int auni = __all(same) ? a0 : -1;
     f32x4 acc[TQ][TP];
     float dw[TP][OM];
 #pragma unroll
@@ -233,20 +243,20 @@ __global__ __launch_bounds__(kLdsBlock) void k_bwd_lds(BwdArgs a) {
       for (; c + 2 < nch; c += 2) {
         bwdl_load<TP, OM>(zb, gb, zrow, grow, (c + 1) * 16 + 4 * lk);
         __builtin_amdgcn_sched_barrier(0);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow);
+        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow, auni);
         __builtin_amdgcn_sched_barrier(0);
         bwdl_load<TP, OM>(za, ga, zrow, grow, (c + 2) * 16 + 4 * lk);
         __builtin_amdgcn_sched_barrier(0);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * (c + 1), SQ, zb, gb, w2, arow);
+        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * (c + 1), SQ, zb, gb, w2, arow, auni);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (c + 1 < nch) {
         bwdl_load<TP, OM>(zb, gb, zrow, grow, (c + 1) * 16 + 4 * lk);
         __builtin_amdgcn_sched_barrier(0);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * (c + 1), SQ, zb, gb, w2, arow);
+        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow, auni);
+        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * (c + 1), SQ, zb, gb, w2, arow, auni);
       } else {
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow);
+        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow, auni);
       }
     }
     // dW2: combine the four lk lanes of each row; lanes lk == 0 write.
