@@ -118,6 +118,9 @@ def main(argv=None):
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time of the oracle baseline sample (0 = skip)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, run a plain device copy of this many MiB (a known-size "
+                         "reference dispatch for hardware byte counters)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -144,6 +147,14 @@ def main(argv=None):
         s = (k % nfull) * w.B
         net.train_step(Xd[s:s + w.B], yd[s:s + w.B], w.lr)
 
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for k in range(args.warmup):
         step(k)
     torch.cuda.synchronize()

@@ -67,7 +67,8 @@ struct pmlp {
   float* W2 = nullptr;  // [O][Npad]
   int64_t* d_seg_off = nullptr;
   int32_t* d_act = nullptr;
-  int32_t* d_mid = nullptr;
+  int32_t* d_mid = nullptr;   // [Npad] model of each hidden unit
+  int32_t* d_actn = nullptr;  // [Npad] activation id of each hidden unit
   Tile3* d_tiles = nullptr;
   int32_t ntiles = 0;
   bool has_split = false;
@@ -101,6 +102,7 @@ void release(pmlp* h) {
   dfree(h->d_seg_off);
   dfree(h->d_act);
   dfree(h->d_mid);
+  dfree(h->d_actn);
   dfree(h->d_tiles);
   dfree(h->loss);
   dfree(h->flag);
@@ -269,7 +271,7 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
     b.G = h->LG;
     b.Xt = h->Xt;
     b.mid = h->d_mid;
-    b.act = h->d_act;
+    b.actn = h->d_actn;
     b.W1 = h->W1;
     b.W2 = h->W2;
     b.dW1 = dW1;
@@ -379,8 +381,12 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
   h->seg_off[0] = 0;
   for (int32_t m = 0; m < M; ++m) h->seg_off[m + 1] = h->seg_off[m] + hidden_sizes[m];
   std::vector<int32_t> mid((size_t)h->Npad, M - 1);  // padding rows map to the last model
+  std::vector<int32_t> actn((size_t)h->Npad, act_ids[M - 1]);
   for (int32_t m = 0; m < M; ++m)
-    for (int64_t n = h->seg_off[m]; n < h->seg_off[m + 1]; ++n) mid[n] = m;
+    for (int64_t n = h->seg_off[m]; n < h->seg_off[m + 1]; ++n) {
+      mid[n] = m;
+      actn[n] = act_ids[m];
+    }
   std::vector<Tile3> tiles;
   build_tiles(h->hs, tiles, h->has_split);
   h->ntiles = (int32_t)tiles.size();
@@ -407,6 +413,7 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
       hipMalloc(&h->d_seg_off, ((size_t)M + 1) * sizeof(int64_t)) != hipSuccess ||
       hipMalloc(&h->d_act, (size_t)M * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->d_mid, (size_t)Npad * sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&h->d_actn, (size_t)Npad * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->d_tiles, tiles.size() * sizeof(Tile3)) != hipSuccess ||
       hipMalloc(&h->loss, (size_t)M * sizeof(float)) != hipSuccess ||
       hipMalloc(&h->flag, sizeof(int32_t)) != hipSuccess ||
@@ -420,6 +427,8 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
                        hipMemcpyHostToDevice));
     PMLP_HIP(hipMemcpy(h->d_act, act_ids, (size_t)M * sizeof(int32_t), hipMemcpyHostToDevice));
     PMLP_HIP(hipMemcpy(h->d_mid, mid.data(), (size_t)Npad * sizeof(int32_t),
+                       hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(h->d_actn, actn.data(), (size_t)Npad * sizeof(int32_t),
                        hipMemcpyHostToDevice));
     PMLP_HIP(hipMemset(h->W1, 0, w1_bytes));
     PMLP_HIP(hipMemset(h->W2, 0, (size_t)O * Npad * sizeof(float)));

@@ -12,9 +12,12 @@ namespace pmlpk {
 // shapes these kernels accept, so each workgroup of 8 waves copies it into
 // LDS once and then streams its share of the hidden units.  Each wave takes
 // tiles t, t + stride, ... (stride = all waves of the grid), so every wave
-// reaches the end of the tile range and exits.  MFMA operands of the batch
-// come from LDS with ds_read_b128 (row stride chosen so 16 consecutive rows
-// hit distinct banks); operands of the big matrix come from global memory.
+// reaches the end of the tile range and exits.  The batch is stored in LDS
+// in MFMA-operand order: for each (16-row tile i, 16-wide k chunk c) one
+// block of 64 x 16 bytes whose slot l holds the four k values lane l feeds
+// to the MFMA, so every ds_read_b128 reads one contiguous 1 KB block (no
+// bank conflicts whatever the lane grouping).  Operands of the big matrix
+// come from global memory.
 // ---------------------------------------------------------------------------
 
 static constexpr int kLdsBlock = 512;
@@ -52,23 +55,32 @@ __device__ __forceinline__ void fwd_lds_load(f32x4 (&pc)[kKCMax], float (&pt)[3]
 template <int TQ>
 __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds(FwdLdsArgs a) {
   extern __shared__ float lds[];
-  const int K = a.K, SQ = a.SQ, K4 = K >> 2;
-  for (int idx = threadIdx.x; idx < 16 * TQ * K4; idx += kLdsBlock) {
-    const int row = idx / K4;
-    const int c4 = idx - row * K4;
-    *(f32x4*)(lds + row * SQ + 4 * c4) = *(const f32x4*)(a.Xp + (int64_t)row * K + 4 * c4);
+  const int K = a.K;
+  const int nch = K >> 4, tr = (K & 15) >> 2;
+  // full chunks: float4 slot ((i*nch + c)*64 + l) = Xp[16i + l%16][16c + 4(l/16) .. +3]
+  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / nch, c = rest - (rest / nch) * nch;
+    *(f32x4*)(lds + 4 * slot) =
+        *(const f32x4*)(a.Xp + (int64_t)(16 * i + (l & 15)) * K + 16 * c + 4 * (l >> 4));
+  }
+  // remainder: float slot T0 + (i*tr + s)*64 + l = Xp[16i + l%16][16nch + 4s + l/16]
+  const int T0 = TQ * nch * 256;
+  for (int slot = threadIdx.x; slot < TQ * tr * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / tr, s = rest - (rest / tr) * tr;
+    lds[T0 + slot] = a.Xp[(int64_t)(16 * i + (l & 15)) * K + 16 * nch + 4 * s + (l >> 4)];
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int li = lane & 15, lk = lane >> 4;
-  const int nch = K >> 4, tr = (K & 15) >> 2;
   const int64_t T = (a.N + 15) >> 4;
   const int64_t tstride = (int64_t)gridDim.x * kLdsWaves;
   int64_t t = (int64_t)blockIdx.x * kLdsWaves + wave;
   if (t >= T) return;
-  const float* qbase = lds + li * SQ + 4 * lk;        // + 16*i*SQ + 16*c
-  const float* qtail = lds + li * SQ + 16 * nch + lk;  // + 16*i*SQ + 4*s
+  const f32x4* qbase = (const f32x4*)lds + lane;  // + (i*nch + c)*64
+  const float* qtail = lds + T0 + lane;            // + (i*tr + s)*64
   f32x4 pc[kKCMax];
   float pt[3];
   fwd_lds_load(pc, pt, a.W1, t, a.N, K, nch, li, lk);
@@ -87,7 +99,7 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds(FwdLdsArgs a) {
         // one LDS operand at a time; the four steps accumulate back to back
 #pragma unroll
         for (int i = 0; i < TQ; ++i) {
-          const f32x4 q = *(const f32x4*)(qbase + 16 * i * SQ + 16 * c);
+          const f32x4 q = qbase[(i * nch + c) * 64];
 #pragma unroll
           for (int s = 0; s < 4; ++s)
             acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[s], pc[c][s], acc[i], 0, 0, 0);
@@ -99,7 +111,7 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds(FwdLdsArgs a) {
       if (s < tr) {
 #pragma unroll
         for (int i = 0; i < TQ; ++i)
-          acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(qtail[16 * i * SQ + 4 * s], pt[s], acc[i],
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(qtail[(i * tr + s) * 64], pt[s], acc[i],
                                                         0, 0, 0);
       }
     }
@@ -123,191 +135,185 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds(FwdLdsArgs a) {
 //   dW1[n][f] = sum_b dZ[n][b] X[b][f]                      (MFMA, K = batch)
 //   dW2[o][n] = sum_b G[m][b][o] act(Z[n][b])
 //   W1 -= lr dW1, W2 -= lr dW2  (or both gradients stored)
-// Lane (li, lk) owns rows p0 + 16j + li and, in each 16-wide batch chunk,
-// the four samples b = c*16 + 4lk .. +3: every dZ element is formed once,
-// in registers, by the lane that feeds it to the MFMA (the backward of the
-// scatter-add is this gather of G by model id, Section 3).  dW2 partial
-// sums stay in registers and are combined over the four lk lanes of a row
-// at the end of the tile; one wave covers all F columns, so each row's dW2
-// comes from exactly one wave.  Z and G chunks are double-buffered in
-// registers (loop body without branches, so wait counts stay exact).
+// Each wave takes tiles of 16 rows; lane (li, lk) owns row t*16 + li and,
+// in each 16-wide batch chunk, the four samples b = c*16 + 4lk .. +3: every
+// dZ element is formed once, in registers, by the lane that feeds it to the
+// MFMA (the backward of the scatter-add is this gather of G by model id,
+// Section 3).  dW2 partial sums stay in registers and are combined over the
+// four lk lanes of a row at the end of the tile; one wave covers all F
+// columns, so each row's dW2 comes from exactly one wave.  The tile's W1
+// strip is loaded before its chunks, so the update at the end of the tile
+// does not wait on memory.
 // ---------------------------------------------------------------------------
 
-template <int TP, int OM>
-__device__ __forceinline__ void bwdl_load(f32x4 (&cz)[TP], f32x4 (&cg)[TP][OM],
-                                          const float* const (&zrow)[TP],
-                                          const float* const (&grow)[TP], int kofs) {
+template <int OM>
+__device__ __forceinline__ void bwdl_load(f32x4& cz, f32x4 (&cg)[OM], const float* zrow,
+                                          const float* grow, int kofs) {
+  cz = *(const f32x4*)(zrow + kofs);
+  // G[m][b .. b+3][0 .. OM-1] is 4*OM consecutive floats (OM == O)
 #pragma unroll
-  for (int j = 0; j < TP; ++j) {
-    cz[j] = *(const f32x4*)(zrow[j] + kofs);
-    // G[m][b .. b+3][0 .. OM-1] is 4*OM consecutive floats (OM == O)
+  for (int v = 0; v < OM; ++v) cg[v] = *(const f32x4*)(grow + kofs * OM + 4 * v);
+}
+
+// One batch chunk of one tile row: dZ = (sum_o G W2) act'(Z) for the lane's
+// four samples, the dW2 partial sums, then the TQ x 4 MFMAs with the batch
+// operand from LDS.  A < 0: each lane dispatches on its own row's id.
+template <int TQ, int OM, int A>
+__device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ], float (&dw)[OM], const f32x4* qptr,
+                                           int qstride, const f32x4& cz, const f32x4 (&cg)[OM],
+                                           const float (&w2)[OM], int arow) {
+  const float* g = (const float*)&cg[0];  // g[s*OM + o] = G[m][b+s][o]
+  float dz[4];
 #pragma unroll
-    for (int v = 0; v < OM; ++v) cg[j][v] = *(const f32x4*)(grow[j] + kofs * OM + 4 * v);
+  for (int s = 0; s < 4; ++s) {
+    float hp;
+    const float h = act_fwd_bwd(A >= 0 ? A : arow, cz[s], &hp);
+    float dh = 0.f;
+#pragma unroll
+    for (int o = 0; o < OM; ++o) {
+      dh = fmaf(g[s * OM + o], w2[o], dh);
+      dw[o] = fmaf(g[s * OM + o], h, dw[o]);
+    }
+    dz[s] = dh * hp;
+  }
+  // one LDS operand at a time; the four steps accumulate back to back
+#pragma unroll
+  for (int i = 0; i < TQ; ++i) {
+    const f32x4 q = qptr[i * qstride];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[s], dz[s], acc[i], 0, 0, 0);
   }
 }
 
-template <int TQ, int TP, int OM>
-__device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ][TP], float (&dw)[TP][OM],
-                                           const float* qptr, int SQ, const f32x4 (&cz)[TP],
-                                           const f32x4 (&cg)[TP][OM],
-                                           const float (&w2)[TP][OM], const int (&arow)[TP],
-                                           int auni) {
-  f32x4 q[TQ];
+// All batch chunks of one tile.  Z and G chunks go through a ring of RING
+// register buffers, loaded RING-1 chunks ahead of their use; chunk indices
+// past the end are clamped to the last chunk (redundant in-bounds loads) so
+// every pass issues the same loads and wait counts stay exact.  The loop is
+// instantiated per activation so that no activation switch sits inside it.
+template <int TQ, int OM, int RING, int A>
+__device__ __forceinline__ void bwdl_tile(f32x4 (&acc)[TQ], float (&dw)[OM], const f32x4* qbase,
+                                          int qstride, int nch, const float* zrow,
+                                          const float* grow, int lk, const float (&w2)[OM],
+                                          int arow) {
+  f32x4 zb[RING], gb[RING][OM];
 #pragma unroll
-  for (int i = 0; i < TQ; ++i) q[i] = *(const f32x4*)(qptr + 16 * i * SQ);
-  float dz[TP][4];
+  for (int r = 0; r < RING - 1; ++r)
+    bwdl_load<OM>(zb[r], gb[r], zrow, grow, 16 * (r < nch ? r : nch - 1) + 4 * lk);
+  for (int c0 = 0; c0 < nch; c0 += RING) {
 #pragma unroll
-  for (int j = 0; j < TP; ++j) {
-    const float* g = (const float*)&cg[j][0];  // g[s*OM + o] = G[m][b+s][o]
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      float hp;
-      // auni >= 0: every row of the tile has this activation (wave-uniform
-      // branch); otherwise each lane dispatches on its own row's id.
-      const float h = auni >= 0 ? act_fwd_bwd(auni, cz[j][s], &hp)
-                                : act_fwd_bwd(arow[j], cz[j][s], &hp);
-      float dh = 0.f;
-#pragma unroll
-      for (int o = 0; o < OM; ++o) {
-        dh = fmaf(g[s * OM + o], w2[j][o], dh);
-        dw[j][o] = fmaf(g[s * OM + o], h, dw[j][o]);
-      }
-      dz[j][s] = dh * hp;
+    for (int r = 0; r < RING; ++r) {
+      const int c = c0 + r;
+      const int cl = c + RING - 1 < nch ? c + RING - 1 : nch - 1;
+      bwdl_load<OM>(zb[(r + RING - 1) % RING], gb[(r + RING - 1) % RING], zrow, grow,
+                    16 * cl + 4 * lk);
+      if (c < nch) bwdl_chunk<TQ, OM, A>(acc, dw, qbase + 64 * c, qstride, zb[r], gb[r], w2, arow);
     }
   }
-#pragma unroll
-  for (int s = 0; s < 4; ++s)
-#pragma unroll
-    for (int i = 0; i < TQ; ++i)
-#pragma unroll
-      for (int j = 0; j < TP; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[i][s], dz[j][s], acc[i][j], 0, 0, 0);
 }
 
-template <int TQ, int TP, int OM, bool GRAD>
+template <int TQ, int OM, int RING>
 __global__ __launch_bounds__(kLdsBlock) void k_bwd_lds(BwdArgs a) {
   extern __shared__ float lds[];
-  const int Bp = a.Bp, SQ = a.SQ, B4 = Bp >> 2;
-  for (int idx = threadIdx.x; idx < 16 * TQ * B4; idx += kLdsBlock) {
-    const int row = idx / B4;
-    const int c4 = idx - row * B4;
-    const f32x4 v = row < a.F4 ? *(const f32x4*)(a.Xt + (int64_t)row * Bp + 4 * c4)
-                               : f32x4{0.f, 0.f, 0.f, 0.f};
-    *(f32x4*)(lds + row * SQ + 4 * c4) = v;
+  const int Bp = a.Bp;
+  const int nch = Bp >> 4;
+  const bool grad = a.dW1 != nullptr;
+  // float4 slot ((i*nch + c)*64 + l) = Xt[16i + l%16][16c + 4(l/16) .. +3] (0 past F4)
+  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / nch, c = rest - (rest / nch) * nch;
+    const int row = 16 * i + (l & 15);
+    *(f32x4*)(lds + 4 * slot) =
+        row < a.F4 ? *(const f32x4*)(a.Xt + (int64_t)row * Bp + 16 * c + 4 * (l >> 4))
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int li = lane & 15, lk = lane >> 4;
-  const int nch = Bp >> 4;
-  const int64_t T = (a.N + 16 * TP - 1) / (16 * TP);
+  const int64_t T = (a.N + 15) >> 4;
   const int64_t tstride = (int64_t)gridDim.x * kLdsWaves;
-  const float* qbase = lds + li * SQ + 4 * lk;  // + 16*i*SQ + 16*c
+  const f32x4* qbase = (const f32x4*)lds + lane;  // + (i*nch + c)*64
+  const int qstride = nch * 64;
   for (int64_t t = (int64_t)blockIdx.x * kLdsWaves + wave; t < T; t += tstride) {
-    const int64_t p0 = t * 16 * TP;
-    const float* zrow[TP];
-    const float* grow[TP];
-    float w2[TP][OM];
-    int arow[TP];
+    const int64_t p = t * 16 + li;          // this lane's row; < Npad
+    const int64_t pc = p < a.N ? p : a.N - 1;
+    const int m = a.mid[pc];
+    const int arow = a.actn[pc];
+    float w2[OM];
 #pragma unroll
-    for (int j = 0; j < TP; ++j) {
-      int64_t p = p0 + 16 * j + li;
-      if (p > a.N - 1) p = a.N - 1;
-      const int m = a.mid[p];
-      arow[j] = a.act[m];
-      zrow[j] = a.Zt + p * Bp;
-      grow[j] = a.G + (int64_t)m * Bp * OM;
+    for (int o = 0; o < OM; ++o) w2[o] = a.W2[(int64_t)o * a.ldw + pc];
+    const float* zrow = a.Zt + pc * Bp;
+    const float* grow = a.G + (int64_t)m * Bp * OM;
+    // W1 strip for the update at the end of the tile
+    f32x4 w1v[TQ];
+    float* orow = a.W1 + p * a.F4;
+    if (!grad) {
 #pragma unroll
-      for (int o = 0; o < OM; ++o) w2[j][o] = a.W2[(int64_t)o * a.ldw + p];
-    }
-    // one activation for the whole tile (the common case: segments are wide)
-    const int a0 = __builtin_amdgcn_readfirstlane(arow[0]);
-    bool same = true;
-#pragma unroll
-    for (int j = 0; j < TP; ++j) same = same && arow[j] == a0;
-    const int auni = __all(same) ? a0 : -1;
-    f32x4 acc[TQ][TP];
-    float dw[TP][OM];
-#pragma unroll
-    for (int i = 0; i < TQ; ++i)
-#pragma unroll
-      for (int j = 0; j < TP; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < TP; ++j)
-#pragma unroll
-      for (int o = 0; o < OM; ++o) dw[j][o] = 0.f;
-    {
-      f32x4 za[TP], ga[TP][OM], zb[TP], gb[TP][OM];
-      bwdl_load<TP, OM>(za, ga, zrow, grow, 4 * lk);
-      int c = 0;
-      for (; c + 2 < nch; c += 2) {
-        bwdl_load<TP, OM>(zb, gb, zrow, grow, (c + 1) * 16 + 4 * lk);
-        __builtin_amdgcn_sched_barrier(0);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow, auni);
-        __builtin_amdgcn_sched_barrier(0);
-        bwdl_load<TP, OM>(za, ga, zrow, grow, (c + 2) * 16 + 4 * lk);
-        __builtin_amdgcn_sched_barrier(0);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * (c + 1), SQ, zb, gb, w2, arow, auni);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      if (c + 1 < nch) {
-        bwdl_load<TP, OM>(zb, gb, zrow, grow, (c + 1) * 16 + 4 * lk);
-        __builtin_amdgcn_sched_barrier(0);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow, auni);
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * (c + 1), SQ, zb, gb, w2, arow, auni);
-      } else {
-        bwdl_chunk<TQ, TP, OM>(acc, dw, qbase + 16 * c, SQ, za, ga, w2, arow, auni);
+      for (int i = 0; i < TQ; ++i) {
+        int q = 16 * i + 4 * lk;
+        if (q > a.F4 - 4) q = a.F4 - 4;  // columns past F4 are never stored
+        w1v[i] = *(const f32x4*)(orow + q);
       }
     }
-    // dW2: combine the four lk lanes of each row; lanes lk == 0 write.
+    f32x4 acc[TQ];
+    float dw[OM];
 #pragma unroll
-    for (int j = 0; j < TP; ++j)
+    for (int i = 0; i < TQ; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int o = 0; o < OM; ++o) {
-        float v = dw[j][o];
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
-        dw[j][o] = v;
-      }
+    for (int o = 0; o < OM; ++o) dw[o] = 0.f;
+    // One activation for the whole tile in the common case (segments are
+    // wide): a single wave-uniform branch selects the instantiated loop.
+    const int a0 = __builtin_amdgcn_readfirstlane(arow);
+    const int auni = __all(arow == a0) ? a0 : -1;
+    switch (auni) {
+      case 0: bwdl_tile<TQ, OM, RING, 0>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 1: bwdl_tile<TQ, OM, RING, 1>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 2: bwdl_tile<TQ, OM, RING, 2>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 3: bwdl_tile<TQ, OM, RING, 3>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 4: bwdl_tile<TQ, OM, RING, 4>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 5: bwdl_tile<TQ, OM, RING, 5>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 6: bwdl_tile<TQ, OM, RING, 6>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 7: bwdl_tile<TQ, OM, RING, 7>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 8: bwdl_tile<TQ, OM, RING, 8>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 9: bwdl_tile<TQ, OM, RING, 9>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      default: bwdl_tile<TQ, OM, RING, -1>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+    }
+    // dW2: combine the four lk lanes of the row; lanes lk == 0 write.
 #pragma unroll
-    for (int j = 0; j < TP; ++j) {
-      const int64_t p = p0 + 16 * j + li;  // < Npad: padded rows absorb the tail
-      if (GRAD) {
-        if (p >= a.N) continue;
+    for (int o = 0; o < OM; ++o) {
+      float v = dw[o];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      dw[o] = v;
+    }
+    if (grad) {
+      if (p < a.N) {
         if (lk == 0)
 #pragma unroll
-          for (int o = 0; o < OM; ++o) a.dW2[(int64_t)o * a.N + p] = dw[j][o];
-        float* orow = a.dW1 + p * a.F;
+          for (int o = 0; o < OM; ++o) a.dW2[(int64_t)o * a.N + p] = dw[o];
+        float* grow1 = a.dW1 + p * a.F;
 #pragma unroll
         for (int i = 0; i < TQ; ++i) {
           const int q = 16 * i + 4 * lk;
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (q + r < a.F) orow[q + r] = acc[i][j][r];
+            if (q + r < a.F) grow1[q + r] = acc[i][r];
         }
-      } else {
-        if (lk == 0)
+      }
+    } else {
+      // padded rows (p >= N) absorb the tail of the last tile
+      if (lk == 0)
 #pragma unroll
-          for (int o = 0; o < OM; ++o)
-            a.W2[(int64_t)o * a.ldw + p] = w2[j][o] - a.lr * dw[j][o];
-        float* orow = a.W1 + p * a.F4;
+        for (int o = 0; o < OM; ++o) a.W2[(int64_t)o * a.ldw + p] = w2[o] - a.lr * dw[o];
 #pragma unroll
-        for (int i = 0; i < TQ; ++i) {
-          const int q = 16 * i + 4 * lk;
-          if (q < a.F4) {
-            f32x4 w = *(f32x4*)(orow + q);
-            w -= a.lr * acc[i][j];
-            *(f32x4*)(orow + q) = w;
-          }
-        }
+      for (int i = 0; i < TQ; ++i) {
+        const int q = 16 * i + 4 * lk;
+        if (q < a.F4) *(f32x4*)(orow + q) = w1v[i] - a.lr * acc[i];
       }
     }
   }
 }
-
-// LDS row stride (floats) for rows of K floats: an odd number of float4
-// per row keeps ds_read_b128 of 16 consecutive rows free of bank conflicts.
-static int lds_stride(int K) { return ((K >> 2) & 1) ? K : K + 4; }
 
 struct DevInfo {
   int cus = 0;
@@ -327,8 +333,9 @@ static DevInfo dev_info() {
 }
 
 template <class Arg>
-static hipError_t launch_persistent(void (*kern)(Arg), size_t lds_bytes, int64_t waves_needed,
-                                    hipStream_t s, const Arg& arg) {
+static hipError_t launch_persistent(void (*kern)(Arg), int nthreads, size_t lds_bytes,
+                                    int64_t waves_needed, hipStream_t s, const Arg& arg) {
+  const int nwaves = nthreads / 64;
   const DevInfo d = dev_info();
   if (d.cus <= 0) return hipErrorNoDevice;
   if (lds_bytes > 65536) {
@@ -339,18 +346,18 @@ static hipError_t launch_persistent(void (*kern)(Arg), size_t lds_bytes, int64_t
   }
   int per_cu = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)kern,
-                                                              kLdsBlock, lds_bytes);
+                                                              nthreads, lds_bytes);
   if (e != hipSuccess) return e;
   if (per_cu < 1) return hipErrorInvalidConfiguration;
   int64_t blocks = (int64_t)d.cus * per_cu;
-  const int64_t need = (waves_needed + kLdsWaves - 1) / kLdsWaves;
+  const int64_t need = (waves_needed + nwaves - 1) / nwaves;
   if (blocks > need) blocks = need;
   if (blocks < 1) blocks = 1;
-  kern<<<(unsigned)blocks, kLdsBlock, lds_bytes, s>>>(arg);
+  kern<<<(unsigned)blocks, nthreads, lds_bytes, s>>>(arg);
   return hipGetLastError();
 }
 
-static size_t fwd_lds_bytes(int32_t Bp, int32_t F4) { return (size_t)Bp * lds_stride(F4) * 4; }
+static size_t fwd_lds_bytes(int32_t Bp, int32_t F4) { return (size_t)Bp * F4 * 4; }
 
 bool fwd_lds_supported(int32_t Bp, int32_t F4) {
   const DevInfo d = dev_info();
@@ -361,16 +368,15 @@ bool fwd_lds_supported(int32_t Bp, int32_t F4) {
 hipError_t launch_fwd_lds(const FwdLdsArgs& a0, hipStream_t s) {
   if (a0.N <= 0) return hipSuccess;
   if (!fwd_lds_supported(a0.Bp, a0.K)) return hipErrorInvalidValue;
-  FwdLdsArgs a = a0;
-  a.SQ = lds_stride(a.K);
+  const FwdLdsArgs& a = a0;
   const size_t lds = fwd_lds_bytes(a.Bp, a.K);
   const int64_t T = (a.N + 15) / 16;
   switch (a.Bp) {
-    case 16: return launch_persistent(k_fwd_lds<1>, lds, T, s, a);
-    case 32: return launch_persistent(k_fwd_lds<2>, lds, T, s, a);
-    case 64: return launch_persistent(k_fwd_lds<4>, lds, T, s, a);
-    case 128: return launch_persistent(k_fwd_lds<8>, lds, T, s, a);
-    default: return launch_persistent(k_fwd_lds<16>, lds, T, s, a);
+    case 16: return launch_persistent(k_fwd_lds<1>, kLdsBlock, lds, T, s, a);
+    case 32: return launch_persistent(k_fwd_lds<2>, kLdsBlock, lds, T, s, a);
+    case 64: return launch_persistent(k_fwd_lds<4>, kLdsBlock, lds, T, s, a);
+    case 128: return launch_persistent(k_fwd_lds<8>, kLdsBlock, lds, T, s, a);
+    default: return launch_persistent(k_fwd_lds<16>, kLdsBlock, lds, T, s, a);
   }
 }
 
@@ -378,9 +384,7 @@ static int bwd_tq(int32_t F4) {
   return F4 <= 16 ? 1 : F4 <= 32 ? 2 : F4 <= 64 ? 4 : F4 <= 112 ? 7 : 8;
 }
 
-static size_t bwd_lds_bytes(int32_t Bp, int32_t F4) {
-  return (size_t)16 * bwd_tq(F4) * lds_stride(Bp) * 4;
-}
+static size_t bwd_lds_bytes(int32_t Bp, int32_t F4) { return (size_t)16 * bwd_tq(F4) * Bp * 4; }
 
 bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O) {
   const DevInfo d = dev_info();
@@ -388,32 +392,30 @@ bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O) {
          bwd_lds_bytes(Bp, F4) <= (size_t)d.lds_max;
 }
 
-template <int TQ, int TP, int OM>
+template <int TQ, int OM>
 static hipError_t bwd_lds_go(const BwdArgs& a, size_t lds, hipStream_t s) {
-  const int64_t T = (a.N + 16 * TP - 1) / (16 * TP);
-  if (a.dW1) return launch_persistent(k_bwd_lds<TQ, TP, OM, true>, lds, T, s, a);
-  return launch_persistent(k_bwd_lds<TQ, TP, OM, false>, lds, T, s, a);
+  // One 16-row tile per wave, 8 waves per workgroup; prefetch depth set by
+  // the size of the per-chunk G buffers.
+  constexpr int RING = OM <= 2 ? 4 : (OM <= 4 ? 3 : 2);
+  const int64_t T = (a.N + 15) / 16;
+  return launch_persistent(k_bwd_lds<TQ, OM, RING>, kLdsBlock, lds, T, s, a);
 }
 
-// Row tiles per wave (TP): two when the per-row G buffers are small (O = 2),
-// one otherwise, which keeps the double-buffered operands in registers.
 template <int OM>
 static hipError_t bwd_lds_by_f(const BwdArgs& a, size_t lds, hipStream_t s) {
-  constexpr int tp = OM >= 4 ? 1 : 2;
   switch (bwd_tq(a.F4)) {
-    case 1: return bwd_lds_go<1, tp, OM>(a, lds, s);
-    case 2: return bwd_lds_go<2, tp, OM>(a, lds, s);
-    case 4: return bwd_lds_go<4, tp, OM>(a, lds, s);
-    case 7: return bwd_lds_go<7, tp, OM>(a, lds, s);
-    default: return bwd_lds_go<8, 1, OM>(a, lds, s);
+    case 1: return bwd_lds_go<1, OM>(a, lds, s);
+    case 2: return bwd_lds_go<2, OM>(a, lds, s);
+    case 4: return bwd_lds_go<4, OM>(a, lds, s);
+    case 7: return bwd_lds_go<7, OM>(a, lds, s);
+    default: return bwd_lds_go<8, OM>(a, lds, s);
   }
 }
 
 hipError_t launch_bwd_lds(const BwdArgs& a0, hipStream_t s) {
   if (a0.N <= 0) return hipSuccess;
   if (!bwd_lds_supported(a0.Bp, a0.F4, a0.O)) return hipErrorInvalidValue;
-  BwdArgs a = a0;
-  a.SQ = lds_stride(a.Bp);
+  const BwdArgs& a = a0;
   const size_t lds = bwd_lds_bytes(a.Bp, a.F4);
   if (a.O == 2) return bwd_lds_by_f<2>(a, lds, s);
   if (a.O == 4) return bwd_lds_by_f<4>(a, lds, s);

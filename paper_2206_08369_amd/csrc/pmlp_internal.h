@@ -66,7 +66,6 @@ struct FwdLdsArgs {
   int64_t N;
   int32_t Bp;
   int32_t K;         // F4
-  int32_t SQ;        // LDS row stride (set by the launcher)
 };
 bool fwd_lds_supported(int32_t Bp, int32_t F4);
 hipError_t launch_fwd_lds(const FwdLdsArgs& a, hipStream_t s);
@@ -77,8 +76,8 @@ struct BwdArgs {
   const float* Zt;   // [Npad][Bp] pre-activations
   const float* G;    // [M][Bp][O] dLoss/dlogits (0 for padded samples)
   const float* Xt;   // [F4][Bp]
-  const int32_t* mid;
-  const int32_t* act;
+  const int32_t* mid;   // [Npad] model of each hidden unit
+  const int32_t* actn;  // [Npad] activation id of each hidden unit
   float* W1;         // [Npad][F4], updated unless dW1 is set
   float* W2;         // [O][ldw], updated unless dW2 is set
   float* dW1;        // gradient mode: [N][F]
@@ -86,7 +85,6 @@ struct BwdArgs {
   int64_t N;
   int64_t ldw;
   int32_t Bp, F, F4, O;
-  int32_t SQ;        // LDS row stride (set by the launcher)
   float lr;
 };
 bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O);
