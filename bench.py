@@ -69,12 +69,21 @@ def load_traffic(kernel: str, workload: str):
         table = json.load(open(path))
     except ValueError:
         return None
-    src = os.path.join(ROOT, "paper_2206_08369_amd", "csrc", "kernels.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     ent = table.get("%s/%s" % (kernel, workload))
-    if not ent or ent.get("kernels_sha") != digest:
+    if not ent or ent.get("kernels_sha") != kernel_source_digest():
         return None
     return ent.get("bytes_per_launch")
+
+
+def kernel_source_digest() -> str:
+    """sha256 (16 hex digits) over the HIP sources and headers of the library."""
+    csrc = os.path.join(ROOT, "paper_2206_08369_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def cpu_baseline(w, hs, acts, X, y, seconds_hint: float):

@@ -212,14 +212,15 @@ __device__ __forceinline__ void bwdl_tile(f32x4 (&acc)[TQ], float (&dw)[OM], con
   }
 }
 
-template <int TQ, int OM, int RING>
-__global__ __launch_bounds__(kLdsBlock) void k_bwd_lds(BwdArgs a) {
+template <int TQ, int OM, int RING, int NT>
+__global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
+  constexpr int NW = NT / 64;
   extern __shared__ float lds[];
   const int Bp = a.Bp;
   const int nch = Bp >> 4;
   const bool grad = a.dW1 != nullptr;
   // float4 slot ((i*nch + c)*64 + l) = Xt[16i + l%16][16c + 4(l/16) .. +3] (0 past F4)
-  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += kLdsBlock) {
+  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += NT) {
     const int l = slot & 63, rest = slot >> 6;
     const int i = rest / nch, c = rest - (rest / nch) * nch;
     const int row = 16 * i + (l & 15);
@@ -232,10 +233,10 @@ __global__ __launch_bounds__(kLdsBlock) void k_bwd_lds(BwdArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int li = lane & 15, lk = lane >> 4;
   const int64_t T = (a.N + 15) >> 4;
-  const int64_t tstride = (int64_t)gridDim.x * kLdsWaves;
+  const int64_t tstride = (int64_t)gridDim.x * NW;
   const f32x4* qbase = (const f32x4*)lds + lane;  // + (i*nch + c)*64
   const int qstride = nch * 64;
-  for (int64_t t = (int64_t)blockIdx.x * kLdsWaves + wave; t < T; t += tstride) {
+  for (int64_t t = (int64_t)blockIdx.x * NW + wave; t < T; t += tstride) {
     const int64_t p = t * 16 + li;          // this lane's row; < Npad
     const int64_t pc = p < a.N ? p : a.N - 1;
     const int m = a.mid[pc];
@@ -394,11 +395,13 @@ bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O) {
 
 template <int TQ, int OM>
 static hipError_t bwd_lds_go(const BwdArgs& a, size_t lds, hipStream_t s) {
-  // One 16-row tile per wave, 8 waves per workgroup; prefetch depth set by
-  // the size of the per-chunk G buffers.
+  // One 16-row tile per wave; 12 waves per workgroup (3 per SIMD) when the
+  // per-chunk G buffers are small, 8 otherwise; prefetch depth set by the
+  // size of those buffers.
   constexpr int RING = OM <= 2 ? 4 : (OM <= 4 ? 3 : 2);
+  constexpr int NT = OM <= 2 && TQ <= 7 ? 768 : 512;
   const int64_t T = (a.N + 15) / 16;
-  return launch_persistent(k_bwd_lds<TQ, OM, RING>, kLdsBlock, lds, T, s, a);
+  return launch_persistent(k_bwd_lds<TQ, OM, RING, NT>, NT, lds, T, s, a);
 }
 
 template <int OM>
