@@ -87,34 +87,41 @@ def kernel_source_digest() -> str:
 
 
 def cpu_baseline(w, hs, acts, X, y, seconds_hint: float):
-    """Oracle (every MLP trained alone, fp64, OpenMP over models) on a
-    strided subset of the models for one batch; the rate is extrapolated to
-    the whole pack by total hidden units (the oracle's cost is linear in
-    each model's width)."""
+    """Oracle (every MLP trained alone, fp64, OpenMP over models) on a bounded
+    sample of the same workload: all models (or every k-th one when a single
+    batch of the whole pack would exceed the time budget) for as many batches
+    as fit in about `seconds_hint` seconds.  The oracle's cost is linear in
+    each model's width, so a strided sample is scaled by total hidden units."""
     import oracle
     oracle.build(force=False)
     cores = len(os.sched_getaffinity(0))
     if os.environ.get("OMP_NUM_THREADS", "").isdigit():
         cores = max(1, min(cores, int(os.environ["OMP_NUM_THREADS"])))
     N = int(hs.sum())
-    # choose the stride so that the sample costs roughly seconds_hint
-    flop_all = (4.0 * w.F + 6.0 * w.O) * N * w.B
-    est_rate = 1.0e9 * cores                    # ~1 GFLOP/s per core, plain loops
-    stride = int(max(1, round(flop_all / (est_rate * seconds_hint))))
+    flop_batch = (4.0 * w.F + 6.0 * w.O) * N * w.B      # forward + backward + update
+    est_rate = 3.5e9 * cores                              # measured order for the plain loops
+    est_batch = flop_batch / est_rate
+    if est_batch <= seconds_hint:
+        stride, nb = 1, int(max(1, min(w.S // w.B, seconds_hint // est_batch)))
+    else:
+        stride, nb = int(np.ceil(est_batch / seconds_hint)), 1
     models = np.arange(0, w.M, stride)
     W1, W2 = oracle.init_params(w.F, w.O, hs[models], 1)   # any weights: cost is data-independent
+    batches = [(k * w.B, w.B) for k in range(nb)]
     t0 = time.perf_counter()
-    oracle.train(hs[models], acts[models], W1, W2, X[:w.B], y[:w.B], [(0, w.B)], w.lr,
-                 nthreads=cores)
+    oracle.train(hs[models], acts[models], W1, W2, X, y, batches, w.lr, nthreads=cores)
     dt = time.perf_counter() - t0
     sub_h = float(hs[models].sum())
-    rate = w.M * w.B / (dt * N / sub_h)
+    rate = w.M * w.B * nb / (dt * N / sub_h)
+    what = ("all %d models" % w.M if stride == 1 else
+            "every %d-th model (%d of %d models, %d of %d hidden units)"
+            % (stride, len(models), w.M, int(sub_h), N))
     return {
         "value": rate, "unit": "model-samples/s", "cores": oracle.max_threads(),
         "kind": "oracle",
-        "sample": "every %d-th model (%d of %d models, %d of %d hidden units), one batch of %d "
-                  "samples, fp64, %.1f s; rate scaled to the full pack by total hidden units"
-                  % (stride, len(models), w.M, int(sub_h), N, w.B, dt),
+        "sample": "%s, %d batch(es) of %d samples, fp64, %.1f s%s"
+                  % (what, nb, w.B, dt, "" if stride == 1 else
+                     "; rate scaled to the full pack by total hidden units"),
     }
 
 
