@@ -7,9 +7,15 @@ result the packed method of Section 3 is constructed to reproduce exactly.
 
 `build()` compiles `pmlp_oracle.c` with gcc into `liboracle.so` next to
 this file; the wrappers below only marshal numpy arrays through ctypes.
+
+`rounding="bf16"` (forward, gradients, train, hidden, dataset_loss) emulates
+the bf16-in / fp32-accumulate variant of the two input-layer products: X,
+W1 and dZ go to fp32 and then to the nearest bfloat16 before they are
+multiplied; all other arithmetic stays fp64.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes as C
 import os
 import subprocess
@@ -61,6 +67,12 @@ def _load():
                                   dbl, P, P, P, P, i32, C.c_int]
         lib.orc_hidden.restype = C.c_int
         lib.orc_hidden.argtypes = [i32, i32, P, P, P, P, i32, P, P]
+        lib.orc_set_input_rounding.restype = C.c_int
+        lib.orc_set_input_rounding.argtypes = [C.c_int]
+        lib.orc_bf16.restype = C.c_float
+        lib.orc_bf16.argtypes = [C.c_float]
+        lib.orc_bf16_array.restype = None
+        lib.orc_bf16_array.argtypes = [P, P, i64]
         lib.orc_dataset_loss.restype = C.c_int
         lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, i64,
                                          i32, P, C.c_int]
@@ -79,6 +91,29 @@ def _c(a, dtype) -> np.ndarray:
 def _check(rc: int, what: str):
     if rc != 0:
         raise RuntimeError("oracle %s failed with code %d" % (what, rc))
+
+
+_ROUNDING = {"exact": 0, "bf16": 1}
+
+
+@contextlib.contextmanager
+def _rounding(mode: str):
+    if mode not in _ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(_ROUNDING))
+    lib = _load()
+    _check(lib.orc_set_input_rounding(_ROUNDING[mode]), "set_input_rounding")
+    try:
+        yield
+    finally:
+        lib.orc_set_input_rounding(0)
+
+
+def bf16_round(x) -> np.ndarray:
+    """Nearest bfloat16 (ties to even) of each fp32 value, as fp32."""
+    a = _c(x, np.float32)
+    out = np.empty_like(a)
+    _load().orc_bf16_array(_p(a), _p(out), a.size)
+    return out
 
 
 def splitmix64(state: int) -> int:
@@ -107,20 +142,22 @@ def init_params(F: int, O: int, hidden_sizes, seed: int) -> Tuple[np.ndarray, np
     return W1, W2
 
 
-def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0) -> np.ndarray:
+def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
+            rounding: str = "exact") -> np.ndarray:
     """logits [B, M, O] in fp64."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     B, F = Xf.shape
     O = W2d.shape[0]
     out = np.empty((B, len(hs), O), np.float64)
-    _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf), B,
-                               _p(out), nthreads), "forward")
+    with _rounding(rounding):
+        _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf), B,
+                                   _p(out), nthreads), "forward")
     return out
 
 
 def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
-              with_allowance: bool = True, nthreads: int = 0):
+              with_allowance: bool = True, nthreads: int = 0, rounding: str = "exact"):
     """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
 
     The gradient is that of sum_m L_m, so each model's slice is the gradient
@@ -133,14 +170,16 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     dW2 = np.empty((O, N), np.float64)
     loss = np.empty(len(hs), np.float64)
     allow = np.empty((N, F), np.float64) if with_allowance else None
-    _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
-                                 _p(yi), B, _p(dW1), _p(dW2), _p(loss), _p(allow),
-                                 float(kink_rel), nthreads), "gradients")
+    with _rounding(rounding):
+        _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
+                                     _p(yi), B, _p(dW1), _p(dW2), _p(loss), _p(allow),
+                                     float(kink_rel), nthreads), "gradients")
     return dW1, dW2, loss, allow
 
 
 def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
-          lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0):
+          lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0,
+          rounding: str = "exact"):
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
@@ -157,14 +196,16 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     W2o = np.full((O, N), np.nan)
     loss = np.full(len(hs), np.nan)
     sel = None if models is None else _c(models, np.int32)
-    _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf), _p(yi),
-                             len(batches), _p(off), _p(ln), float(lr), _p(W1o), _p(W2o),
-                             _p(loss), _p(sel), 0 if sel is None else len(sel), nthreads),
-           "train")
+    with _rounding(rounding):
+        _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
+                                 _p(yi), len(batches), _p(off), _p(ln), float(lr), _p(W1o),
+                                 _p(W2o), _p(loss), _p(sel), 0 if sel is None else len(sel),
+                                 nthreads), "train")
     return W1o, W2o, loss
 
 
-def hidden(hidden_sizes, act_ids, W1, X) -> Tuple[np.ndarray, np.ndarray]:
+def hidden(hidden_sizes, act_ids, W1, X,
+           rounding: str = "exact") -> Tuple[np.ndarray, np.ndarray]:
     """Z = X W1^T and H = act(Z), both [B, N] fp64."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
@@ -172,18 +213,21 @@ def hidden(hidden_sizes, act_ids, W1, X) -> Tuple[np.ndarray, np.ndarray]:
     N = int(hs.sum())
     Z = np.empty((B, N), np.float64)
     H = np.empty((B, N), np.float64)
-    _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B, _p(Z), _p(H)),
-           "hidden")
+    with _rounding(rounding):
+        _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B, _p(Z), _p(H)),
+               "hidden")
     return Z, H
 
 
 def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,
-                 nthreads: int = 0) -> np.ndarray:
+                 nthreads: int = 0, rounding: str = "exact") -> np.ndarray:
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
     S, F = Xf.shape
     O = W2d.shape[0]
     loss = np.empty(len(hs), np.float64)
-    _check(_load().orc_dataset_loss(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
-                                    _p(yi), S, chunk, _p(loss), nthreads), "dataset_loss")
+    with _rounding(rounding):
+        _check(_load().orc_dataset_loss(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d),
+                                        _p(Xf), _p(yi), S, chunk, _p(loss), nthreads),
+               "dataset_loss")
     return loss

@@ -31,6 +31,11 @@
  * model's arithmetic is sequential and independent of the thread count, so
  * results are bitwise reproducible.
  *
+ * Optional operand rounding of the two input-layer products (Z = X W1^T and
+ * dW1 = dZ^T X) emulates the bf16-in / fp32-accumulate variant: X, W1 and
+ * dZ are first taken to fp32 and then to the nearest bfloat16 (ties to
+ * even) before they are multiplied; everything else stays fp64.
+ *
  * Parity pins (see tests/test_oracle_*.py): the Scatter Add worked example of
  * Section 3, the 4-1-2 + 4-2-2 packing example of Section 3, closed forms for
  * W2 = 0, reductions to textbook matrix products (M = 1 identity; all h = 1),
@@ -170,6 +175,48 @@ int orc_init_params(int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes
 }
 
 /* ------------------------------------------------------------------------ */
+/* Operand rounding of the input-layer products.                            */
+/* ------------------------------------------------------------------------ */
+
+/* 0: exact (fp64 products of the given values); 1: bfloat16 operands. */
+static int orc_rounding = 0;
+
+int orc_set_input_rounding(int mode) {
+  if (mode != 0 && mode != 1) return ORC_EINVAL;
+  orc_rounding = mode;
+  return ORC_OK;
+}
+
+/* Nearest bfloat16 of an fp32 value, ties to even.  bfloat16 keeps the
+ * sign, the 8 exponent bits and the top 7 fraction bits of fp32, so the
+ * rounding works on the bit pattern: adding 0x7FFF plus the lowest kept
+ * bit carries into the kept bits exactly when the dropped 16 bits exceed
+ * half an ulp, or equal it with an odd kept part; the carry may run into
+ * the exponent (the next binade, or infinity past the largest finite
+ * bfloat16).  NaNs stay NaN (the quiet bit is set before truncation). */
+float orc_bf16(float x) {
+  uint32_t u;
+  memcpy(&u, &x, sizeof u);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) {
+    u |= 0x00400000u;
+  } else {
+    u += 0x7FFFu + ((u >> 16) & 1u);
+  }
+  u &= 0xFFFF0000u;
+  memcpy(&x, &u, sizeof x);
+  return x;
+}
+
+void orc_bf16_array(const float* in, float* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_bf16(in[i]);
+}
+
+/* An operand of the input-layer products as the selected variant sees it. */
+static double orc_in(double v) {
+  return orc_rounding ? (double)orc_bf16((float)v) : v;
+}
+
+/* ------------------------------------------------------------------------ */
 /* One model's forward / backward on one batch, Section 3 and Section 2.3.  */
 /* ------------------------------------------------------------------------ */
 
@@ -209,7 +256,8 @@ static void orc_model_forward(const orc_scratch* s, int B, const float* X,
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
       double acc = 0.0;
-      for (int f = 0; f < F; ++f) acc += (double)X[(int64_t)b * F + f] * w1[(int64_t)j * F + f];
+      for (int f = 0; f < F; ++f)
+        acc += orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]);
       s->Z[(int64_t)b * h + j] = acc;
       s->H[(int64_t)b * h + j] = orc_act(s->act, acc);
     }
@@ -267,7 +315,8 @@ static void orc_model_backward(const orc_scratch* s, int B, const float* X,
   for (int j = 0; j < h; ++j)
     for (int f = 0; f < F; ++f) {
       double acc = 0.0;
-      for (int b = 0; b < B; ++b) acc += s->dZ[(int64_t)b * h + j] * (double)X[(int64_t)b * F + f];
+      for (int b = 0; b < B; ++b)
+        acc += orc_in(s->dZ[(int64_t)b * h + j]) * orc_in(X[(int64_t)b * F + f]);
       dw1[(int64_t)j * F + f] = acc;
     }
 }
@@ -286,11 +335,13 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
       double mag = 0.0;
-      for (int f = 0; f < F; ++f) mag += fabs((double)X[(int64_t)b * F + f] * w1[(int64_t)j * F + f]);
+      for (int f = 0; f < F; ++f)
+        mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
       double z = s->Z[(int64_t)b * h + j];
       if (fabs(z) <= kink_rel * mag) {
         double d = fabs(s->dH[(int64_t)b * h + j]) * jump;
-        for (int f = 0; f < F; ++f) allow[(int64_t)j * F + f] += d * fabs((double)X[(int64_t)b * F + f]);
+        for (int f = 0; f < F; ++f)
+          allow[(int64_t)j * F + f] += d * fabs(orc_in(X[(int64_t)b * F + f]));
       }
     }
 }
@@ -507,7 +558,7 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
     for (int j = 0; j < hs[m]; ++j, ++n) {
       for (int b = 0; b < B; ++b) {
         double acc = 0.0;
-        for (int f = 0; f < F; ++f) acc += (double)X[(int64_t)b * F + f] * W1[n * F + f];
+        for (int f = 0; f < F; ++f) acc += orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]);
         Z[(int64_t)b * N + n] = acc;
         H[(int64_t)b * N + n] = orc_act(acts[m], acc);
       }
