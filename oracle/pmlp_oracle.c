@@ -346,6 +346,47 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
     }
 }
 
+/* Rounding-tie allowance of the bf16 operand mode.  dZ reaches the dW1
+ * product as the bfloat16 nearest to its fp32 value; an fp32 evaluation of
+ * dZ that is correct to within rounding may sit on the other side of a
+ * bfloat16 rounding midpoint than the fp32 value of the exact dZ, and then
+ * rounds to the neighbouring bfloat16.  When the fp32 value of dZ lies
+ * within tie_rel * mag of a midpoint, with
+ *   mag = sum_o |G[b,o] W2[o,j]| * |act'(Z[b,j])|
+ * (a bound on the size of the terms dZ is computed from), dW1 can move by
+ * at most
+ *   allow[j,f] += (the larger bfloat16 spacing next to dZ) * |X[b,f]|.     */
+static void orc_model_tie_allow(const orc_scratch* s, int B, const float* X,
+                                const double* w2, double* allow, double tie_rel) {
+  const int F = s->F, O = s->O, h = s->h;
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < h; ++j) {
+      const float z32 = (float)s->dZ[(int64_t)b * h + j];
+      if (!(fabsf(z32) > 1e-30f) || isinf(z32)) continue;
+      double mag = 0.0;
+      for (int o = 0; o < O; ++o) mag += fabs(s->G[(int64_t)b * O + o] * w2[(int64_t)o * h + j]);
+      mag *= fabs(orc_act_deriv(s->act, s->Z[(int64_t)b * h + j]));
+      /* the bfloat16 r nearest to z32 and its two neighbours (bit patterns
+       * one unit of the 16-bit pattern apart, same sign) */
+      const float r = orc_bf16(z32);
+      uint32_t u;
+      memcpy(&u, &r, sizeof u);
+      const uint32_t uu = u + 0x10000u, ud = u - 0x10000u;
+      float up, dn;
+      memcpy(&up, &uu, sizeof up);
+      memcpy(&dn, &ud, sizeof dn);
+      const double a = fabs((double)z32), ar = fabs((double)r);
+      const double mid_up = 0.5 * (ar + fabs((double)up));
+      const double mid_dn = 0.5 * (ar + fabs((double)dn));
+      const double dist = fmin(fabs(a - mid_up), fabs(a - mid_dn));
+      if (dist <= tie_rel * mag) {
+        const double gap = fmax(fabs((double)up) - ar, ar - fabs((double)dn));
+        for (int f = 0; f < F; ++f)
+          allow[(int64_t)j * F + f] += gap * fabs(orc_in(X[(int64_t)b * F + f]));
+      }
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Packed-layout helpers: model m owns rows [off_m, off_m+h_m) of W1 [N,F]  */
 /* and columns [off_m, off_m+h_m) of W2 [O,N] (Section 3, Figure 2 layout). */
@@ -435,11 +476,12 @@ int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_
 /* Gradients of L = sum_m L_m on one batch, without an update.  dW1 [N,F],
  * dW2 [O,N], loss [M] (per-model mean cross-entropy).  allow_dW1 [N,F]
  * (may be NULL) receives the kink allowance described above, with
- * kink_rel the relative distance to the kink treated as undetermined. */
+ * kink_rel the relative distance to the kink treated as undetermined, plus
+ * in the bf16 operand mode the rounding-tie allowance with tie_rel. */
 int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
                   const double* W1, const double* W2, const float* X, const int32_t* y,
                   int32_t B, double* dW1, double* dW2, double* loss, double* allow_dW1,
-                  double kink_rel, int nthreads) {
+                  double kink_rel, double tie_rel, int nthreads) {
   if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !y || !dW1 || !dW2 || !loss)
     return ORC_EINVAL;
   int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
@@ -468,6 +510,7 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
       orc_put(N, F, O, off[m], h, g1, g2, dW1, dW2);
       if (al) {
         orc_model_kink_allow(&s, B, X, w1, al, kink_rel);
+        if (orc_rounding) orc_model_tie_allow(&s, B, X, w2, al, tie_rel);
         memcpy(allow_dW1 + off[m] * F, al, sizeof(double) * (size_t)h * F);
       }
     }

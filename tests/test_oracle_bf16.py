@@ -150,3 +150,28 @@ def test_bf16_loss_close_to_exact_loss(orc):
     rel = np.abs(lb - le) / np.abs(le)
     assert rel.max() < 2e-2
     assert rel.max() > 0  # the variant is really different
+
+
+def test_bf16_tie_allowance_covers_the_neighbouring_rounding(orc):
+    """M = 1 identity: perturb the exact dZ by up to tie_rel/2 of its term
+    magnitude before the bfloat16 rounding (what a correct fp32 evaluation
+    may do); the textbook dW1 of the perturbed dZ stays within the
+    allowance, and the allowance is zero for all but a few entries."""
+    hs, acts, W1, W2, X, y = _problem(21, [40], [0], F=9, O=2, B=64)
+    tie_rel = 1e-5
+    Xr = _torch_bf16(X).astype(np.float64)
+    Z = Xr @ _torch_bf16(W1).astype(np.float64).T
+    _, G = _softmax_grad(Z @ W2.astype(np.float64).T, y)
+    dZ = G @ W2.astype(np.float64)
+    mag = np.abs(G) @ np.abs(W2.astype(np.float64))
+    g1, _, _, allow = orc.gradients(hs, acts, W1, W2, X, y, rounding="bf16", tie_rel=tie_rel)
+    rng = np.random.default_rng(4)
+    flipped = 0
+    for trial in range(20):
+        pert = dZ + rng.uniform(-0.5, 0.5, dZ.shape) * tie_rel * mag
+        dZr = _torch_bf16(pert.astype(np.float32)).astype(np.float64)
+        flipped += int(np.sum(dZr != _torch_bf16(dZ.astype(np.float32))))
+        dW1 = dZr.T @ Xr
+        assert np.all(np.abs(dW1 - g1) <= allow + 1e-12 * np.abs(g1).max())
+    assert flipped > 0                       # the perturbation does reach ties
+    assert 0 < np.count_nonzero(allow.sum(axis=1)) < 0.5 * allow.shape[0]
