@@ -35,16 +35,18 @@ PEAK_FP32_MFMA = 157.3         # TFLOP/s, dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0        # TFLOP/s, dense bf16 matrix
 
 
-def kernel_work(name, B, F, N, M, O):
+def kernel_work(name, B, F, N, M, O, precision="fp32"):
     """(bound, algorithmic bytes, algorithmic flops) of one launch.
 
-    Bytes count each tensor the kernel must read or write once (fp32);
-    flops count multiply-adds as two operations."""
+    Bytes count each tensor the kernel must read or write once (fp32, and
+    the bf16 batch copies at 2 bytes in the bf16 mode); flops count
+    multiply-adds as two operations."""
     f4 = 4.0
+    fx = 2.0 if precision == "bf16" else 4.0   # bytes per element of the batch copy
     if name == "gemm_fwd":      # Z = X W1^T: read W1, X; write Z
-        return "mfma", f4 * (N * F + B * F + N * B), 2.0 * B * F * N
+        return "mfma", f4 * (N * F + N * B) + fx * B * F, 2.0 * B * F * N
     if name == "gemm_bwd":      # W1 -= lr dZ^T X: read dZ, X; read+write W1
-        return "mfma", f4 * (N * B + B * F + 2 * N * F), 2.0 * B * F * N
+        return "mfma", f4 * (N * B + 2 * N * F) + fx * B * F, 2.0 * B * F * N
     if name == "m3_fwd":        # read Z, W2; write logits
         return "hbm", f4 * (N * B + O * N + B * M * O), 2.0 * B * O * N
     if name == "m3_bwd":        # read Z, G, W2; write dZ, W2
@@ -55,7 +57,7 @@ def kernel_work(name, B, F, N, M, O):
     if name == "ce":            # read logits, y; write G, loss
         return "hbm", f4 * (2 * B * M * O + B + M), 0.0
     if name == "pack_x":        # read X; write two padded copies
-        return "hbm", f4 * 3 * B * F, 0.0
+        return "hbm", f4 * B * F + 2 * fx * B * F, 0.0
     return "hbm", 0.0, 0.0
 
 
@@ -195,13 +197,13 @@ def main(argv=None):
     for name, (ms, n) in times.items():
         if n == 0:
             continue
-        bound, nbytes, flops = kernel_work(name, w.B, w.F, N, M, w.O)
+        bound, nbytes, flops = kernel_work(name, w.B, w.F, N, M, w.O, args.precision)
         avg = ms / n
         kernels[name] = {"avg_ms": avg, "launches": n,
                          "gbs": nbytes / (avg * 1e-3) / 1e9 if nbytes else None,
                          "tflops": flops / (avg * 1e-3) / 1e12 if flops else None}
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
-    bound, nbytes, flops = kernel_work(dom, w.B, w.F, N, M, w.O)
+    bound, nbytes, flops = kernel_work(dom, w.B, w.F, N, M, w.O, args.precision)
     avg_s = kernels[dom]["avg_ms"] * 1e-3
     if bound == "mfma":
         peak = PEAK_BF16_MFMA if args.precision == "bf16" else PEAK_FP32_MFMA

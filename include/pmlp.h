@@ -97,7 +97,14 @@ int pmlp_destroy(pmlp_t h);
  * the handle was created on. */
 int pmlp_set_stream(pmlp_t h, void* stream);
 
-/* PMLP_FP32 (default) or PMLP_BF16_GEMM. */
+/* Select the arithmetic of the two input-layer products (Section 3 step 1,
+ * Z = X W1^T, and its gradient dW1 = dZ^T X) for all later calls:
+ *   PMLP_FP32 (default): fp32 operands, fp32 accumulation.
+ *   PMLP_BF16_GEMM: X, W1 and dZ are rounded to bf16 (nearest even) as
+ *     the products read them and the products accumulate in fp32; the
+ *     weights, Z, the activations, logits, loss, gradients of W2 and the
+ *     SGD updates stay fp32.  Every shape is supported.
+ * Returns PMLP_EINVAL for any other mode; the handle keeps its mode. */
 int pmlp_set_precision(pmlp_t h, int32_t mode);
 
 /* Forward pass only (Section 3: input-to-hidden product, per-model

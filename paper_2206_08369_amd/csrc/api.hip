@@ -80,6 +80,9 @@ struct pmlp {
   float* Xt = nullptr;
   float* Zt = nullptr;
   float* LG = nullptr;
+  int32_t capBp16 = 0;            // bf16 batch copies (bf16 GEMM mode only)
+  unsigned short* Xp16 = nullptr; // [Bp][bf16_ld(F4)]
+  unsigned short* Xt16 = nullptr; // [F4][bf16_ld(Bp)]
   bool have_loss = false;
   bool lds_kernels = true;  // persistent LDS-resident GEMMs where they apply
 
@@ -110,7 +113,10 @@ void release(pmlp* h) {
   dfree(h->Xt);
   dfree(h->Zt);
   dfree(h->LG);
+  dfree(h->Xp16);
+  dfree(h->Xt16);
   h->capBp = 0;
+  h->capBp16 = 0;
   for (auto& p : h->pending) {
     (void)hipEventDestroy(p.a);
     (void)hipEventDestroy(p.b);
@@ -185,6 +191,27 @@ int ensure_workspace(pmlp* h, int32_t Bp) {
   return PMLP_OK;
 }
 
+// bf16 copies of the batch, allocated on the first bf16-mode call.
+int ensure_workspace_bf16(pmlp* h, int32_t Bp) {
+  if (Bp <= h->capBp16) return PMLP_OK;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  dfree(h->Xp16);
+  dfree(h->Xt16);
+  h->capBp16 = 0;
+  const size_t np = (size_t)Bp * bf16_ld(h->F4) * 2;
+  const size_t nt = (size_t)h->F4 * bf16_ld(Bp) * 2;
+  if (hipMalloc(&h->Xp16, np) != hipSuccess || hipMalloc(&h->Xt16, nt) != hipSuccess) {
+    (void)hipGetLastError();
+    dfree(h->Xp16);
+    dfree(h->Xt16);
+    return fail(PMLP_ENOMEM, "bf16 workspace allocation failed for batch " + std::to_string(Bp));
+  }
+  h->capBp16 = Bp;
+  return PMLP_OK;
+}
+
+bool bf16_mode(const pmlp* h) { return h->precision == PMLP_BF16_GEMM; }
+
 int check_handle(pmlp* h) {
   if (!h) return fail(PMLP_EINVAL, "null handle");
   return PMLP_OK;
@@ -211,6 +238,25 @@ int32_t pad_batch(int32_t B) {
 
 // Batch copy and the input-to-hidden product (Section 3, step 1).
 int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
+  if (bf16_mode(h)) {
+    if (int rc = ensure_workspace_bf16(h, Bp)) return rc;
+    if (int rc = run(h, KID_PACK_X, [&] {
+          return launch_pack_x_bf16(X, B, h->F, Bp, h->F4, h->Xp16, h->Xt16, h->stream);
+        }))
+      return rc;
+    GemmBfArgs g{};
+    g.P = h->W1;
+    g.ldp = h->F4;
+    g.NP = h->N;
+    g.Q = h->Xp16;
+    g.ldq = bf16_ld(h->F4);
+    g.NQ = Bp;
+    g.K = h->F4;
+    g.out = h->Zt;
+    g.ldo = Bp;
+    g.ncols = Bp;
+    return run(h, KID_GEMM_FWD, [&] { return launch_gemm_bf16(g, EPI_STORE, h->stream); });
+  }
   if (int rc = run(h, KID_PACK_X, [&] {
         return launch_pack_x(X, B, h->F, Bp, h->F4, h->Xp, h->Xt, h->stream);
       }))
@@ -237,7 +283,6 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
   g.ldo = Bp;
   g.ncols = Bp;
   g.lr = 0.f;
-  g.bf16 = h->precision == PMLP_BF16_GEMM;
   return run(h, KID_GEMM_FWD, [&] { return launch_gemm(g, EPI_STORE, h->stream); });
 }
 
@@ -265,7 +310,7 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
         return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, h->stream);
       }))
     return rc;
-  if (h->lds_kernels && bwd_lds_supported(Bp, h->F4, h->O)) {
+  if (h->lds_kernels && !bf16_mode(h) && bwd_lds_supported(Bp, h->F4, h->O)) {
     BwdArgs b{};
     b.Zt = h->Zt;
     b.G = h->LG;
@@ -292,6 +337,26 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
                              h->d_act, h->LG, lr, dW2, h->stream);
       }))
     return rc;
+  if (bf16_mode(h)) {
+    GemmBfArgs g{};
+    g.P = h->Zt;  // dZ, rounded to bf16 as it is loaded
+    g.ldp = Bp;
+    g.NP = h->N;
+    g.Q = h->Xt16;
+    g.ldq = bf16_ld(Bp);
+    g.NQ = h->F4;
+    g.K = Bp;
+    g.out = dW1 ? dW1 : h->W1;
+    g.ldo = dW1 ? h->F : h->F4;
+    g.ncols = h->F;
+    g.lr = lr;
+    if (int rc = run(h, KID_GEMM_BWD, [&] {
+          return launch_gemm_bf16(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
+        }))
+      return rc;
+    h->have_loss = true;
+    return PMLP_OK;
+  }
   GemmArgs g{};
   g.P = h->Zt;
   g.ldp = Bp;
@@ -304,7 +369,6 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
   g.ldo = dW1 ? h->F : h->F4;
   g.ncols = h->F;
   g.lr = lr;
-  g.bf16 = h->precision == PMLP_BF16_GEMM;
   if (int rc = run(h, KID_GEMM_BWD, [&] {
         return launch_gemm(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
       }))
@@ -466,7 +530,6 @@ int pmlp_set_stream(pmlp_t h, void* stream) {
 int pmlp_set_precision(pmlp_t h, int32_t mode) {
   if (int rc = check_handle(h)) return rc;
   if (mode != PMLP_FP32 && mode != PMLP_BF16_GEMM) return fail(PMLP_EINVAL, "unknown precision mode");
-  if (mode == PMLP_BF16_GEMM) return fail(PMLP_EINVAL, "the bf16 GEMM variant is not available in this build");
   h->precision = mode;
   return PMLP_OK;
 }

@@ -81,6 +81,39 @@ hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32
   return hipGetLastError();
 }
 
+// bf16 copies of the batch for the bf16-in GEMMs (nearest-even rounding,
+// v_cvt_pk_bf16_f32); padding (b >= B, f >= F, and the row tails up to the
+// 64-element stride) is zero.
+__global__ __launch_bounds__(kBlock) void k_pack_x_bf16(const float* __restrict__ X, int B,
+                                                        int F, int Bp, int F4, int ldp, int ldt,
+                                                        unsigned short* __restrict__ Xp16,
+                                                        unsigned short* __restrict__ Xt16) {
+  const int64_t np = (int64_t)Bp * ldp, nt = (int64_t)F4 * ldt;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < np + nt;
+       i += (int64_t)gridDim.x * kBlock) {
+    int b, f;
+    if (i < np) {
+      b = (int)(i / ldp);
+      f = (int)(i - (int64_t)b * ldp);
+    } else {
+      f = (int)((i - np) / ldt);
+      b = (int)(i - np - (int64_t)f * ldt);
+    }
+    const float v = (b < B && f < F) ? X[(int64_t)b * F + f] : 0.f;
+    const unsigned short u = __builtin_bit_cast(unsigned short, (__bf16)v);
+    if (i < np) Xp16[i] = u;
+    else Xt16[i - np] = u;
+  }
+}
+
+hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
+                              unsigned short* Xp16, unsigned short* Xt16, hipStream_t s) {
+  const int ldp = bf16_ld(F4), ldt = bf16_ld(Bp);
+  k_pack_x_bf16<<<grid_for((int64_t)Bp * ldp + (int64_t)F4 * ldt), kBlock, 0, s>>>(
+      X, B, F, Bp, F4, ldp, ldt, Xp16, Xt16);
+  return hipGetLastError();
+}
+
 __global__ __launch_bounds__(kBlock) void k_fill(float* __restrict__ p, int64_t n, float v) {
   for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * kBlock)

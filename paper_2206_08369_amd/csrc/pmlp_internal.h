@@ -52,10 +52,30 @@ struct GemmArgs {
   int64_t ldo;
   int32_t ncols;   // EPI_GRAD: number of valid q columns
   float lr;
-  int32_t bf16;    // round both operands to bf16 before the products
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
+
+// bf16-in / fp32-accumulate input-layer GEMM:
+// C[p][q] = sum_k bf16(P[p][k]) Q[q][k], epilogues as above.
+struct GemmBfArgs {
+  const float* P;           // [NP][ldp] fp32, rounded to bf16 on load; k < K read
+  int64_t ldp;              // >= K
+  int64_t NP;
+  const unsigned short* Q;  // [NQ][ldq] bf16 bit patterns, zero for K <= k < ldq
+  int64_t ldq;              // multiple of 64, >= K rounded up to 64
+  int32_t NQ;               // multiple of 4
+  int32_t K;                // multiple of 4
+  float* out;
+  int64_t ldo;
+  int32_t ncols;            // EPI_GRAD: number of valid q columns
+  float lr;
+};
+bool gemm_bf16_args_ok(const GemmBfArgs& a);
+hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s);
+
+// Row stride (elements) of the bf16 batch copies: n rounded up to 64.
+inline int32_t bf16_ld(int32_t n) { return (n + 63) & ~63; }
 
 // Persistent forward GEMM with the batch resident in LDS:
 // Zt[p][q] = sum_k W1[p][k] Xp[q][k], p < N, q < Bp (Bp in {16,...,256}).
@@ -96,6 +116,12 @@ hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float
 
 hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
                          float* Xp, float* Xt, hipStream_t s);
+
+// bf16 copies of the batch (round to nearest even), zero padded:
+//   Xp16 [Bp][bf16_ld(F4)]  (operand of Z = X W1^T)
+//   Xt16 [F4][bf16_ld(Bp)]  (operand of dW1)
+hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
+                              unsigned short* Xp16, unsigned short* Xt16, hipStream_t s);
 
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
