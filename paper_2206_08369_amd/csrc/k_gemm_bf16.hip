@@ -40,8 +40,6 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kKs = 32;  // k per pipeline stage
-
 __device__ __forceinline__ u32x4 pack_bf16x8(const f32x4& a, const f32x4& b) {
   bf16x8 r;
   r[0] = (__bf16)a[0];
@@ -55,17 +53,21 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const f32x4& a, const f32x4& b) {
   return __builtin_bit_cast(u32x4, r);
 }
 
-template <int TP, int TQ, int WP, int WQ, int EPI>
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, int EPI>
 __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   constexpr int NT = 64 * WP * WQ;
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
-  // (row, half) pairs per thread; with fewer pairs than threads the last
-  // waves of the workgroup skip the load (a wave-uniform condition)
-  constexpr int LP = (2 * MP + NT - 1) / NT, LQ = (2 * MQ + NT - 1) / NT;
-  static_assert((2 * MP) % NT == 0 || 2 * MP < NT, "loader shape");
-  static_assert((2 * MQ) % NT == 0 || 2 * MQ < NT, "loader shape");
-  static_assert((2 * MP) % 64 == 0 && (2 * MQ) % 64 == 0, "loader shape");
-  constexpr int PS = MP * 4, QS = MQ * 4;  // 16-byte slots per stage
+  constexpr int KH = KS / 2;   // k owned by one lane half of an MFMA operand
+  constexpr int NS = KS / 16;  // MFMA k-steps per stage
+  // Loader: consecutive lanes read consecutive 16-byte chunks of one row, so
+  // one wave load covers whole cache lines of a few rows.  P chunks are four
+  // fp32 (half of one lane's 8-k bf16 operand entry), Q chunks eight bf16.
+  constexpr int CP = KS / 4, CQ = KS / 8;  // chunks per row and stage
+  constexpr int LP = (MP * CP + NT - 1) / NT, LQ = (MQ * CQ + NT - 1) / NT;
+  static_assert((MP * CP) % NT == 0 || MP * CP < NT, "loader shape");
+  static_assert((MQ * CQ) % NT == 0 || MQ * CQ < NT, "loader shape");
+  static_assert((MP * CP) % 64 == 0 && (MQ * CQ) % 64 == 0, "loader shape");
+  constexpr int PS = MP * 2 * NS, QS = MQ * 2 * NS;  // 16-byte entries per stage
   __shared__ u32x4 lds[2 * (PS + QS)];
 
   const int blk = blockIdx.x;
@@ -79,65 +81,80 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wp = wave / WQ, wq = wave - (wave / WQ) * WQ;
 
-  // Loader: pair e covers row idx/2 of the tile, k half idx%2.
-  const float* prow[LP];
-  int pslot[LP], ph[LP];
+  // LDS position of operand entry (32-row group g, k-step s, MFMA lane l):
+  // fragment (g, s) is 64 consecutive 16-byte entries; inside it lane l's
+  // entry sits at l ^ 8(l/32) ^ 4(s&1), a permutation that keeps the MFMA
+  // reads conflict-free and spreads the loader's scattered writes evenly
+  // over the banks.
+  auto entry = [](int g, int s, int l) {
+    return (g * NS + s) * 64 + (l ^ (8 * (l >> 5)) ^ (4 * (s & 1)));
+  };
+  const float* pptr[LP];
+  int pk[LP], poff[LP];  // k of the chunk within the stage; LDS byte offset
 #pragma unroll
   for (int e = 0; e < LP; ++e) {
-    const int idx = (t + e * NT) % (2 * MP), row = idx >> 1, h = idx & 1;
+    const int idx = (t + e * NT) % (MP * CP), row = idx / CP, c = idx % CP;
     int64_t p = p0 + row;
     if (p > a.NP - 1) p = a.NP - 1;
-    prow[e] = a.P + p * a.ldp + 16 * h;
-    ph[e] = 16 * h;
-    pslot[e] = (row >> 5) * 128 + (row & 31) + 32 * h;
+    const int k = 4 * c, h = k / KH, st = (k % KH) / 8;
+    pptr[e] = a.P + p * a.ldp + k;
+    pk[e] = k;
+    poff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + 8 * (c & 1);
   }
-  const unsigned short* qrow[LQ];
-  int qslot[LQ];
+  const unsigned short* qptr[LQ];
+  int qoff[LQ];
 #pragma unroll
   for (int e = 0; e < LQ; ++e) {
-    const int idx = (t + e * NT) % (2 * MQ), row = idx >> 1, h = idx & 1;
+    const int idx = (t + e * NT) % (MQ * CQ), row = idx / CQ, c = idx % CQ;
     const int q = min(q0 + row, a.NQ - 1);
-    qrow[e] = a.Q + (int64_t)q * a.ldq + 16 * h;
-    qslot[e] = (row >> 5) * 128 + (row & 31) + 32 * h;
+    const int k = 8 * c, h = k / KH, st = (k % KH) / 8;
+    qptr[e] = a.Q + (int64_t)q * a.ldq + k;
+    qoff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16;
   }
 
-  f32x4 pr[LP][4];
-  u32x4 qr[LQ][2];
-  auto load = [&](int kt, bool masked) {
-    const int k0 = kt * kKs;
-#pragma unroll
-    for (int e = 0; e < LP; ++e)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        if (2 * MP < NT && t >= 2 * MP) continue;
-        if (masked) {
-          pr[e][v] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (k0 + ph[e] + 4 * v < a.K) pr[e][v] = *(const f32x4*)(prow[e] + k0 + 4 * v);
-        } else {
-          pr[e][v] = *(const f32x4*)(prow[e] + k0 + 4 * v);
-        }
-      }
-#pragma unroll
-    for (int e = 0; e < LQ; ++e) {
-      if (2 * MQ < NT && t >= 2 * MQ) continue;
-      qr[e][0] = *(const u32x4*)(qrow[e] + k0);
-      qr[e][1] = *(const u32x4*)(qrow[e] + k0 + 8);
-    }
+  // Global loads of one stage into registers, without branches so that the
+  // compiler's wait counts stay exact: the stage index is clamped to the
+  // last stage, and fp32 reads past K (the last stage when K is not a
+  // multiple of KS) are redirected to the start of the row, a finite value
+  // that meets the zero padding of Q.
+  struct Regs {
+    f32x4 p[LP];
+    u32x4 q[LQ];
   };
-  auto store = [&](int sb) {
-    u32x4* ps = lds + sb * (PS + QS);
-    u32x4* qs = ps + PS;
+  const int K = a.K;
+  const int nk = (K + KS - 1) / KS;
+  auto load = [&](Regs& r, int kt) {
+    const int k0 = min(kt, nk - 1) * KS;
 #pragma unroll
     for (int e = 0; e < LP; ++e) {
-      if (2 * MP < NT && t >= 2 * MP) continue;
-      ps[pslot[e]] = pack_bf16x8(pr[e][0], pr[e][1]);
-      ps[pslot[e] + 64] = pack_bf16x8(pr[e][2], pr[e][3]);
+      if (MP * CP < NT && t >= MP * CP) continue;
+      const int off = k0 + pk[e] < K ? k0 : -pk[e];
+      r.p[e] = *(const f32x4*)(pptr[e] + off);
     }
 #pragma unroll
     for (int e = 0; e < LQ; ++e) {
-      if (2 * MQ < NT && t >= 2 * MQ) continue;
-      qs[qslot[e]] = qr[e][0];
-      qs[qslot[e] + 64] = qr[e][1];
+      if (MQ * CQ < NT && t >= MQ * CQ) continue;
+      r.q[e] = *(const u32x4*)(qptr[e] + k0);
+    }
+  };
+  auto store = [&](const Regs& r, int sb) {
+    char* ps = (char*)(lds + sb * (PS + QS));
+    char* qs = ps + PS * 16;
+#pragma unroll
+    for (int e = 0; e < LP; ++e) {
+      if (MP * CP < NT && t >= MP * CP) continue;
+      typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+      bf16x4 v;
+      v[0] = (__bf16)r.p[e][0];
+      v[1] = (__bf16)r.p[e][1];
+      v[2] = (__bf16)r.p[e][2];
+      v[3] = (__bf16)r.p[e][3];
+      *(bf16x4*)(ps + poff[e]) = v;
+    }
+#pragma unroll
+    for (int e = 0; e < LQ; ++e) {
+      if (MQ * CQ < NT && t >= MQ * CQ) continue;
+      *(u32x4*)(qs + qoff[e]) = r.q[e];
     }
   };
 
@@ -150,17 +167,17 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   auto compute = [&](int sb) {
-    const u32x4* ps = lds + sb * (PS + QS) + lane;
+    const u32x4* ps = lds + sb * (PS + QS);
     const u32x4* qs = ps + PS;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int s = 0; s < NS; ++s) {
       bf16x8 pf[TP], qf[TQ];
 #pragma unroll
       for (int j = 0; j < TP; ++j)
-        pf[j] = __builtin_bit_cast(bf16x8, ps[((wp * TP + j) * 2 + s) * 64]);
+        pf[j] = __builtin_bit_cast(bf16x8, ps[entry(wp * TP + j, s, lane)]);
 #pragma unroll
       for (int i = 0; i < TQ; ++i)
-        qf[i] = __builtin_bit_cast(bf16x8, qs[((wq * TQ + i) * 2 + s) * 64]);
+        qf[i] = __builtin_bit_cast(bf16x8, qs[entry(wq * TQ + i, s, lane)]);
 #pragma unroll
       for (int i = 0; i < TQ; ++i)
 #pragma unroll
@@ -169,21 +186,45 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
     }
   };
 
-  const int K = a.K;
-  const int nfull = K / kKs;
-  const int nk = (K + kKs - 1) / kKs;
-  load(0, nfull == 0);
-  store(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int nx = kt + 1;
-    if (nx < nfull) load(nx, false);
-    else if (nx < nk) load(nx, true);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(kt & 1);
-    __builtin_amdgcn_sched_barrier(0);
-    if (nx < nk) store(nx & 1);
+  if (DEPTH == 1) {
+    // stage kt+1 is loaded while stage kt is multiplied
+    Regs r;
+    load(r, 0);
+    store(r, 0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      load(r, kt + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(kt & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 1 >= nk) break;
+      store(r, (kt + 1) & 1);
+      __syncthreads();
+    }
+  } else {
+    // stage kt+2 is loaded while stage kt is multiplied: two stages of
+    // multiplies cover the latency of every load
+    Regs r0, r1;
+    load(r0, 0);
+    store(r0, 0);
+    load(r1, 1);
+    __syncthreads();
+    for (int kt = 0;; kt += 2) {
+      load(r0, kt + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 1 >= nk) break;
+      store(r1, 1);
+      __syncthreads();
+      load(r1, kt + 3);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + 2 >= nk) break;
+      store(r0, 0);
+      __syncthreads();
+    }
   }
 
 #pragma unroll
@@ -214,7 +255,7 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   }
 }
 
-template <int TP, int TQ, int WP, int WQ>
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH>
 hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
   const int64_t npt64 = (a.NP + MP - 1) / MP;
@@ -224,9 +265,15 @@ hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   const int npt = (int)npt64;
   const dim3 grid((unsigned)nblk), block(64 * WP * WQ);
   switch (epi) {
-    case EPI_STORE: k_gemm_bf<TP, TQ, WP, WQ, EPI_STORE><<<grid, block, 0, s>>>(a, npt, nqt); break;
-    case EPI_SGD: k_gemm_bf<TP, TQ, WP, WQ, EPI_SGD><<<grid, block, 0, s>>>(a, npt, nqt); break;
-    default: k_gemm_bf<TP, TQ, WP, WQ, EPI_GRAD><<<grid, block, 0, s>>>(a, npt, nqt); break;
+    case EPI_STORE:
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, EPI_STORE><<<grid, block, 0, s>>>(a, npt, nqt);
+      break;
+    case EPI_SGD:
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, EPI_SGD><<<grid, block, 0, s>>>(a, npt, nqt);
+      break;
+    default:
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, EPI_GRAD><<<grid, block, 0, s>>>(a, npt, nqt);
+      break;
   }
   return hipGetLastError();
 }
@@ -241,8 +288,12 @@ bool gemm_bf16_args_ok(const GemmBfArgs& a) {
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
   if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
   if (!gemm_bf16_args_ok(a)) return hipErrorInvalidValue;
-  if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2>(a, epi, s);
-  return gemm_bf_go<2, 2, 2, 2>(a, epi, s);
+  // q tile no wider than needed for small q; 256 x 256 tiles otherwise (the
+  // largest that keeps the accumulators in registers, and the least operand
+  // traffic per product from L2)
+  if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 32, 2>(a, epi, s);
+  if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 32, 2>(a, epi, s);
+  return gemm_bf_go<4, 2, 2, 4, 32, 2>(a, epi, s);
 }
 
 }  // namespace pmlpk
