@@ -83,6 +83,9 @@ struct pmlp {
   int32_t capBp16 = 0;            // bf16 batch copies (bf16 GEMM mode only)
   unsigned short* Xp16 = nullptr; // [Bp][bf16_ld(F4)]
   unsigned short* Xt16 = nullptr; // [F4][bf16_ld(Bp)]
+  unsigned short* dZ16 = nullptr; // [Npad][Bp] dZ rounded to bf16
+  unsigned short* W1b = nullptr;  // [Npad][bf16_ld(F4)] bf16 of W1 (operand of Z = X W1^T)
+  bool w1b_valid = false;         // W1b equals bf16(W1)
   bool have_loss = false;
   bool lds_kernels = true;  // persistent LDS-resident GEMMs where they apply
 
@@ -115,6 +118,9 @@ void release(pmlp* h) {
   dfree(h->LG);
   dfree(h->Xp16);
   dfree(h->Xt16);
+  dfree(h->dZ16);
+  dfree(h->W1b);
+  h->w1b_valid = false;
   h->capBp = 0;
   h->capBp16 = 0;
   for (auto& p : h->pending) {
@@ -197,13 +203,17 @@ int ensure_workspace_bf16(pmlp* h, int32_t Bp) {
   PMLP_HIP(hipStreamSynchronize(h->stream));
   dfree(h->Xp16);
   dfree(h->Xt16);
+  dfree(h->dZ16);
   h->capBp16 = 0;
   const size_t np = (size_t)Bp * bf16_ld(h->F4) * 2;
   const size_t nt = (size_t)h->F4 * bf16_ld(Bp) * 2;
-  if (hipMalloc(&h->Xp16, np) != hipSuccess || hipMalloc(&h->Xt16, nt) != hipSuccess) {
+  const size_t nd = (size_t)h->Npad * Bp * 2;
+  if (hipMalloc(&h->Xp16, np) != hipSuccess || hipMalloc(&h->Xt16, nt) != hipSuccess ||
+      hipMalloc(&h->dZ16, nd) != hipSuccess) {
     (void)hipGetLastError();
     dfree(h->Xp16);
     dfree(h->Xt16);
+    dfree(h->dZ16);
     return fail(PMLP_ENOMEM, "bf16 workspace allocation failed for batch " + std::to_string(Bp));
   }
   h->capBp16 = Bp;
@@ -211,6 +221,30 @@ int ensure_workspace_bf16(pmlp* h, int32_t Bp) {
 }
 
 bool bf16_mode(const pmlp* h) { return h->precision == PMLP_BF16_GEMM; }
+
+// The bf16 copy of W1 read by the bf16 input-to-hidden product: allocated
+// on first use, rebuilt whenever W1 changed outside a bf16-mode SGD step
+// (whose update epilogue keeps it current).
+int ensure_w1b(pmlp* h) {
+  if (!h->W1b) {
+    const size_t n = (size_t)h->Npad * bf16_ld(h->F4) * 2;
+    if (hipMalloc(&h->W1b, n) != hipSuccess) {
+      (void)hipGetLastError();
+      h->W1b = nullptr;
+      return fail(PMLP_ENOMEM, "bf16 weight copy allocation failed (" +
+                                   std::to_string(n >> 20) + " MiB)");
+    }
+    h->w1b_valid = false;
+  }
+  if (!h->w1b_valid) {
+    if (int rc = run(h, KID_AUX, [&] {
+          return launch_w1_to_bf16(h->W1, h->Npad, h->F4, h->W1b, bf16_ld(h->F4), h->stream);
+        }))
+      return rc;
+    h->w1b_valid = true;
+  }
+  return PMLP_OK;
+}
 
 int check_handle(pmlp* h) {
   if (!h) return fail(PMLP_EINVAL, "null handle");
@@ -240,13 +274,15 @@ int32_t pad_batch(int32_t B) {
 int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
   if (bf16_mode(h)) {
     if (int rc = ensure_workspace_bf16(h, Bp)) return rc;
+    if (int rc = ensure_w1b(h)) return rc;
     if (int rc = run(h, KID_PACK_X, [&] {
           return launch_pack_x_bf16(X, B, h->F, Bp, h->F4, h->Xp16, h->Xt16, h->stream);
         }))
       return rc;
     GemmBfArgs g{};
-    g.P = h->W1;
-    g.ldp = h->F4;
+    g.Pb = h->W1b;
+    g.ldp = bf16_ld(h->F4);
+    g.kp = bf16_ld(h->F4);  // zero past F4
     g.NP = h->N;
     g.Q = h->Xp16;
     g.ldq = bf16_ld(h->F4);
@@ -294,6 +330,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
   if (int rc = use_device(h)) return rc;
   if (int rc = ensure_workspace(h, Bp)) return rc;
   if (int rc = forward_hidden(h, X, B, Bp)) return rc;
+  // an fp32-mode update leaves the bf16 copy of W1 behind
+  if (!bf16_mode(h) && !dW1) h->w1b_valid = false;
   if (h->has_split) {
     if (int rc = run(h, KID_AUX, [&] {
           return launch_fill(h->LG, (int64_t)h->M * Bp * h->O, 0.f, h->stream);
@@ -333,14 +371,16 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
     return PMLP_OK;
   }
   if (int rc = run(h, KID_M3_BWD, [&] {
-        return launch_m3_bwd(h->Zt, Bp, h->W2, h->N, h->Npad, h->O, h->d_mid, h->d_seg_off,
+        return launch_m3_bwd(h->Zt, bf16_mode(h) ? h->dZ16 : nullptr, Bp, h->W2, h->N, h->Npad,
+                             h->O, h->d_mid, h->d_seg_off,
                              h->d_act, h->LG, lr, dW2, h->stream);
       }))
     return rc;
   if (bf16_mode(h)) {
     GemmBfArgs g{};
-    g.P = h->Zt;  // dZ, rounded to bf16 as it is loaded
+    g.Pb = h->dZ16;
     g.ldp = Bp;
+    g.kp = Bp;
     g.NP = h->N;
     g.Q = h->Xt16;
     g.ldq = bf16_ld(Bp);
@@ -350,6 +390,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
     g.ldo = dW1 ? h->F : h->F4;
     g.ncols = h->F;
     g.lr = lr;
+    g.outb = dW1 ? nullptr : h->W1b;  // the update keeps the bf16 copy current
+    g.ldob = bf16_ld(h->F4);
     if (int rc = run(h, KID_GEMM_BWD, [&] {
           return launch_gemm_bf16(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
         }))
@@ -614,6 +656,7 @@ int pmlp_set_params(pmlp_t h, const float* W1_host, const float* W2_host) {
   if (int rc = check_handle(h)) return rc;
   if (int rc = use_device(h)) return rc;
   PMLP_HIP(hipStreamSynchronize(h->stream));
+  if (W1_host) h->w1b_valid = false;
   if (W1_host)
     PMLP_HIP(hipMemcpy2D(h->W1, (size_t)h->F4 * sizeof(float), W1_host,
                          (size_t)h->F * sizeof(float), (size_t)h->F * sizeof(float),

@@ -33,11 +33,14 @@
 
 #include "device_common.h"
 
+#include <type_traits>
+
 namespace pmlpk {
 
 namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ u32x4 pack_bf16x8(const f32x4& a, const f32x4& b) {
@@ -53,16 +56,18 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const f32x4& a, const f32x4& b) {
   return __builtin_bit_cast(u32x4, r);
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, int EPI>
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, int EPI>
 __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   constexpr int NT = 64 * WP * WQ;
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
   constexpr int KH = KS / 2;   // k owned by one lane half of an MFMA operand
   constexpr int NS = KS / 16;  // MFMA k-steps per stage
   // Loader: consecutive lanes read consecutive 16-byte chunks of one row, so
-  // one wave load covers whole cache lines of a few rows.  P chunks are four
-  // fp32 (half of one lane's 8-k bf16 operand entry), Q chunks eight bf16.
-  constexpr int CP = KS / 4, CQ = KS / 8;  // chunks per row and stage
+  // one wave load covers whole cache lines of a few rows.  fp32 P chunks are
+  // four fp32 (half of one lane's 8-k bf16 operand entry); bf16 P (PB) and
+  // Q chunks are eight bf16.
+  constexpr int PE = PB ? 8 : 4;           // P elements per chunk
+  constexpr int CP = KS / PE, CQ = KS / 8;  // chunks per row and stage
   constexpr int LP = (MP * CP + NT - 1) / NT, LQ = (MQ * CQ + NT - 1) / NT;
   static_assert((MP * CP) % NT == 0 || MP * CP < NT, "loader shape");
   static_assert((MQ * CQ) % NT == 0 || MQ * CQ < NT, "loader shape");
@@ -89,17 +94,19 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   auto entry = [](int g, int s, int l) {
     return (g * NS + s) * 64 + (l ^ (8 * (l >> 5)) ^ (4 * (s & 1)));
   };
-  const float* pptr[LP];
+  typedef typename std::conditional<PB, unsigned short, float>::type PT;
+  const PT* pbase = PB ? (const PT*)a.Pb : (const PT*)a.P;
+  const PT* pptr[LP];
   int pk[LP], poff[LP];  // k of the chunk within the stage; LDS byte offset
 #pragma unroll
   for (int e = 0; e < LP; ++e) {
     const int idx = (t + e * NT) % (MP * CP), row = idx / CP, c = idx % CP;
     int64_t p = p0 + row;
     if (p > a.NP - 1) p = a.NP - 1;
-    const int k = 4 * c, h = k / KH, st = (k % KH) / 8;
-    pptr[e] = a.P + p * a.ldp + k;
+    const int k = PE * c, h = k / KH, st = (k % KH) / 8;
+    pptr[e] = pbase + p * a.ldp + k;
     pk[e] = k;
-    poff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + 8 * (c & 1);
+    poff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (PB ? 0 : 8 * (c & 1));
   }
   const unsigned short* qptr[LQ];
   int qoff[LQ];
@@ -114,22 +121,22 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
 
   // Global loads of one stage into registers, without branches so that the
   // compiler's wait counts stay exact: the stage index is clamped to the
-  // last stage, and fp32 reads past K (the last stage when K is not a
+  // last stage, and P reads at or past kp (the last stage when kp is not a
   // multiple of KS) are redirected to the start of the row, a finite value
   // that meets the zero padding of Q.
   struct Regs {
-    f32x4 p[LP];
+    u32x4 p[LP];
     u32x4 q[LQ];
   };
-  const int K = a.K;
+  const int K = a.K, kp = a.kp;
   const int nk = (K + KS - 1) / KS;
   auto load = [&](Regs& r, int kt) {
     const int k0 = min(kt, nk - 1) * KS;
 #pragma unroll
     for (int e = 0; e < LP; ++e) {
       if (MP * CP < NT && t >= MP * CP) continue;
-      const int off = k0 + pk[e] < K ? k0 : -pk[e];
-      r.p[e] = *(const f32x4*)(pptr[e] + off);
+      const int off = k0 + pk[e] < kp ? k0 : -pk[e];
+      r.p[e] = *(const u32x4*)(pptr[e] + off);
     }
 #pragma unroll
     for (int e = 0; e < LQ; ++e) {
@@ -143,13 +150,17 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
 #pragma unroll
     for (int e = 0; e < LP; ++e) {
       if (MP * CP < NT && t >= MP * CP) continue;
-      typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-      bf16x4 v;
-      v[0] = (__bf16)r.p[e][0];
-      v[1] = (__bf16)r.p[e][1];
-      v[2] = (__bf16)r.p[e][2];
-      v[3] = (__bf16)r.p[e][3];
-      *(bf16x4*)(ps + poff[e]) = v;
+      if (PB) {
+        *(u32x4*)(ps + poff[e]) = r.p[e];
+      } else {
+        const f32x4 f = __builtin_bit_cast(f32x4, r.p[e]);
+        bf16x4 v;
+        v[0] = (__bf16)f[0];
+        v[1] = (__bf16)f[1];
+        v[2] = (__bf16)f[2];
+        v[3] = (__bf16)f[3];
+        *(bf16x4*)(ps + poff[e]) = v;
+      }
     }
 #pragma unroll
     for (int e = 0; e < LQ; ++e) {
@@ -227,35 +238,58 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
     }
   }
 
+  // Epilogue: each 32 x 32 block goes through a per-wave LDS scratch so that
+  // eight consecutive lanes hold one row's 32 consecutive q; every store (and
+  // the read of the SGD update) then covers whole 128-byte row segments
+  // instead of 16 bytes of 32 rows.  Scratch rows are padded to 36 floats:
+  // the column writes of the MFMA layout and the row reads both stay within
+  // two lanes per bank.
+  constexpr int LDT = 36;
+  static_assert(NT / 64 * 32 * LDT * 4 <= (int)sizeof(lds), "epilogue scratch");
+  float* scr = (float*)lds + wave * (32 * LDT);
+  __syncthreads();  // every wave is done with the operand stages
 #pragma unroll
-  for (int j = 0; j < TP; ++j) {
-    const int64_t p = p0 + 32 * (wp * TP + j) + (lane & 31);
-    if (p >= a.NP) continue;
-    float* orow = a.out + p * a.ldo;
+  for (int j = 0; j < TP; ++j)
 #pragma unroll
-    for (int i = 0; i < TQ; ++i)
+    for (int i = 0; i < TQ; ++i) {
 #pragma unroll
       for (int i4 = 0; i4 < 4; ++i4) {
-        const int q = q0 + 32 * (wq * TQ + i) + 8 * i4 + 4 * (lane >> 5);
-        if (q >= a.NQ) continue;
         const f32x4 v = {acc[i][j][4 * i4], acc[i][j][4 * i4 + 1], acc[i][j][4 * i4 + 2],
                          acc[i][j][4 * i4 + 3]};
+        *(f32x4*)(scr + (lane & 31) * LDT + 8 * i4 + 4 * (lane >> 5)) = v;
+      }
+      __syncthreads();
+      const int64_t pb = p0 + 32 * (wp * TP + j);
+      const int qb = q0 + 32 * (wq * TQ + i);
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {
+        const int r = 8 * pass + (lane >> 3), c4 = 4 * (lane & 7);
+        const f32x4 v = *(const f32x4*)(scr + r * LDT + c4);
+        const int64_t p = pb + r;
+        const int q = qb + c4;
+        if (p >= a.NP || q >= a.NQ) continue;
+        float* o = a.out + p * a.ldo + q;
         if (EPI == EPI_STORE) {
-          *(f32x4*)(orow + q) = v;
+          *(f32x4*)o = v;
         } else if (EPI == EPI_SGD) {
-          f32x4 w = *(f32x4*)(orow + q);
+          f32x4 w = *(f32x4*)o;
           w -= a.lr * v;
-          *(f32x4*)(orow + q) = w;
+          *(f32x4*)o = w;
+          if (a.outb) {
+            const bf16x4 wb = {(__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};
+            *(bf16x4*)(a.outb + p * a.ldob + q) = wb;
+          }
         } else {
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (q + r < a.ncols) orow[q + r] = v[r];
+          for (int e = 0; e < 4; ++e)
+            if (q + e < a.ncols) o[e] = v[e];
         }
       }
-  }
+      __syncthreads();
+    }
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH>
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB>
 hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
   const int64_t npt64 = (a.NP + MP - 1) / MP;
@@ -266,13 +300,13 @@ hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   const dim3 grid((unsigned)nblk), block(64 * WP * WQ);
   switch (epi) {
     case EPI_STORE:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, EPI_STORE><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_STORE><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
     case EPI_SGD:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, EPI_SGD><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_SGD><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
     default:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, EPI_GRAD><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_GRAD><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
   }
   return hipGetLastError();
@@ -281,8 +315,16 @@ hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
 }  // namespace
 
 bool gemm_bf16_args_ok(const GemmBfArgs& a) {
-  return a.NP > 0 && a.NQ > 0 && a.K > 0 && a.K % 4 == 0 && a.NQ % 4 == 0 && a.ldp >= a.K &&
-         a.ldq % 64 == 0 && a.ldq >= ((a.K + 63) / 64) * 64;
+  const int pe = a.Pb ? 8 : 4;
+  return a.NP > 0 && a.NQ > 0 && a.K > 0 && a.K % 4 == 0 && a.NQ % 4 == 0 &&
+         (a.P != nullptr) != (a.Pb != nullptr) && a.kp > 0 && a.kp % pe == 0 &&
+         a.ldp >= a.kp && a.ldq % 64 == 0 && a.ldq >= ((a.K + 63) / 64) * 64;
+}
+
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH>
+hipError_t gemm_bf_p(const GemmBfArgs& a, int epi, hipStream_t s) {
+  if (a.Pb) return gemm_bf_go<TP, TQ, WP, WQ, KS, DEPTH, true>(a, epi, s);
+  return gemm_bf_go<TP, TQ, WP, WQ, KS, DEPTH, false>(a, epi, s);
 }
 
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
@@ -291,9 +333,9 @@ hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
   // q tile no wider than needed for small q; 256 x 256 tiles otherwise (the
   // largest that keeps the accumulators in registers, and the least operand
   // traffic per product from L2)
-  if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 32, 2>(a, epi, s);
-  if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 32, 2>(a, epi, s);
-  return gemm_bf_go<4, 2, 2, 4, 32, 2>(a, epi, s);
+  if (a.NQ <= 64) return gemm_bf_p<4, 1, 2, 2, 32, 2>(a, epi, s);
+  if (a.NQ <= 128) return gemm_bf_p<2, 2, 2, 2, 32, 2>(a, epi, s);
+  return gemm_bf_p<4, 2, 2, 4, 32, 2>(a, epi, s);
 }
 
 }  // namespace pmlpk

@@ -173,7 +173,8 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
 static constexpr int kT5 = 256;
 
 template <int OM, int A>
-__device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, int Bp, int bl, bool bvalid,
+__device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, unsigned short* __restrict__ dZ16,
+                                            int Bp, int bl, bool bvalid,
                                             const float* __restrict__ W2, int64_t ldw, int O,
                                             int64_t nbeg, int64_t nend, int g, int NG, int LG,
                                             int pp, const float (&gr)[4][OM],
@@ -211,7 +212,15 @@ __device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, int Bp, int 
 #pragma unroll
         for (int o = 0; o < OM; ++o) dw[o] = fmaf(gr[i][o], h, dw[o]);
       }
-      if (bvalid) *(f32x4*)(Zt + n * Bp + bl) = dz;
+      if (bvalid) {
+        if (dZ16) {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          const bf16x4 v = {(__bf16)dz[0], (__bf16)dz[1], (__bf16)dz[2], (__bf16)dz[3]};
+          *(bf16x4*)(dZ16 + n * Bp + bl) = v;
+        } else {
+          *(f32x4*)(Zt + n * Bp + bl) = dz;
+        }
+      }
 #pragma unroll
       for (int o = 0; o < OM; ++o) dw[o] = group_sum_to_last(dw[o], LG);
       if (pp == LG - 1) {
@@ -226,10 +235,10 @@ __device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, int Bp, int 
 
 template <int OM, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_m3_bwd(
-    float* __restrict__ Zt, int Bp, float* __restrict__ W2, int64_t N, int64_t ldw, int O,
-    const int32_t* __restrict__ mid, const int64_t* __restrict__ seg_off,
-    const int32_t* __restrict__ act, const float* __restrict__ G, int LG, int slots, float lr,
-    float* __restrict__ dW2) {
+    float* __restrict__ Zt, unsigned short* __restrict__ dZ16, int Bp, float* __restrict__ W2,
+    int64_t N, int64_t ldw, int O, const int32_t* __restrict__ mid,
+    const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
+    const float* __restrict__ G, int LG, int slots, float lr, float* __restrict__ dW2) {
   __shared__ float lds[4 * kT5 * OM];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -262,16 +271,16 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
           }
         const bool first = slot == 0;
         switch (a) {
-          case 0: bwd_segment<OM, 0>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 1: bwd_segment<OM, 1>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 2: bwd_segment<OM, 2>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 3: bwd_segment<OM, 3>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 4: bwd_segment<OM, 4>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 5: bwd_segment<OM, 5>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 6: bwd_segment<OM, 6>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 7: bwd_segment<OM, 7>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 8: bwd_segment<OM, 8>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          default: bwd_segment<OM, 9>(Zt, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 0: bwd_segment<OM, 0>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 1: bwd_segment<OM, 1>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 2: bwd_segment<OM, 2>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 3: bwd_segment<OM, 3>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 4: bwd_segment<OM, 4>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 5: bwd_segment<OM, 5>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 6: bwd_segment<OM, 6>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 7: bwd_segment<OM, 7>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 8: bwd_segment<OM, 8>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          default: bwd_segment<OM, 9>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
         }
         n = se;
         ++m;
@@ -291,9 +300,10 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
 }
 
 template <int OM>
-static void m3_bwd_dispatch(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t ldw, int32_t O,
-                            const int32_t* mid, const int64_t* seg_off, const int32_t* act,
-                            const float* G, float lr, float* dW2, hipStream_t s) {
+static void m3_bwd_dispatch(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
+                            int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
+                            const int32_t* act, const float* G, float lr, float* dW2,
+                            hipStream_t s) {
   int LG = 64;
   const int q = (Bp + 3) / 4;
   if (q < 64) {
@@ -304,21 +314,22 @@ static void m3_bwd_dispatch(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t
   const int64_t waves = (N + kT5 - 1) / kT5;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
   if (dW2)
-    k_m3_bwd<OM, true><<<blocks, kBlock, 0, s>>>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, LG,
-                                                 slots, lr, dW2);
+    k_m3_bwd<OM, true><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act,
+                                                 G, LG, slots, lr, dW2);
   else
-    k_m3_bwd<OM, false><<<blocks, kBlock, 0, s>>>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, LG,
-                                                  slots, lr, dW2);
+    k_m3_bwd<OM, false><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act,
+                                                  G, LG, slots, lr, dW2);
 }
 
-hipError_t launch_m3_bwd(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t ldw, int32_t O,
-                         const int32_t* mid, const int64_t* seg_off, const int32_t* act,
-                         const float* G, float lr, float* dW2, hipStream_t s) {
-  if (O <= 2) m3_bwd_dispatch<2>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else if (O <= 4) m3_bwd_dispatch<4>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else if (O <= 8) m3_bwd_dispatch<8>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else if (O <= 10) m3_bwd_dispatch<10>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else m3_bwd_dispatch<16>(Zt, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
+                         int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
+                         const int32_t* act, const float* G, float lr, float* dW2,
+                         hipStream_t s) {
+  if (O <= 2) m3_bwd_dispatch<2>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else if (O <= 4) m3_bwd_dispatch<4>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else if (O <= 8) m3_bwd_dispatch<8>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else if (O <= 10) m3_bwd_dispatch<10>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+  else m3_bwd_dispatch<16>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
   return hipGetLastError();
 }
 

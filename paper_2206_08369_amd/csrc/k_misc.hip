@@ -114,6 +114,25 @@ hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, 
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(kBlock) void k_w1_to_bf16(const float* __restrict__ W1,
+                                                       int64_t total, int F4, int ldb,
+                                                       unsigned short* __restrict__ W1b) {
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int64_t n = i / ldb;
+    const int c = (int)(i - n * ldb);
+    const float v = c < F4 ? W1[n * F4 + c] : 0.f;
+    W1b[i] = __builtin_bit_cast(unsigned short, (__bf16)v);
+  }
+}
+
+hipError_t launch_w1_to_bf16(const float* W1, int64_t Npad, int32_t F4, unsigned short* W1b,
+                             int32_t ldb, hipStream_t s) {
+  const int64_t total = Npad * ldb;
+  k_w1_to_bf16<<<grid_for(total), kBlock, 0, s>>>(W1, total, F4, ldb, W1b);
+  return hipGetLastError();
+}
+
 __global__ __launch_bounds__(kBlock) void k_fill(float* __restrict__ p, int64_t n, float v) {
   for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * kBlock)

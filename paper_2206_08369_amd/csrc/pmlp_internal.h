@@ -59,8 +59,10 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
 // bf16-in / fp32-accumulate input-layer GEMM:
 // C[p][q] = sum_k bf16(P[p][k]) Q[q][k], epilogues as above.
 struct GemmBfArgs {
-  const float* P;           // [NP][ldp] fp32, rounded to bf16 on load; k < K read
-  int64_t ldp;              // >= K
+  const float* P;           // [NP][ldp] fp32, rounded to bf16 on load, or null and
+  const unsigned short* Pb; // [NP][ldp] bf16 bit patterns
+  int64_t ldp;              // >= kp
+  int32_t kp;               // P columns k < kp are read (finite); later k count as 0
   int64_t NP;
   const unsigned short* Q;  // [NQ][ldq] bf16 bit patterns, zero for K <= k < ldq
   int64_t ldq;              // multiple of 64, >= K rounded up to 64
@@ -70,6 +72,8 @@ struct GemmBfArgs {
   int64_t ldo;
   int32_t ncols;            // EPI_GRAD: number of valid q columns
   float lr;
+  unsigned short* outb;     // EPI_SGD: also store bf16 of the updated values (or null)
+  int64_t ldob;
 };
 bool gemm_bf16_args_ok(const GemmBfArgs& a);
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s);
@@ -120,6 +124,10 @@ hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32
 // bf16 copies of the batch (round to nearest even), zero padded:
 //   Xp16 [Bp][bf16_ld(F4)]  (operand of Z = X W1^T)
 //   Xt16 [F4][bf16_ld(Bp)]  (operand of dW1)
+// W1b [Npad][ldb] = bf16(W1 [Npad][F4]), zero for F4 <= k < ldb.
+hipError_t launch_w1_to_bf16(const float* W1, int64_t Npad, int32_t F4, unsigned short* W1b,
+                             int32_t ldb, hipStream_t s);
+
 hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
                               unsigned short* Xp16, unsigned short* Xt16, hipStream_t s);
 
@@ -131,9 +139,13 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
                      float* loss, int32_t* flag, hipStream_t s);
 
-hipError_t launch_m3_bwd(float* Zt, int32_t Bp, float* W2, int64_t N, int64_t ldw, int32_t O,
-                         const int32_t* mid, const int64_t* seg_off, const int32_t* act,
-                         const float* G, float lr, float* dW2, hipStream_t s);
+// M3 backward + activation derivative: dZ over Zt in place (fp32), or, with
+// dZ16 set, as bf16 into dZ16 [Npad][Bp] leaving Zt unchanged; then the W2
+// update (dW2 null) or the dW2 store.
+hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
+                         int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
+                         const int32_t* act, const float* G, float lr, float* dW2,
+                         hipStream_t s);
 
 hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              const int32_t* mid, const int32_t* act, float* Z, float* H,

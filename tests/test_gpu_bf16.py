@@ -208,3 +208,32 @@ def test_bf16_full_size_w10k_f1000_on_sampled_models(pm, orc, torch):
     assert err_rows(T1[rows], O1, shs).max() <= TOL_STEP
     assert err_cols(T2[:, rows], O2, shs).max() <= TOL_STEP
     net.close()
+
+
+def test_bf16_weight_copy_follows_every_update(pm, torch):
+    """The bf16 operand copy of W1 tracks W1 through fp32-mode steps, bf16-mode
+    steps and set_params: forward results equal, bit for bit, those of a fresh
+    bf16 handle given the same weights."""
+    hs, acts, F, O, B, X, y = case_inputs("f100_b250")
+    Xd, yd = dev(torch, X), dev(torch, y)
+    net = pm.PackedMLP(F, O, hs, acts, seed=26)
+    ref = bf16_net(pm, F, O, hs, acts, seed=27)
+
+    def same_as_fresh():
+        W1, W2 = net.get_params()
+        ref.set_params(W1, W2)
+        return np.array_equal(net.forward(Xd).cpu().numpy(), ref.forward(Xd).cpu().numpy())
+
+    net.set_precision(pm.PMLP_BF16_GEMM)
+    assert same_as_fresh()
+    net.set_precision(pm.PMLP_FP32)
+    net.train_step(Xd, yd, 0.1)                 # fp32 update
+    net.set_precision(pm.PMLP_BF16_GEMM)
+    assert same_as_fresh()
+    net.train_step(Xd, yd, 0.1)                 # bf16 update (copy kept by the update)
+    assert same_as_fresh()
+    W1, W2 = net.get_params()
+    net.set_params(W1 * 0.5, W2)                # host update
+    assert same_as_fresh()
+    net.close()
+    ref.close()
