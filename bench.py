@@ -38,30 +38,39 @@ PEAK_BF16_MFMA = 2500.0        # TFLOP/s, dense bf16 matrix
 def kernel_work(name, B, F, N, M, O, precision="fp32"):
     """(bound, algorithmic bytes, algorithmic flops) of one launch.
 
-    Bytes count each tensor the kernel must read or write once (fp32, and
-    the bf16 batch copies at 2 bytes in the bf16 mode); flops count
-    multiply-adds as two operations."""
+    Bytes count each tensor the kernel must read or write once, at the width
+    the path stores it: fp32, except in the bf16 mode the batch copies, the
+    bf16 copy of W1 (read by the input-to-hidden product, rewritten by the
+    update) and dZ (written by the M3 backward, read by the dW1 product);
+    flops count multiply-adds as two operations."""
     f4 = 4.0
-    fx = 2.0 if precision == "bf16" else 4.0   # bytes per element of the batch copy
-    if name == "gemm_fwd":      # Z = X W1^T: read W1, X; write Z
-        return "mfma", f4 * (N * F + N * B) + fx * B * F, 2.0 * B * F * N
-    if name == "gemm_bwd":      # W1 -= lr dZ^T X: read dZ, X; read+write W1
-        return "mfma", f4 * (N * B + 2 * N * F) + fx * B * F, 2.0 * B * F * N
-    if name == "m3_fwd":        # read Z, W2; write logits
+    bf = precision == "bf16"
+    fx = 2.0 if bf else 4.0      # bytes per element of the batch copy
+    if name == "gemm_fwd":       # Z = X W1^T: read W1 (bf16 copy in bf16 mode), X; write Z
+        return "mfma", (2.0 if bf else f4) * N * F + fx * B * F + f4 * N * B, 2.0 * B * F * N
+    if name == "gemm_bwd":       # W1 -= lr dZ^T X: read dZ, X; read+write W1 (+ its bf16 copy)
+        return ("mfma", (2.0 if bf else f4) * N * B + fx * B * F + 2 * f4 * N * F
+                + (2.0 * N * F if bf else 0.0), 2.0 * B * F * N)
+    if name == "m3_fwd":         # read Z, W2; write logits
         return "hbm", f4 * (N * B + O * N + B * M * O), 2.0 * B * O * N
-    if name == "m3_bwd":        # read Z, G, W2; write dZ, W2
-        return "hbm", f4 * (2 * N * B + 2 * O * N + B * M * O), 4.0 * B * O * N
-    if name == "bwd_fused":     # read Z, G, X; read+write W1 and W2 (dZ stays in registers)
+    if name == "m3_bwd":         # read Z, G, W2; write dZ (bf16 in bf16 mode), W2
+        return ("hbm", f4 * N * B + (2.0 if bf else f4) * N * B + f4 * (2 * O * N + B * M * O),
+                4.0 * B * O * N)
+    if name == "bwd_fused":      # read Z, G, X; read+write W1 and W2 (dZ stays in registers)
         return ("mfma", f4 * (N * B + B * M * O + B * F + 2 * N * F + 2 * O * N),
                 2.0 * B * F * N + 4.0 * B * O * N)
-    if name == "ce":            # read logits, y; write G, loss
+    if name == "ce":             # read logits, y; write G, loss
         return "hbm", f4 * (2 * B * M * O + B + M), 0.0
-    if name == "pack_x":        # read X; write two padded copies
+    if name == "pack_x":         # read X; write two padded copies
         return "hbm", f4 * B * F + 2 * fx * B * F, 0.0
     return "hbm", 0.0, 0.0
 
 
-def load_traffic(kernel: str, workload: str):
+def traffic_key(kernel: str, workload: str, precision: str) -> str:
+    return "%s/%s%s" % (kernel, workload, "" if precision == "fp32" else "+" + precision)
+
+
+def load_traffic(kernel: str, workload: str, precision: str = "fp32"):
     """HBM bytes per launch from committed rocprofv3 counter summaries, if
     they were taken on the current kernel source; otherwise None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -71,20 +80,36 @@ def load_traffic(kernel: str, workload: str):
         table = json.load(open(path))
     except ValueError:
         return None
-    ent = table.get("%s/%s" % (kernel, workload))
-    if not ent or ent.get("kernels_sha") != kernel_source_digest():
+    ent = table.get(traffic_key(kernel, workload, precision))
+    if not ent or ent.get("kernels_sha") != kernel_source_digest(kernel, precision):
         return None
     return ent.get("bytes_per_launch")
 
 
-def kernel_source_digest() -> str:
-    """sha256 (16 hex digits) over the HIP sources and headers of the library."""
+# Source file that defines each timed kernel, per precision mode (the shared
+# headers are hashed with it).
+KERNEL_SOURCE = {
+    "fp32": {"gemm_fwd": "k_lds.hip", "bwd_fused": "k_lds.hip", "gemm_bwd": "k_gemm.hip",
+             "m3_fwd": "k_m3.hip", "m3_bwd": "k_m3.hip", "ce": "k_misc.hip",
+             "pack_x": "k_misc.hip", "aux": "k_misc.hip"},
+    "bf16": {"gemm_fwd": "k_gemm_bf16.hip", "gemm_bwd": "k_gemm_bf16.hip",
+             "m3_fwd": "k_m3.hip", "m3_bwd": "k_m3.hip", "ce": "k_misc.hip",
+             "pack_x": "k_misc.hip", "aux": "k_misc.hip"},
+}
+
+
+def kernel_source_digest(kernel: str = None, precision: str = "fp32") -> str:
+    """sha256 (16 hex digits) over the source of one kernel and the shared
+    headers (all HIP sources when the kernel is not named)."""
     csrc = os.path.join(ROOT, "paper_2206_08369_amd", "csrc")
+    names = sorted(n for n in os.listdir(csrc) if n.endswith((".hip", ".h")))
+    src = KERNEL_SOURCE.get(precision, {}).get(kernel) if kernel else None
+    if src:
+        names = sorted(n for n in names if n.endswith(".h") or n == src)
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h")):
-            h.update(name.encode())
-            h.update(open(os.path.join(csrc, name), "rb").read())
+    for name in names:
+        h.update(name.encode())
+        h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -211,7 +236,7 @@ def main(argv=None):
     else:
         peak, achieved, unit = PEAK_HBM_GBS, nbytes / avg_s / 1e9, "GB/s"
     roofline = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                "frac": achieved / peak, "traffic": load_traffic(dom, w.name),
+                "frac": achieved / peak, "traffic": load_traffic(dom, w.name, args.precision),
                 "kernel": dom}
 
     cpu = None

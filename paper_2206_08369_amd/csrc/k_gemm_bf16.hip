@@ -73,7 +73,11 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   static_assert((MQ * CQ) % NT == 0 || MQ * CQ < NT, "loader shape");
   static_assert((MP * CP) % 64 == 0 && (MQ * CQ) % 64 == 0, "loader shape");
   constexpr int PS = MP * 2 * NS, QS = MQ * 2 * NS;  // 16-byte entries per stage
-  __shared__ u32x4 lds[2 * (PS + QS)];
+  // epilogue scratch: QB adjacent 32 x 32 blocks per wave, rows padded by 4
+  constexpr int QB = TQ % 2 == 0 ? 2 : 1, LDT = 32 * QB + 4;
+  constexpr int SCR = NT / 64 * 32 * LDT / 4;  // 16-byte units
+  constexpr int LDSN = 2 * (PS + QS) > SCR ? 2 * (PS + QS) : SCR;
+  __shared__ u32x4 lds[LDSN];
 
   const int blk = blockIdx.x;
   const int xcd = blk & 7, jb = blk >> 3;
@@ -238,32 +242,35 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
     }
   }
 
-  // Epilogue: each 32 x 32 block goes through a per-wave LDS scratch so that
-  // eight consecutive lanes hold one row's 32 consecutive q; every store (and
-  // the read of the SGD update) then covers whole 128-byte row segments
-  // instead of 16 bytes of 32 rows.  Scratch rows are padded to 36 floats:
-  // the column writes of the MFMA layout and the row reads both stay within
-  // two lanes per bank.
-  constexpr int LDT = 36;
-  static_assert(NT / 64 * 32 * LDT * 4 <= (int)sizeof(lds), "epilogue scratch");
+  // Epilogue: QB horizontally adjacent 32 x 32 blocks at a time go through a
+  // per-wave LDS scratch so that 8*QB consecutive lanes hold one row's 32*QB
+  // consecutive q; every store (and the read of the SGD update) then covers
+  // whole row segments -- 256 bytes of fp32 and a full 128-byte line of the
+  // bf16 copy when QB = 2 -- instead of 16 bytes of 32 rows.  Scratch rows
+  // are padded by four floats: the column writes of the MFMA layout and the
+  // row reads both stay conflict-free.
   float* scr = (float*)lds + wave * (32 * LDT);
   __syncthreads();  // every wave is done with the operand stages
 #pragma unroll
   for (int j = 0; j < TP; ++j)
 #pragma unroll
-    for (int i = 0; i < TQ; ++i) {
+    for (int i0 = 0; i0 < TQ; i0 += QB) {
 #pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) {
-        const f32x4 v = {acc[i][j][4 * i4], acc[i][j][4 * i4 + 1], acc[i][j][4 * i4 + 2],
-                         acc[i][j][4 * i4 + 3]};
-        *(f32x4*)(scr + (lane & 31) * LDT + 8 * i4 + 4 * (lane >> 5)) = v;
-      }
+      for (int ib = 0; ib < QB; ++ib)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int i = i0 + ib;
+          const f32x4 v = {acc[i][j][4 * i4], acc[i][j][4 * i4 + 1], acc[i][j][4 * i4 + 2],
+                           acc[i][j][4 * i4 + 3]};
+          *(f32x4*)(scr + (lane & 31) * LDT + 32 * ib + 8 * i4 + 4 * (lane >> 5)) = v;
+        }
       __syncthreads();
       const int64_t pb = p0 + 32 * (wp * TP + j);
-      const int qb = q0 + 32 * (wq * TQ + i);
+      const int qb = q0 + 32 * (wq * TQ + i0);
+      constexpr int LPR = 8 * QB;  // lanes per row
 #pragma unroll
-      for (int pass = 0; pass < 4; ++pass) {
-        const int r = 8 * pass + (lane >> 3), c4 = 4 * (lane & 7);
+      for (int pass = 0; pass < 32 * LPR / 64; ++pass) {
+        const int r = pass * (64 / LPR) + lane / LPR, c4 = 4 * (lane % LPR);
         const f32x4 v = *(const f32x4*)(scr + r * LDT + c4);
         const int64_t p = pb + r;
         const int q = qb + c4;
