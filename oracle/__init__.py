@@ -73,6 +73,8 @@ def _load():
         lib.orc_bf16.argtypes = [C.c_float]
         lib.orc_bf16_array.restype = None
         lib.orc_bf16_array.argtypes = [P, P, i64]
+        lib.orc_value_ties.restype = C.c_int
+        lib.orc_value_ties.argtypes = [i32, i32, P, P, P, P, i32, dbl, P]
         lib.orc_dataset_loss.restype = C.c_int
         lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, i64,
                                          i32, P, C.c_int]
@@ -225,6 +227,21 @@ def hidden(hidden_sizes, act_ids, W1, X,
         _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B, _p(Z), _p(H)),
                "hidden")
     return Z, H
+
+
+def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
+               rounding: str = "exact") -> np.ndarray:
+    """Per-model count of (sample, unit) pairs whose Z sits within rounding
+    of a jump of its activation (Hardshrink at +-0.5); models with a nonzero
+    count have several correct fp32 results and are left out of comparisons."""
+    hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
+    W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
+    B, F = Xf.shape
+    counts = np.empty(len(hs), np.int32)
+    with _rounding(rounding):
+        _check(_load().orc_value_ties(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B,
+                                      float(rel), _p(counts)), "value_ties")
+    return counts
 
 
 def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,

@@ -58,12 +58,24 @@
 /* ------------------------------------------------------------------------ */
 /* Activations.  Ids: 0 identity, 1 ReLU, 2 tanh, 3 sigmoid, 4 ELU(alpha=1), */
 /* 5 LeakyReLU(0.01), 6 GELU (exact: z * normal CDF), 7 SiLU, 8 softplus  */
-/* (beta=1, linear above 20), 9 Swish with beta=2.                          */
+/* (beta=1, linear above 20), 9 Swish with beta=2, and the remaining       */
+/* functions of the paper's list (Section 4.2): 10 SELU (the self-        */
+/* normalising constants of Klambauer et al., 2017), 11 Hardshrink with    */
+/* threshold 0.5, 12 Mish (z tanh(softplus z), Misra 2019).                */
 /* Section 3 (last paragraph) applies a different activation to each       */
 /* contiguous portion of the hidden layer; which functions is a workload   */
 /* choice.  Kinks follow the usual autograd conventions: ReLU'(0)=0,        */
-/* LeakyReLU'(0)=0.01, ELU'(0)=1.                                            */
+/* LeakyReLU'(0)=0.01, ELU'(0)=1, SELU'(0)=lambda*alpha (the negative       */
+/* branch), Hardshrink'(+-0.5)=0 and Hardshrink(+-0.5)=0.                   */
 /* ------------------------------------------------------------------------ */
+
+#define ORC_SELU_ALPHA 1.6732632423543772848170429916717
+#define ORC_SELU_LAMBDA 1.0507009873554804934193349852946
+#define ORC_NUM_ACTS 13
+
+static double orc_softplus(double z) {
+  return (z > 0.0 ? z : 0.0) + log1p(exp(-fabs(z)));
+}
 
 static double orc_logistic(double x) {
   /* 1/(1+e^-x) written so that exp never overflows */
@@ -88,6 +100,9 @@ double orc_act(int id, double z) {
     case 7: return z * orc_logistic(z);
     case 8: return z > 20.0 ? z : (z > 0.0 ? z : 0.0) + log1p(exp(-fabs(z)));
     case 9: return z * orc_logistic(2.0 * z);
+    case 10: return ORC_SELU_LAMBDA * (z > 0.0 ? z : ORC_SELU_ALPHA * expm1(z));
+    case 11: return (z > 0.5 || z < -0.5) ? z : 0.0;
+    case 12: return z * tanh(orc_softplus(z));
     default: return NAN;
   }
 }
@@ -108,18 +123,32 @@ double orc_act_deriv(int id, double z) {
     case 7: { double s = orc_logistic(z); return s + z * s * (1.0 - s); }
     case 8: return z > 20.0 ? 1.0 : orc_logistic(z);
     case 9: { double s = orc_logistic(2.0 * z); return s + 2.0 * z * s * (1.0 - s); }
+    case 10: return z > 0.0 ? ORC_SELU_LAMBDA : ORC_SELU_LAMBDA * ORC_SELU_ALPHA * exp(z);
+    case 11: return (z > 0.5 || z < -0.5) ? 1.0 : 0.0;
+    case 12: {
+      double t = tanh(orc_softplus(z));
+      return t + z * (1.0 - t * t) * orc_logistic(z);
+    }
     default: return NAN;
   }
 }
 
-/* Slope jump across the kink at z = 0 for piecewise-linear activations
- * (right slope minus left slope); 0 for activations differentiable at 0. */
+/* Size of the slope jump at the activation's kinks (0 for activations
+ * differentiable everywhere): ReLU and LeakyReLU at 0, SELU at 0
+ * (lambda*alpha left, lambda right), Hardshrink at +-0.5. */
 static double orc_kink_jump(int id) {
   switch (id) {
     case 1: return 1.0;
     case 5: return 0.99;
+    case 10: return ORC_SELU_LAMBDA * (ORC_SELU_ALPHA - 1.0);
+    case 11: return 1.0;
     default: return 0.0;
   }
+}
+
+/* Distance of z from the nearest kink of the activation. */
+static double orc_kink_dist(int id, double z) {
+  return id == 11 ? fabs(fabs(z) - 0.5) : fabs(z);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -338,7 +367,7 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
       for (int f = 0; f < F; ++f)
         mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
       double z = s->Z[(int64_t)b * h + j];
-      if (fabs(z) <= kink_rel * mag) {
+      if (orc_kink_dist(s->act, z) <= kink_rel * mag) {
         double d = fabs(s->dH[(int64_t)b * h + j]) * jump;
         for (int f = 0; f < F; ++f)
           allow[(int64_t)j * F + f] += d * fabs(orc_in(X[(int64_t)b * F + f]));
@@ -419,7 +448,7 @@ static void orc_put(int64_t N, int F, int O, int64_t off, int h, const double* w
 static int orc_check(int F, int O, int M, const int32_t* hs, const int32_t* acts) {
   if (F < 1 || O < 2 || M < 1 || !hs || !acts) return ORC_EINVAL;
   for (int m = 0; m < M; ++m)
-    if (hs[m] < 1 || acts[m] < 0 || acts[m] > 9) return ORC_EINVAL;
+    if (hs[m] < 1 || acts[m] < 0 || acts[m] >= ORC_NUM_ACTS) return ORC_EINVAL;
   return ORC_OK;
 }
 
@@ -593,7 +622,7 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
   if (F < 1 || M < 1 || !hs || !acts || !W1 || !X || B < 1 || !Z || !H) return ORC_EINVAL;
   int64_t N = 0;
   for (int m = 0; m < M; ++m) {
-    if (hs[m] < 1 || acts[m] < 0 || acts[m] > 9) return ORC_EINVAL;
+    if (hs[m] < 1 || acts[m] < 0 || acts[m] >= ORC_NUM_ACTS) return ORC_EINVAL;
     N += hs[m];
   }
   int64_t n = 0;
@@ -604,6 +633,35 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
         for (int f = 0; f < F; ++f) acc += orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]);
         Z[(int64_t)b * N + n] = acc;
         H[(int64_t)b * N + n] = orc_act(acts[m], acc);
+      }
+    }
+  }
+  return ORC_OK;
+}
+
+/* Value ties of activations with a jump (Hardshrink at +-0.5): counts[m]
+ * receives the number of (sample, hidden unit) pairs of model m whose Z lies
+ * within rel * sum_f |x_f w_f| of a jump.  An fp32 evaluation that is correct
+ * to within rounding may land on either side there, and the hidden value
+ * then differs by the size of the jump; a comparison leaves such models out
+ * (several results are correct for them). */
+int orc_value_ties(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
+                   const double* W1, const float* X, int32_t B, double rel, int32_t* counts) {
+  if (F < 1 || M < 1 || !hs || !acts || !W1 || !X || B < 1 || !counts) return ORC_EINVAL;
+  int64_t n = 0;
+  for (int m = 0; m < M; ++m) {
+    if (hs[m] < 1 || acts[m] < 0 || acts[m] >= ORC_NUM_ACTS) return ORC_EINVAL;
+    counts[m] = 0;
+    for (int j = 0; j < hs[m]; ++j, ++n) {
+      if (acts[m] != 11) continue;
+      for (int b = 0; b < B; ++b) {
+        double acc = 0.0, mag = 0.0;
+        for (int f = 0; f < F; ++f) {
+          const double t = orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]);
+          acc += t;
+          mag += fabs(t);
+        }
+        if (fabs(fabs(acc) - 0.5) <= rel * mag) counts[m] += 1;
       }
     }
   }

@@ -340,7 +340,7 @@ def test_invalid_labels_and_sizes_rejected(orc):
     with pytest.raises(RuntimeError):
         orc.forward(np.array([0], np.int32), [0], W1[:1], W2[:, :1], X)
     with pytest.raises(RuntimeError):
-        orc.forward([1], [10], W1[:1], W2[:, :1], X)
+        orc.forward([1], [13], W1[:1], W2[:, :1], X)
 
 
 # --------------------------------------------------------------------------
