@@ -64,7 +64,7 @@ def _load():
                                       P, P, P, P, dbl, dbl, C.c_int]
         lib.orc_train.restype = C.c_int
         lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32, P, P,
-                                  dbl, P, P, P, P, i32, C.c_int]
+                                  dbl, P, P, P, P, i32, P, dbl, C.c_int]
         lib.orc_hidden.restype = C.c_int
         lib.orc_hidden.argtypes = [i32, i32, P, P, P, P, i32, P, P]
         lib.orc_set_input_rounding.restype = C.c_int
@@ -189,11 +189,14 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
 
 def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
           lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0,
-          rounding: str = "exact"):
+          rounding: str = "exact", return_ties: bool = False, tie_rel: float = 1e-6):
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
-    subset, entries of the other models are NaN."""
+    subset, entries of the other models are NaN.  With return_ties, a fourth
+    item counts per model the value ties met during training (Z within
+    tie_rel * sum_f |x w| of a jump of the activation, at that step's
+    weights; see value_ties)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
     F = Xf.shape[1]
@@ -206,11 +209,14 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     W2o = np.full((O, N), np.nan)
     loss = np.full(len(hs), np.nan)
     sel = None if models is None else _c(models, np.int32)
+    ties = np.zeros(len(hs), np.int32) if return_ties else None
     with _rounding(rounding):
         _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
                                  _p(yi), len(batches), _p(off), _p(ln), float(lr), _p(W1o),
                                  _p(W2o), _p(loss), _p(sel), 0 if sel is None else len(sel),
-                                 nthreads), "train")
+                                 _p(ties), float(tie_rel), nthreads), "train")
+    if return_ties:
+        return W1o, W2o, loss, ties
     return W1o, W2o, loss
 
 

@@ -375,6 +375,23 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
     }
 }
 
+/* Number of samples b and units j of one model whose Z lies within
+ * rel * sum_f |x_f w_f| of a jump of the activation (Hardshrink at +-0.5). */
+static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
+                                    const double* w1, double rel) {
+  if (s->act != 11) return 0;
+  const int F = s->F, h = s->h;
+  int32_t n = 0;
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < h; ++j) {
+      double mag = 0.0;
+      for (int f = 0; f < F; ++f)
+        mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
+      if (fabs(fabs(s->Z[(int64_t)b * h + j]) - 0.5) <= rel * mag) ++n;
+    }
+  return n;
+}
+
 /* Rounding-tie allowance of the bf16 operand mode.  dZ reaches the dW1
  * product as the bfloat16 nearest to its fp32 value; an fp32 evaluation of
  * dZ that is correct to within rounding may sit on the other side of a
@@ -562,7 +579,8 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
               const double* W1, const double* W2, const float* X, const int32_t* y,
               int32_t nbatches, const int64_t* batch_off, const int32_t* batch_len,
               double lr, double* W1_out, double* W2_out, double* loss_last,
-              const int32_t* models, int32_t nmodels, int nthreads) {
+              const int32_t* models, int32_t nmodels, int32_t* ties, double tie_rel,
+              int nthreads) {
   if (orc_check(F, O, M, hs, acts) || nbatches < 0 || !W1 || !W2 || !X || !y ||
       (nbatches > 0 && (!batch_off || !batch_len)) || !W1_out || !W2_out)
     return ORC_EINVAL;
@@ -576,6 +594,8 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
   orc_offsets(M, hs, off);
   const int64_t N = off[M];
   const int count = models ? nmodels : M;
+  if (ties)
+    for (int m = 0; m < M; ++m) ties[m] = 0;
   int err = ORC_OK;
   orc_set_threads(nthreads);
 #pragma omp parallel for schedule(dynamic, 1)
@@ -599,6 +619,7 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
         const int B = batch_len[k];
         orc_model_forward(&s, B, Xb, w1, w2);
         last = orc_model_ce(&s, B, yb);
+        if (ties) ties[m] += orc_model_value_ties(&s, B, Xb, w1, tie_rel);
         orc_model_backward(&s, B, Xb, w2, g1, g2);
         for (int64_t t = 0; t < (int64_t)h * F; ++t) w1[t] -= lr * g1[t];
         for (int64_t t = 0; t < (int64_t)h * O; ++t) w2[t] -= lr * g2[t];

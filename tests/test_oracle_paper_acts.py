@@ -110,3 +110,23 @@ def test_value_ties_count_hardshrink_jumps_only(orc):
     assert list(counts) == [1, 0, 0, 1]           # unit 3: Z[0] = 0.5 as well
     far = orc.value_ties([1], [HARDSHRINK], np.array([[0.05, 0.05]]), X)
     assert list(far) == [0]
+
+
+def test_training_counts_ties_at_each_step(orc):
+    """The tie count of training equals value_ties evaluated at the weights
+    each step actually uses."""
+    rng = np.random.default_rng(3)
+    hs = np.array([3, 4, 2], np.int32)
+    acts = np.array([HARDSHRINK, MISH, HARDSHRINK], np.int32)
+    X = rng.standard_normal((12, 2)).astype(np.float32)
+    y = rng.integers(0, 2, 12).astype(np.int32)
+    W1 = np.array([[0.25, 0.25], [0.1, -0.3], [0.6, 0.2], [0.1, 0.1], [0.2, 0.2], [0.3, 0.3],
+                   [0.4, 0.4], [0.3, -0.2], [0.5, 0.0]])
+    X[0] = [1.0, 1.0]                                  # unit 0 meets the jump at step 1
+    W2 = rng.uniform(-0.5, 0.5, (2, 9))
+    batches = [(0, 6), (6, 6)]
+    _, _, _, ties = orc.train(hs, acts, W1, W2, X, y, batches, 0.1, return_ties=True)
+    want = orc.value_ties(hs, acts, W1, X[:6])
+    W1a, W2a, _ = orc.train(hs, acts, W1, W2, X, y, batches[:1], 0.1)
+    want = want + orc.value_ties(hs, acts, W1a, X[6:])
+    assert list(ties) == list(want) and ties[0] >= 1 and ties[1] == 0
