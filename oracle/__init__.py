@@ -61,7 +61,7 @@ def _load():
         lib.orc_forward.argtypes = [i32, i32, i32, P, P, P, P, P, i32, P, C.c_int]
         lib.orc_gradients.restype = C.c_int
         lib.orc_gradients.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32,
-                                      P, P, P, P, dbl, dbl, C.c_int]
+                                      P, P, P, P, dbl, dbl, dbl, C.c_int]
         lib.orc_train.restype = C.c_int
         lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32, P, P,
                                   dbl, P, P, P, P, i32, P, dbl, C.c_int]
@@ -160,14 +160,16 @@ def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
 
 def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
               with_allowance: bool = True, nthreads: int = 0, rounding: str = "exact",
-              tie_rel: float = 1e-5):
+              tie_rel: float = 1e-5, cond_rel: float = 2.4e-7):
     """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
 
     allow_dW1 bounds what a correct fp32 evaluation may differ by where a
     discrete choice is within rounding of its boundary: the derivative branch
     at a ReLU/LeakyReLU kink (|Z| <= kink_rel * sum_f |x w|) and, with
     rounding="bf16", the bfloat16 neighbour dZ rounds to (fp32 dZ within
-    tie_rel * sum_o |G W2| |act'| of a rounding midpoint).
+    tie_rel * sum_o |G W2| |act'| of a rounding midpoint); and the amplified
+    fp32 error of dH = G W2 where its terms cancel more than 16-fold
+    (cond_rel, about 4 units in the last fp32 place, times the excess).
 
     The gradient is that of sum_m L_m, so each model's slice is the gradient
     of its own mean cross-entropy."""
@@ -182,7 +184,8 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     with _rounding(rounding):
         _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
                                      _p(yi), B, _p(dW1), _p(dW2), _p(loss), _p(allow),
-                                     float(kink_rel), float(tie_rel), nthreads),
+                                     float(kink_rel), float(tie_rel), float(cond_rel),
+                                     nthreads),
                "gradients")
     return dW1, dW2, loss, allow
 

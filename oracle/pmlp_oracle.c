@@ -392,6 +392,35 @@ static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
   return n;
 }
 
+/* Cancellation allowance of dH = sum_o G[b,o] W2[o,j].  The rows of G sum
+ * to zero, so dH can be much smaller than its terms (O = 2 with nearly equal
+ * W2 entries).  An fp32 evaluation of G = (softmax - onehot)/B is off by a
+ * few units in the last place of Ghat[b,o] = (p[b,o] + [o == y_b]) / B, so
+ * dH is off by up to a few ulp of mag = sum_o Ghat |W2[o,j]|.  The per-model
+ * tolerance absorbs that while mag stays within 16 |dH|; beyond it, dW1 can
+ * move by
+ *   allow[j,f] += cond_rel * (mag - 16 |dH|) * |act'(Z)| * |X[b,f]|
+ * summed over b (nothing where dH does not cancel). */
+static void orc_model_cond_allow(const orc_scratch* s, int B, const float* X,
+                                 const int32_t* y, const double* w2, double* allow,
+                                 double cond_rel) {
+  const int F = s->F, O = s->O, h = s->h;
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < h; ++j) {
+      double mag = 0.0;
+      for (int o = 0; o < O; ++o) {
+        const double g = s->G[(int64_t)b * O + o];
+        const double gh = o == y[b] ? g + 2.0 / B : g;   /* (p + [o == y]) / B */
+        mag += gh * fabs(w2[(int64_t)o * h + j]);
+      }
+      const double excess = mag - 16.0 * fabs(s->dH[(int64_t)b * h + j]);
+      if (!(excess > 0.0)) continue;
+      const double d = cond_rel * excess * fabs(orc_act_deriv(s->act, s->Z[(int64_t)b * h + j]));
+      for (int f = 0; f < F; ++f)
+        allow[(int64_t)j * F + f] += d * fabs(orc_in(X[(int64_t)b * F + f]));
+    }
+}
+
 /* Rounding-tie allowance of the bf16 operand mode.  dZ reaches the dW1
  * product as the bfloat16 nearest to its fp32 value; an fp32 evaluation of
  * dZ that is correct to within rounding may sit on the other side of a
@@ -523,11 +552,12 @@ int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_
  * dW2 [O,N], loss [M] (per-model mean cross-entropy).  allow_dW1 [N,F]
  * (may be NULL) receives the kink allowance described above, with
  * kink_rel the relative distance to the kink treated as undetermined, plus
- * in the bf16 operand mode the rounding-tie allowance with tie_rel. */
+ * in the bf16 operand mode the rounding-tie allowance with tie_rel, plus the
+ * cancellation allowance of dH with cond_rel (0 switches it off). */
 int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
                   const double* W1, const double* W2, const float* X, const int32_t* y,
                   int32_t B, double* dW1, double* dW2, double* loss, double* allow_dW1,
-                  double kink_rel, double tie_rel, int nthreads) {
+                  double kink_rel, double tie_rel, double cond_rel, int nthreads) {
   if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !y || !dW1 || !dW2 || !loss)
     return ORC_EINVAL;
   int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
@@ -557,6 +587,7 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
       if (al) {
         orc_model_kink_allow(&s, B, X, w1, al, kink_rel);
         if (orc_rounding) orc_model_tie_allow(&s, B, X, w2, al, tie_rel);
+        if (cond_rel > 0.0) orc_model_cond_allow(&s, B, X, y, w2, al, cond_rel);
         memcpy(allow_dW1 + off[m] * F, al, sizeof(double) * (size_t)h * F);
       }
     }

@@ -164,7 +164,8 @@ def test_bf16_tie_allowance_covers_the_neighbouring_rounding(orc):
     _, G = _softmax_grad(Z @ W2.astype(np.float64).T, y)
     dZ = G @ W2.astype(np.float64)
     mag = np.abs(G) @ np.abs(W2.astype(np.float64))
-    g1, _, _, allow = orc.gradients(hs, acts, W1, W2, X, y, rounding="bf16", tie_rel=tie_rel)
+    g1, _, _, allow = orc.gradients(hs, acts, W1, W2, X, y, rounding="bf16", tie_rel=tie_rel,
+                                    cond_rel=0.0)
     rng = np.random.default_rng(4)
     flipped = 0
     for trial in range(20):

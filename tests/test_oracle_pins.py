@@ -421,3 +421,38 @@ def test_hidden_layer_is_matmul_then_activation(orc):
     for n in range(N):
         np.testing.assert_allclose(H[:, n], _reference_act(acts[mid[n]], Z[:, n]),
                                    rtol=1e-12, atol=1e-300)
+
+
+def test_cancellation_allowance_covers_fp32_error_of_dH(orc):
+    """One width-1 unit with nearly equal output weights (dH = G W2 cancels
+    ~500-fold): a CPU fp32 evaluation with G carrying a few ulp of error
+    stays within the allowance; with output weights of opposite sign (no
+    cancellation across outputs) it is negligible."""
+    rng = np.random.default_rng(12)
+    F, O, B = 6, 2, 40
+    X = rng.standard_normal((B, F)).astype(np.float32)
+    y = rng.integers(0, O, B).astype(np.int32)
+    W1 = rng.uniform(-0.5, 0.5, (1, F))
+    for W2, cancels in ((np.array([[0.5392], [0.5415]]), True),
+                        (np.array([[0.5392], [-0.5415]]), False)):
+        d0, _, _, allow = orc.gradients([1], [2], W1, W2, X, y)
+        if not cancels:
+            assert allow.max() <= 1e-7 * np.abs(d0).max()
+            continue
+        L = orc.forward([1], [2], W1, W2, X)[:, 0, :]
+        P = np.exp(L - L.max(axis=1, keepdims=True))
+        P /= P.sum(axis=1, keepdims=True)
+        G = P.copy()
+        G[np.arange(B), y] -= 1
+        G /= B
+        Z = (X.astype(np.float64) @ W1[0])
+        worst = 0.0
+        for trial in range(10):
+            Gp = (G * (1 + rng.uniform(-3, 3, G.shape) * 2.0 ** -24)).astype(np.float32)
+            dH = (Gp[:, 0] * np.float32(W2[0, 0]) + Gp[:, 1] * np.float32(W2[1, 0]))
+            dZ = dH.astype(np.float64) * (1 - np.tanh(Z) ** 2)
+            dW1 = dZ @ X.astype(np.float64)
+            assert np.all(np.abs(dW1 - d0[0]) <= allow[0]), trial
+            worst = max(worst, np.abs(dW1 - d0[0]).max())
+        # the fp32 error really exceeds the per-model budget of 1e-5 here
+        assert worst > 1e-5 * np.abs(d0[0]).max()
