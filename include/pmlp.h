@@ -30,8 +30,12 @@
  * Activation ids: 0 identity, 1 ReLU, 2 tanh, 3 logistic sigmoid,
  * 4 ELU (alpha 1), 5 LeakyReLU (slope 0.01), 6 GELU (exact, z * normal
  * CDF), 7 SiLU, 8 softplus (beta 1, identity above 20), 9 Swish with
- * beta 2 (z * sigmoid(2z)).  Derivatives at the kinks: ReLU'(0) = 0,
- * LeakyReLU'(0) = 0.01, ELU'(0) = 1.
+ * beta 2 (z * sigmoid(2z)), and the rest of the activation list of
+ * Section 4.2: 10 SELU (alpha 1.6732632423543772, lambda
+ * 1.0507009873554805), 11 Hardshrink (threshold 0.5: z if |z| > 0.5,
+ * else 0), 12 Mish (z * tanh(softplus z)).  Derivatives at the kinks:
+ * ReLU'(0) = 0, LeakyReLU'(0) = 0.01, ELU'(0) = 1, SELU'(0) =
+ * lambda * alpha, Hardshrink'(+-0.5) = 0.
  *
  * Conventions for every call:
  *   - Return value: PMLP_OK (0) or a negative PMLP_E* code; a message for
@@ -68,12 +72,12 @@ extern "C" {
 #define PMLP_BF16_GEMM 1  /* the two input-layer GEMMs take bf16-rounded
                              operands with fp32 accumulation */
 
-#define PMLP_NUM_ACTS 10
+#define PMLP_NUM_ACTS 13
 
 typedef struct pmlp* pmlp_t;
 
 /* Create a packed model of M MLPs with F inputs and O outputs each.
- * hidden_sizes[M] (each >= 1) and act_ids[M] (each in [0, 9]) are copied;
+ * hidden_sizes[M] (each >= 1) and act_ids[M] (each in [0, 12]) are copied;
  * models are packed in the given order.  Weights start uniform in
  * (-1/sqrt(fan_in), +1/sqrt(fan_in)) with fan_in = F for W1 and h_m for
  * model m's W2, drawn from a counter-based splitmix64 stream:

@@ -38,6 +38,7 @@ PMLP_NUM_KERNELS = 9
 ACT_IDS = {
     "identity": 0, "relu": 1, "tanh": 2, "sigmoid": 3, "elu": 4, "leaky_relu": 5,
     "gelu": 6, "silu": 7, "softplus": 8, "swish2": 9,
+    "selu": 10, "hardshrink": 11, "mish": 12,
 }
 
 _HERE = os.path.dirname(os.path.abspath(__file__))

@@ -43,7 +43,8 @@ inline unsigned grid_for(int64_t n) {
 
 // ---------------------------------------------------------------------------
 // Activations (Section 3, last paragraph: one activation per contiguous
-// portion of the hidden layer).  Ids as in include/pmlp.h.
+// portion of the hidden layer; the list of Section 4.2).  Ids as in
+// include/pmlp.h.
 // ---------------------------------------------------------------------------
 
 // The transcendental pieces use the hardware approximations (v_exp_f32 on
@@ -63,6 +64,20 @@ __device__ __forceinline__ float normal_cdf(float z) {
   return 0.5f * erfcf(-z * 0.70710678118654752f);
 }
 
+// SELU constants (Klambauer et al., 2017)
+constexpr float kSeluAlpha = 1.6732632423543772f;
+constexpr float kSeluLambda = 1.0507009873554805f;
+
+// Mish: tanh(softplus z) = n / (n + 2) with n = e^z (e^z + 2), free of
+// cancellation for z << 0; 1 (to fp32) above 20.
+__device__ __forceinline__ float mish_t(float z, float* u_out) {
+  if (z > 20.f) { *u_out = 0.f; return 1.f; }
+  const float u = fexp(z);
+  const float n = u * (u + 2.f);
+  *u_out = u;
+  return n * frcp(n + 2.f);
+}
+
 __device__ __forceinline__ float act_fwd(int a, float z) {
   switch (a) {
     case 0: return z;
@@ -75,6 +90,9 @@ __device__ __forceinline__ float act_fwd(int a, float z) {
     case 7: return z * logistic(z);
     case 8: return z > 20.f ? z : fmaxf(z, 0.f) + flog(1.f + fexp(-fabsf(z)));
     case 9: return z * logistic(2.f * z);
+    case 10: return z > 0.f ? kSeluLambda * z : (kSeluLambda * kSeluAlpha) * (fexp(z) - 1.f);
+    case 11: return (z > 0.5f || z < -0.5f) ? z : 0.f;
+    case 12: { float u; return z * mish_t(z, &u); }
     default: return 0.f;
   }
 }
@@ -113,6 +131,24 @@ __device__ __forceinline__ float act_fwd_bwd(int a, float z, float* d) {
       const float s = logistic(2.f * z);
       *d = s + 2.f * z * s * (1.f - s);
       return z * s;
+    }
+    case 10: {
+      if (z > 0.f) { *d = kSeluLambda; return kSeluLambda * z; }
+      const float e = (kSeluLambda * kSeluAlpha) * fexp(z);
+      *d = e;
+      return e - kSeluLambda * kSeluAlpha;
+    }
+    case 11: {
+      const bool on = z > 0.5f || z < -0.5f;
+      *d = on ? 1.f : 0.f;
+      return on ? z : 0.f;
+    }
+    case 12: {
+      float u;
+      const float t = mish_t(z, &u);
+      const float s = z > 20.f ? 1.f : u * frcp(1.f + u);
+      *d = t + z * (1.f - t * t) * s;
+      return z * t;
     }
     default: *d = 0.f; return 0.f;
   }

@@ -278,6 +278,9 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
       case 7: bwdl_tile<TQ, OM, RING, 7>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
       case 8: bwdl_tile<TQ, OM, RING, 8>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
       case 9: bwdl_tile<TQ, OM, RING, 9>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 10: bwdl_tile<TQ, OM, RING, 10>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 11: bwdl_tile<TQ, OM, RING, 11>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 12: bwdl_tile<TQ, OM, RING, 12>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
       default: bwdl_tile<TQ, OM, RING, -1>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
     }
     // dW2: combine the four lk lanes of the row; lanes lk == 0 write.

@@ -100,7 +100,10 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
       case 6: fwd_segment<OM, 6>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
       case 7: fwd_segment<OM, 7>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
       case 8: fwd_segment<OM, 8>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      default: fwd_segment<OM, 9>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 9: fwd_segment<OM, 9>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 10: fwd_segment<OM, 10>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 11: fwd_segment<OM, 11>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      default: fwd_segment<OM, 12>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
     }
     for (int s = LG; s < 64; s <<= 1)
 #pragma unroll
@@ -280,7 +283,10 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
           case 6: bwd_segment<OM, 6>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
           case 7: bwd_segment<OM, 7>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
           case 8: bwd_segment<OM, 8>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          default: bwd_segment<OM, 9>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 9: bwd_segment<OM, 9>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 10: bwd_segment<OM, 10>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 11: bwd_segment<OM, 11>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          default: bwd_segment<OM, 12>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
         }
         n = se;
         ++m;

@@ -32,6 +32,7 @@ import numpy as np
 ACT_NAMES = (
     "identity", "relu", "tanh", "sigmoid", "elu", "leaky_relu",
     "gelu", "silu", "softplus", "swish2",
+    "selu", "hardshrink", "mish",
 )
 
 

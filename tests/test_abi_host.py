@@ -54,7 +54,7 @@ def test_kernel_names(pm):
     (3, 17, [1], [0], "O must be"),
     (3, 2, [0], [0], "hidden size"),
     (3, 2, [2, -1], [0, 0], "hidden size"),
-    (3, 2, [1], [10], "activation id"),
+    (3, 2, [1], [13], "activation id"),
     (3, 2, [1], [-1], "activation id"),
 ])
 def test_create_rejects_bad_arguments(pm, F, O, hs, acts, msg):
