@@ -64,7 +64,7 @@ def _load():
                                       P, P, P, P, dbl, dbl, dbl, C.c_int]
         lib.orc_train.restype = C.c_int
         lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32, P, P,
-                                  dbl, P, P, P, P, i32, P, dbl, C.c_int]
+                                  dbl, P, P, P, P, P, i32, P, dbl, C.c_int]
         lib.orc_hidden.restype = C.c_int
         lib.orc_hidden.argtypes = [i32, i32, P, P, P, P, i32, P, P]
         lib.orc_set_input_rounding.restype = C.c_int
@@ -196,7 +196,8 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
-    subset, entries of the other models are NaN.  With return_ties, a fourth
+    subset, entries of the other models are NaN.  lr is one rate for all
+    models or an array of M per-model rates.  With return_ties, a fourth
     item counts per model the value ties met during training (Z within
     tie_rel * sum_f |x w| of a jump of the activation, at that step's
     weights; see value_ties)."""
@@ -213,9 +214,17 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     loss = np.full(len(hs), np.nan)
     sel = None if models is None else _c(models, np.int32)
     ties = np.zeros(len(hs), np.int32) if return_ties else None
+    lr_arr = np.asarray(lr, np.float64)
+    lr_m = None
+    if lr_arr.ndim:
+        lr_m = np.ascontiguousarray(lr_arr.reshape(-1))
+        if lr_m.size != len(hs):
+            raise ValueError("per-model lr needs one rate per model")
+        lr = 0.0
     with _rounding(rounding):
         _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
-                                 _p(yi), len(batches), _p(off), _p(ln), float(lr), _p(W1o),
+                                 _p(yi), len(batches), _p(off), _p(ln), float(lr), _p(lr_m),
+                                 _p(W1o),
                                  _p(W2o), _p(loss), _p(sel), 0 if sel is None else len(sel),
                                  _p(ties), float(tie_rel), nthreads), "train")
     if return_ties:

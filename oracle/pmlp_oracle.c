@@ -602,6 +602,8 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
  * the sample arrays X [S,F], y [S]; each batch performs, for every model
  * independently, forward, loss, backward and the simultaneous update
  *   W1 -= lr dW1;  W2 -= lr dW2
+ * with one learning rate for all models, or model m's own lr_model[m] when
+ * lr_model is given (per-model hyper-parameters, Section 7)
  * (dH uses W2 before the update).  W1_out/W2_out receive the final fp64
  * weights (only the chosen models' entries are written); loss_last [M]
  * receives each model's loss on the last batch, before that batch's
@@ -609,7 +611,8 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
 int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
               const double* W1, const double* W2, const float* X, const int32_t* y,
               int32_t nbatches, const int64_t* batch_off, const int32_t* batch_len,
-              double lr, double* W1_out, double* W2_out, double* loss_last,
+              double lr, const double* lr_model, double* W1_out, double* W2_out,
+              double* loss_last,
               const int32_t* models, int32_t nmodels, int32_t* ties, double tie_rel,
               int nthreads) {
   if (orc_check(F, O, M, hs, acts) || nbatches < 0 || !W1 || !W2 || !X || !y ||
@@ -652,8 +655,9 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
         last = orc_model_ce(&s, B, yb);
         if (ties) ties[m] += orc_model_value_ties(&s, B, Xb, w1, tie_rel);
         orc_model_backward(&s, B, Xb, w2, g1, g2);
-        for (int64_t t = 0; t < (int64_t)h * F; ++t) w1[t] -= lr * g1[t];
-        for (int64_t t = 0; t < (int64_t)h * O; ++t) w2[t] -= lr * g2[t];
+        const double lm = lr_model ? lr_model[m] : lr;
+        for (int64_t t = 0; t < (int64_t)h * F; ++t) w1[t] -= lm * g1[t];
+        for (int64_t t = 0; t < (int64_t)h * O; ++t) w2[t] -= lm * g2[t];
       }
       if (loss_last) loss_last[m] = last;
       orc_put(N, F, O, off[m], h, w1, w2, W1_out, W2_out);

@@ -456,3 +456,21 @@ def test_cancellation_allowance_covers_fp32_error_of_dH(orc):
             worst = max(worst, np.abs(dW1 - d0[0]).max())
         # the fp32 error really exceeds the per-model budget of 1e-5 here
         assert worst > 1e-5 * np.abs(d0[0]).max()
+
+
+def test_per_model_learning_rates_train_each_model_at_its_rate(orc):
+    """Per-model rates (Section 7's per-model hyper-parameters): each model
+    ends exactly where training it alone at its own rate ends."""
+    hs, acts, X, y, W1, W2 = _problem(29)
+    M = len(hs)
+    rates = np.linspace(0.0, 0.4, M)
+    batches = [(0, 7), (7, 7)]
+    P1, P2, pl = orc.train(hs, acts, W1, W2, X, y, batches, rates)
+    off = np.concatenate([[0], np.cumsum(hs)])
+    for m in (0, 5, M - 1):
+        s = slice(off[m], off[m + 1])
+        A1, A2, al = orc.train(hs[m:m + 1], acts[m:m + 1], W1[s], W2[:, s], X, y, batches, rates[m])
+        assert np.array_equal(P1[s], A1) and np.array_equal(P2[:, s], A2) and pl[m] == al[0]
+    assert np.array_equal(P1[off[0]:off[1]], W1[off[0]:off[1]])      # rate 0: unchanged
+    with pytest.raises(ValueError):
+        orc.train(hs, acts, W1, W2, X, y, batches, rates[:-1])
