@@ -44,7 +44,7 @@
  *     pointers are ordinary host memory.  The caller owns every buffer it
  *     passes and must keep it alive until the handle's stream has reached
  *     the call (enqueueing calls return before the GPU work is done).
- *   - Enqueueing calls (pmlp_forward, pmlp_train_step, pmlp_gradients,
+ *   - Enqueueing calls (pmlp_forward, pmlp_train_step[_lr], pmlp_gradients,
  *     pmlp_hidden) never synchronise.  Device-side problems such as labels
  *     outside [0, O) are recorded on the device and reported by the next
  *     synchronising call (pmlp_losses).
@@ -125,6 +125,15 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev);
  * are kept for pmlp_losses. */
 int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev,
                     int32_t B, float lr);
+
+/* pmlp_train_step with a learning rate per model (per-model
+ * hyper-parameters, Section 7): model m's parameters take
+ * W -= lr_dev[m] * dW.  lr_dev [M] fp32, device memory, read by the step's
+ * kernels.  A non-finite rate is not detected before the step (its model's
+ * weights become non-finite); the next pmlp_losses then returns
+ * PMLP_EINVAL.  Null pointers return PMLP_EINVAL. */
+int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev,
+                       int32_t B, const float* lr_dev);
 
 /* Copy the per-model mean cross-entropy of the last pmlp_train_step or
  * pmlp_gradients batch into out_host [M] (fp32).  Synchronises the

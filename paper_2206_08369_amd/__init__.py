@@ -20,7 +20,8 @@ __all__ = [
     "PMLP_OK", "PMLP_EINVAL", "PMLP_ENOMEM", "PMLP_EDEVICE", "PMLP_ESTATE",
     "PMLP_FP32", "PMLP_BF16_GEMM", "PMLP_NUM_KERNELS", "ACT_IDS", "PmlpError",
     "library_path", "load_library", "pmlp_create", "pmlp_destroy", "pmlp_set_stream",
-    "pmlp_set_precision", "pmlp_forward", "pmlp_train_step", "pmlp_losses",
+    "pmlp_set_precision", "pmlp_forward", "pmlp_train_step", "pmlp_train_step_lr",
+    "pmlp_losses",
     "pmlp_gradients", "pmlp_hidden", "pmlp_get_params", "pmlp_set_params", "pmlp_info",
     "pmlp_set_profiling", "pmlp_kernel_time", "pmlp_profile_reset", "pmlp_kernel_name",
     "pmlp_last_error", "PackedMLP",
@@ -72,6 +73,7 @@ def load_library():
         "pmlp_set_precision": [P, i32],
         "pmlp_forward": [P, P, i32, P],
         "pmlp_train_step": [P, P, P, i32, f32],
+        "pmlp_train_step_lr": [P, P, P, i32, P],
         "pmlp_losses": [P, P],
         "pmlp_gradients": [P, P, P, i32, P, P],
         "pmlp_hidden": [P, P, i32, P, P],
@@ -155,6 +157,11 @@ def pmlp_forward(h: int, X, B: int, logits) -> None:
 def pmlp_train_step(h: int, X, y, B: int, lr: float) -> None:
     _check(load_library().pmlp_train_step(h, _ptr(X), _ptr(y), int(B), float(lr)),
            "pmlp_train_step")
+
+
+def pmlp_train_step_lr(h: int, X, y, B: int, lr) -> None:
+    _check(load_library().pmlp_train_step_lr(h, _ptr(X), _ptr(y), int(B), _ptr(lr)),
+           "pmlp_train_step_lr")
 
 
 def pmlp_losses(h: int) -> np.ndarray:
@@ -283,11 +290,19 @@ class PackedMLP:
         pmlp_forward(self.handle, X, B, out)
         return out
 
-    def train_step(self, X, y, lr: float) -> None:
+    def train_step(self, X, y, lr) -> None:
+        """One SGD step; lr is one rate, or a float32 device tensor of M
+        per-model rates."""
         B = self._x(X)
         self._y(y, B)
         self._stream()
-        pmlp_train_step(self.handle, X, y, B, lr)
+        if isinstance(lr, self._torch.Tensor):
+            if not (lr.is_cuda and lr.dtype == self._torch.float32 and lr.is_contiguous()
+                    and lr.numel() == self.M):
+                raise ValueError("per-model lr must be a contiguous float32 device tensor of M rates")
+            pmlp_train_step_lr(self.handle, X, y, B, lr)
+        else:
+            pmlp_train_step(self.handle, X, y, B, lr)
 
     def gradients(self, X, y):
         B = self._x(X)

@@ -324,8 +324,8 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
 
 // Full step: forward, loss, backward and either the SGD update (dW1 and
 // dW2 null) or gradient stores.
-int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* dW1,
-         float* dW2) {
+int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const float* lrm,
+         float* dW1, float* dW2) {
   const int32_t Bp = pad_batch(B);
   if (int rc = use_device(h)) return rc;
   if (int rc = ensure_workspace(h, Bp)) return rc;
@@ -345,7 +345,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
       }))
     return rc;
   if (int rc = run(h, KID_CE, [&] {
-        return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, h->stream);
+        return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, dW1 ? nullptr : lrm,
+                         h->stream);
       }))
     return rc;
   if (h->lds_kernels && !bf16_mode(h) && bwd_lds_supported(Bp, h->F4, h->O)) {
@@ -366,6 +367,7 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
     b.F4 = h->F4;
     b.O = h->O;
     b.lr = lr;
+    b.lrm = lrm;
     if (int rc = run(h, KID_BWD_FUSED, [&] { return launch_bwd_lds(b, h->stream); })) return rc;
     h->have_loss = true;
     return PMLP_OK;
@@ -373,7 +375,7 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
   if (int rc = run(h, KID_M3_BWD, [&] {
         return launch_m3_bwd(h->Zt, bf16_mode(h) ? h->dZ16 : nullptr, Bp, h->W2, h->N, h->Npad,
                              h->O, h->d_mid, h->d_seg_off,
-                             h->d_act, h->LG, lr, dW2, h->stream);
+                             h->d_act, h->LG, lr, lrm, dW2, h->stream);
       }))
     return rc;
   if (bf16_mode(h)) {
@@ -390,6 +392,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
     g.ldo = dW1 ? h->F : h->F4;
     g.ncols = h->F;
     g.lr = lr;
+    g.lrm = lrm;
+    g.mid = h->d_mid;
     g.outb = dW1 ? nullptr : h->W1b;  // the update keeps the bf16 copy current
     g.ldob = bf16_ld(h->F4);
     if (int rc = run(h, KID_GEMM_BWD, [&] {
@@ -411,6 +415,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, float* 
   g.ldo = dW1 ? h->F : h->F4;
   g.ncols = h->F;
   g.lr = lr;
+  g.lrm = lrm;
+  g.mid = h->d_mid;
   if (int rc = run(h, KID_GEMM_BWD, [&] {
         return launch_gemm(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
       }))
@@ -522,7 +528,7 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
       hipMalloc(&h->d_actn, (size_t)Npad * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->d_tiles, tiles.size() * sizeof(Tile3)) != hipSuccess ||
       hipMalloc(&h->loss, (size_t)M * sizeof(float)) != hipSuccess ||
-      hipMalloc(&h->flag, sizeof(int32_t)) != hipSuccess ||
+      hipMalloc(&h->flag, 2 * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&d_bound2, (size_t)M * sizeof(float)) != hipSuccess) {
     (void)hipGetLastError();
     dfree(d_bound2);
@@ -541,7 +547,7 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
     PMLP_HIP(hipMemcpy(h->d_tiles, tiles.data(), tiles.size() * sizeof(Tile3),
                        hipMemcpyHostToDevice));
     PMLP_HIP(hipMemcpy(d_bound2, bound2.data(), (size_t)M * sizeof(float), hipMemcpyHostToDevice));
-    PMLP_HIP(hipMemset(h->flag, 0, sizeof(int32_t)));
+    PMLP_HIP(hipMemset(h->flag, 0, 2 * sizeof(int32_t)));
     PMLP_HIP(launch_init_params(h->W1, N, F, F4, bound1, h->W2, Npad, O, h->d_mid, d_bound2,
                                 splitmix64_host(seed), nullptr));
     PMLP_HIP(hipStreamSynchronize(nullptr));
@@ -599,14 +605,22 @@ int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t 
   if (int rc = check_batch(h, X_dev, B)) return rc;
   if (!y_dev) return fail(PMLP_EINVAL, "null labels");
   if (!std::isfinite(lr)) return fail(PMLP_EINVAL, "learning rate is not finite");
-  return step(h, X_dev, y_dev, B, lr, nullptr, nullptr);
+  return step(h, X_dev, y_dev, B, lr, nullptr, nullptr, nullptr);
+}
+
+int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
+                       const float* lr_dev) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!y_dev) return fail(PMLP_EINVAL, "null labels");
+  if (!lr_dev) return fail(PMLP_EINVAL, "null per-model learning rates");
+  return step(h, X_dev, y_dev, B, 0.f, lr_dev, nullptr, nullptr);
 }
 
 int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
                    float* dW1_dev, float* dW2_dev) {
   if (int rc = check_batch(h, X_dev, B)) return rc;
   if (!y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null labels or gradient buffer");
-  return step(h, X_dev, y_dev, B, 0.f, dW1_dev, dW2_dev);
+  return step(h, X_dev, y_dev, B, 0.f, nullptr, dW1_dev, dW2_dev);
 }
 
 int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev, float* H_dev) {
@@ -628,11 +642,13 @@ int pmlp_losses(pmlp_t h, float* out_host) {
   if (int rc = use_device(h)) return rc;
   PMLP_HIP(hipStreamSynchronize(h->stream));
   PMLP_HIP(hipMemcpy(out_host, h->loss, (size_t)h->M * sizeof(float), hipMemcpyDeviceToHost));
-  int32_t flag = 0;
-  PMLP_HIP(hipMemcpy(&flag, h->flag, sizeof(int32_t), hipMemcpyDeviceToHost));
-  if (flag) {
-    PMLP_HIP(hipMemset(h->flag, 0, sizeof(int32_t)));
-    return fail(PMLP_EINVAL, "a label outside [0, O) was seen since the last pmlp_losses call");
+  int32_t flag[2] = {0, 0};
+  PMLP_HIP(hipMemcpy(flag, h->flag, 2 * sizeof(int32_t), hipMemcpyDeviceToHost));
+  if (flag[0] || flag[1]) {
+    PMLP_HIP(hipMemset(h->flag, 0, 2 * sizeof(int32_t)));
+    return fail(PMLP_EINVAL, flag[0] ? "a label outside [0, O) was seen since the last pmlp_losses call"
+                                     : "a non-finite per-model learning rate was seen since the "
+                                       "last pmlp_losses call");
   }
   return PMLP_OK;
 }

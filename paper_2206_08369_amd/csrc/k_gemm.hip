@@ -126,6 +126,7 @@ __global__ __launch_bounds__(kBlock) void k_gemm_nt(GemmArgs a, int WQ) {
     const int64_t p = p0 + 16 * j + li;
     if (p >= a.NP) continue;
     float* orow = a.out + p * a.ldo;
+    const float lr = (EPI == EPI_SGD && a.lrm) ? a.lrm[a.mid[p]] : a.lr;
 #pragma unroll
     for (int i = 0; i < TQ; ++i) {
       const int q = q0 + 16 * i + 4 * lk;
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(kBlock) void k_gemm_nt(GemmArgs a, int WQ) {
         *(f32x4*)(orow + q) = acc[i][j];
       } else if (EPI == EPI_SGD) {
         f32x4 w = *(f32x4*)(orow + q);
-        w -= a.lr * acc[i][j];
+        w -= lr * acc[i][j];
         *(f32x4*)(orow + q) = w;
       } else {
 #pragma unroll

@@ -276,11 +276,12 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
         const int q = qb + c4;
         if (p >= a.NP || q >= a.NQ) continue;
         float* o = a.out + p * a.ldo + q;
+        const float lr = (EPI == EPI_SGD && a.lrm) ? a.lrm[a.mid[p]] : a.lr;
         if (EPI == EPI_STORE) {
           *(f32x4*)o = v;
         } else if (EPI == EPI_SGD) {
           f32x4 w = *(f32x4*)o;
-          w -= a.lr * v;
+          w -= lr * v;
           *(f32x4*)o = w;
           if (a.outb) {
             const bf16x4 wb = {(__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};

@@ -241,6 +241,7 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
     const int64_t pc = p < a.N ? p : a.N - 1;
     const int m = a.mid[pc];
     const int arow = a.actn[pc];
+    const float lr = a.lrm ? a.lrm[m] : a.lr;
     float w2[OM];
 #pragma unroll
     for (int o = 0; o < OM; ++o) w2[o] = a.W2[(int64_t)o * a.ldw + pc];
@@ -309,11 +310,11 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
       // padded rows (p >= N) absorb the tail of the last tile
       if (lk == 0)
 #pragma unroll
-        for (int o = 0; o < OM; ++o) a.W2[(int64_t)o * a.ldw + p] = w2[o] - a.lr * dw[o];
+        for (int o = 0; o < OM; ++o) a.W2[(int64_t)o * a.ldw + p] = w2[o] - lr * dw[o];
 #pragma unroll
       for (int i = 0; i < TQ; ++i) {
         const int q = 16 * i + 4 * lk;
-        if (q < a.F4) *(f32x4*)(orow + q) = w1v[i] - a.lr * acc[i];
+        if (q < a.F4) *(f32x4*)(orow + q) = w1v[i] - lr * acc[i];
       }
     }
   }

@@ -241,7 +241,8 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
     float* __restrict__ Zt, unsigned short* __restrict__ dZ16, int Bp, float* __restrict__ W2,
     int64_t N, int64_t ldw, int O, const int32_t* __restrict__ mid,
     const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
-    const float* __restrict__ G, int LG, int slots, float lr, float* __restrict__ dW2) {
+    const float* __restrict__ G, int LG, int slots, float lr, const float* __restrict__ lrm,
+    float* __restrict__ dW2) {
   __shared__ float lds[4 * kT5 * OM];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -301,15 +302,15 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
     const int64_t n = r0 + nl;
     const float d = dwl[nl * OM + o];
     if (GRAD) dW2[(int64_t)o * N + n] = d;
-    else W2[(int64_t)o * ldw + n] -= lr * d;
+    else W2[(int64_t)o * ldw + n] -= (lrm ? lrm[mid[n]] : lr) * d;
   }
 }
 
 template <int OM>
 static void m3_bwd_dispatch(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
                             int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
-                            const int32_t* act, const float* G, float lr, float* dW2,
-                            hipStream_t s) {
+                            const int32_t* act, const float* G, float lr, const float* lrm,
+                            float* dW2, hipStream_t s) {
   int LG = 64;
   const int q = (Bp + 3) / 4;
   if (q < 64) {
@@ -321,21 +322,21 @@ static void m3_bwd_dispatch(float* Zt, unsigned short* dZ16, int32_t Bp, float* 
   const unsigned blocks = (unsigned)((waves + 3) / 4);
   if (dW2)
     k_m3_bwd<OM, true><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act,
-                                                 G, LG, slots, lr, dW2);
+                                                 G, LG, slots, lr, lrm, dW2);
   else
     k_m3_bwd<OM, false><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act,
-                                                  G, LG, slots, lr, dW2);
+                                                  G, LG, slots, lr, lrm, dW2);
 }
 
 hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
                          int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
-                         const int32_t* act, const float* G, float lr, float* dW2,
-                         hipStream_t s) {
-  if (O <= 2) m3_bwd_dispatch<2>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else if (O <= 4) m3_bwd_dispatch<4>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else if (O <= 8) m3_bwd_dispatch<8>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else if (O <= 10) m3_bwd_dispatch<10>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
-  else m3_bwd_dispatch<16>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, dW2, s);
+                         const int32_t* act, const float* G, float lr, const float* lrm,
+                         float* dW2, hipStream_t s) {
+  if (O <= 2) m3_bwd_dispatch<2>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else if (O <= 4) m3_bwd_dispatch<4>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else if (O <= 8) m3_bwd_dispatch<8>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else if (O <= 10) m3_bwd_dispatch<10>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else m3_bwd_dispatch<16>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
   return hipGetLastError();
 }
 

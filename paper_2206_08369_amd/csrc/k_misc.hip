@@ -151,7 +151,8 @@ hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s) {
 // equal to each model's own).  One wave per model; in place:
 //   LG[m][b][:] (logits) -> G = (softmax - onehot(y_b)) / B,  G = 0 for b >= B
 //   loss[m] = mean_b (logsumexp - logit_y)
-// A label outside [0, O) raises *flag.
+// A label outside [0, O) raises flag[0]; a non-finite per-model rate (lrm,
+// may be null) raises flag[1].
 // ---------------------------------------------------------------------------
 
 template <int OM>
@@ -159,10 +160,12 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
                                                const int32_t* __restrict__ y, int M, int Bp,
                                                int B, int O, float invB,
                                                float* __restrict__ loss,
-                                               int32_t* __restrict__ flag) {
+                                               int32_t* __restrict__ flag,
+                                               const float* __restrict__ lrm) {
   const int lane = threadIdx.x & 63;
   const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (m >= M) return;
+  if (lrm && lane == 0 && !isfinite(lrm[m])) flag[1] = 1;
   float part = 0.f;
   for (int b = lane; b < Bp; b += 64) {
     float* row = LG + ((int64_t)m * Bp + b) * O;
@@ -199,13 +202,13 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
 }
 
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
-                     float* loss, int32_t* flag, hipStream_t s) {
+                     float* loss, int32_t* flag, const float* lrm, hipStream_t s) {
   const unsigned blocks = (unsigned)((M + 3) / 4);
   const float invB = 1.0f / (float)B;
-  if (O <= 2) k_ce<2><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
-  else if (O <= 4) k_ce<4><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
-  else if (O <= 8) k_ce<8><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
-  else k_ce<16><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag);
+  if (O <= 2) k_ce<2><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
+  else if (O <= 4) k_ce<4><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
+  else if (O <= 8) k_ce<8><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
+  else k_ce<16><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
   return hipGetLastError();
 }
 

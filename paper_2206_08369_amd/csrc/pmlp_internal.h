@@ -52,6 +52,8 @@ struct GemmArgs {
   int64_t ldo;
   int32_t ncols;   // EPI_GRAD: number of valid q columns
   float lr;
+  const float* lrm;    // EPI_SGD: per-model rates (null: lr for every row)
+  const int32_t* mid;  // model of each row p (with lrm)
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
@@ -72,6 +74,8 @@ struct GemmBfArgs {
   int64_t ldo;
   int32_t ncols;            // EPI_GRAD: number of valid q columns
   float lr;
+  const float* lrm;         // EPI_SGD: per-model rates (null: lr for every row)
+  const int32_t* mid;       // model of each row p (with lrm)
   unsigned short* outb;     // EPI_SGD: also store bf16 of the updated values (or null)
   int64_t ldob;
 };
@@ -110,6 +114,7 @@ struct BwdArgs {
   int64_t ldw;
   int32_t Bp, F, F4, O;
   float lr;
+  const float* lrm;  // per-model rates (null: lr for every row)
 };
 bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O);
 hipError_t launch_bwd_lds(const BwdArgs& a, hipStream_t s);
@@ -136,16 +141,18 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
                          const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
                          int64_t sb, hipStream_t s);
 
+// flag[0] is raised by a label outside [0, O), flag[1] by a non-finite
+// per-model rate in lrm (may be null).
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
-                     float* loss, int32_t* flag, hipStream_t s);
+                     float* loss, int32_t* flag, const float* lrm, hipStream_t s);
 
 // M3 backward + activation derivative: dZ over Zt in place (fp32), or, with
 // dZ16 set, as bf16 into dZ16 [Npad][Bp] leaving Zt unchanged; then the W2
 // update (dW2 null) or the dW2 store.
 hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
                          int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
-                         const int32_t* act, const float* G, float lr, float* dW2,
-                         hipStream_t s);
+                         const int32_t* act, const float* G, float lr, const float* lrm,
+                         float* dW2, hipStream_t s);
 
 hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              const int32_t* mid, const int32_t* act, float* Z, float* H,
