@@ -57,16 +57,18 @@ def _load():
         lib.orc_max_threads.restype = C.c_int
         lib.orc_init_params.restype = C.c_int
         lib.orc_init_params.argtypes = [i32, i32, i32, P, u64, P, P]
+        lib.orc_init_biases.restype = C.c_int
+        lib.orc_init_biases.argtypes = [i32, i32, i32, P, u64, P, P]
         lib.orc_forward.restype = C.c_int
-        lib.orc_forward.argtypes = [i32, i32, i32, P, P, P, P, P, i32, P, C.c_int]
+        lib.orc_forward.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, i32, P, C.c_int]
         lib.orc_gradients.restype = C.c_int
-        lib.orc_gradients.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32,
-                                      P, P, P, P, dbl, dbl, dbl, C.c_int]
+        lib.orc_gradients.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32,
+                                      P, P, P, P, P, P, dbl, dbl, dbl, C.c_int]
         lib.orc_train.restype = C.c_int
-        lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, i32, P, P,
-                                  dbl, P, P, P, P, P, i32, P, dbl, C.c_int]
+        lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32, P, P,
+                                  dbl, P, P, P, P, P, P, P, i32, P, dbl, C.c_int]
         lib.orc_hidden.restype = C.c_int
-        lib.orc_hidden.argtypes = [i32, i32, P, P, P, P, i32, P, P]
+        lib.orc_hidden.argtypes = [i32, i32, P, P, P, P, P, i32, P, P]
         lib.orc_set_input_rounding.restype = C.c_int
         lib.orc_set_input_rounding.argtypes = [C.c_int]
         lib.orc_bf16.restype = C.c_float
@@ -74,9 +76,9 @@ def _load():
         lib.orc_bf16_array.restype = None
         lib.orc_bf16_array.argtypes = [P, P, i64]
         lib.orc_value_ties.restype = C.c_int
-        lib.orc_value_ties.argtypes = [i32, i32, P, P, P, P, i32, dbl, P]
+        lib.orc_value_ties.argtypes = [i32, i32, P, P, P, P, P, i32, dbl, P]
         lib.orc_dataset_loss.restype = C.c_int
-        lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, i64,
+        lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i64,
                                          i32, P, C.c_int]
         _lib = lib
     return _lib
@@ -88,6 +90,15 @@ def _p(a: Optional[np.ndarray]):
 
 def _c(a, dtype) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=dtype))
+
+
+def _bias(b, n: int, what: str):
+    if b is None:
+        return None
+    a = _c(b, np.float64).reshape(-1)
+    if a.size != n:
+        raise ValueError("%s needs %d entries" % (what, n))
+    return a
 
 
 def _check(rc: int, what: str):
@@ -144,23 +155,34 @@ def init_params(F: int, O: int, hidden_sizes, seed: int) -> Tuple[np.ndarray, np
     return W1, W2
 
 
+def init_biases(F: int, O: int, hidden_sizes, seed: int) -> Tuple[np.ndarray, np.ndarray]:
+    """b1 [N] and b2 [M, O] (fp32) from the counter-based stream, tags 3 and 4."""
+    hs = _c(hidden_sizes, np.int32)
+    b1 = np.empty(int(hs.sum()), np.float32)
+    b2 = np.empty((len(hs), O), np.float32)
+    _check(_load().orc_init_biases(F, O, len(hs), _p(hs), C.c_uint64(seed), _p(b1), _p(b2)),
+           "init_biases")
+    return b1, b2
+
+
 def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
-            rounding: str = "exact") -> np.ndarray:
-    """logits [B, M, O] in fp64."""
+            rounding: str = "exact", b1=None, b2=None) -> np.ndarray:
+    """logits [B, M, O] in fp64; optional biases b1 [N] and b2 [M, O]."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     B, F = Xf.shape
-    O = W2d.shape[0]
+    O, N = W2d.shape
+    c1, c2 = _bias(b1, N, "b1"), _bias(b2, len(hs) * O, "b2")
     out = np.empty((B, len(hs), O), np.float64)
     with _rounding(rounding):
-        _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf), B,
-                                   _p(out), nthreads), "forward")
+        _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
+                                   _p(c2), _p(Xf), B, _p(out), nthreads), "forward")
     return out
 
 
 def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
               with_allowance: bool = True, nthreads: int = 0, rounding: str = "exact",
-              tie_rel: float = 1e-5, cond_rel: float = 2.4e-7):
+              tie_rel: float = 1e-5, cond_rel: float = 2.4e-7, b1=None, b2=None):
     """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
 
     allow_dW1 bounds what a correct fp32 evaluation may differ by where a
@@ -172,7 +194,8 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     (cond_rel, about 4 units in the last fp32 place, times the excess).
 
     The gradient is that of sum_m L_m, so each model's slice is the gradient
-    of its own mean cross-entropy."""
+    of its own mean cross-entropy.  With biases b1 [N] and b2 [M, O] two more
+    items follow: db1 [N] and db2 [M, O]."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
     B, F = Xf.shape
@@ -181,22 +204,31 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     dW2 = np.empty((O, N), np.float64)
     loss = np.empty(len(hs), np.float64)
     allow = np.empty((N, F), np.float64) if with_allowance else None
+    M = len(hs)
+    c1, c2 = _bias(b1, N, "b1"), _bias(b2, M * O, "b2")
+    db1 = np.empty(N, np.float64) if c1 is not None else None
+    db2 = np.empty((M, O), np.float64) if c2 is not None else None
     with _rounding(rounding):
-        _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
-                                     _p(yi), B, _p(dW1), _p(dW2), _p(loss), _p(allow),
+        _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
+                                     _p(c2), _p(Xf), _p(yi), B, _p(dW1), _p(dW2), _p(db1),
+                                     _p(db2), _p(loss), _p(allow),
                                      float(kink_rel), float(tie_rel), float(cond_rel),
                                      nthreads),
                "gradients")
+    if c1 is not None or c2 is not None:
+        return dW1, dW2, loss, allow, db1, db2
     return dW1, dW2, loss, allow
 
 
 def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
           lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0,
-          rounding: str = "exact", return_ties: bool = False, tie_rel: float = 1e-6):
+          rounding: str = "exact", return_ties: bool = False, tie_rel: float = 1e-6,
+          b1=None, b2=None):
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
-    subset, entries of the other models are NaN.  lr is one rate for all
+    subset, entries of the other models are NaN.  With biases b1 [N] and
+    b2 [M, O], the updated b1' and b2' follow loss_last.  lr is one rate for all
     models or an array of M per-model rates.  With return_ties, a fourth
     item counts per model the value ties met during training (Z within
     tie_rel * sum_f |x w| of a jump of the activation, at that step's
@@ -214,6 +246,9 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     loss = np.full(len(hs), np.nan)
     sel = None if models is None else _c(models, np.int32)
     ties = np.zeros(len(hs), np.int32) if return_ties else None
+    c1, c2 = _bias(b1, N, "b1"), _bias(b2, len(hs) * O, "b2")
+    b1o = np.full(N, np.nan) if c1 is not None else None
+    b2o = np.full((len(hs), O), np.nan) if c2 is not None else None
     lr_arr = np.asarray(lr, np.float64)
     lr_m = None
     if lr_arr.ndim:
@@ -222,18 +257,21 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
             raise ValueError("per-model lr needs one rate per model")
         lr = 0.0
     with _rounding(rounding):
-        _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(Xf),
-                                 _p(yi), len(batches), _p(off), _p(ln), float(lr), _p(lr_m),
-                                 _p(W1o),
-                                 _p(W2o), _p(loss), _p(sel), 0 if sel is None else len(sel),
+        _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
+                                 _p(c2), _p(Xf), _p(yi), len(batches), _p(off), _p(ln),
+                                 float(lr), _p(lr_m), _p(W1o), _p(W2o), _p(b1o), _p(b2o),
+                                 _p(loss), _p(sel), 0 if sel is None else len(sel),
                                  _p(ties), float(tie_rel), nthreads), "train")
+    out = [W1o, W2o, loss]
+    if c1 is not None or c2 is not None:
+        out += [b1o, b2o]
     if return_ties:
-        return W1o, W2o, loss, ties
-    return W1o, W2o, loss
+        out.append(ties)
+    return tuple(out)
 
 
 def hidden(hidden_sizes, act_ids, W1, X,
-           rounding: str = "exact") -> Tuple[np.ndarray, np.ndarray]:
+           rounding: str = "exact", b1=None) -> Tuple[np.ndarray, np.ndarray]:
     """Z = X W1^T and H = act(Z), both [B, N] fp64."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
@@ -242,13 +280,13 @@ def hidden(hidden_sizes, act_ids, W1, X,
     Z = np.empty((B, N), np.float64)
     H = np.empty((B, N), np.float64)
     with _rounding(rounding):
-        _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B, _p(Z), _p(H)),
-               "hidden")
+        _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(_bias(b1, N, "b1")),
+                                  _p(Xf), B, _p(Z), _p(H)), "hidden")
     return Z, H
 
 
 def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
-               rounding: str = "exact") -> np.ndarray:
+               rounding: str = "exact", b1=None) -> np.ndarray:
     """Per-model count of (sample, unit) pairs whose Z sits within rounding
     of a jump of its activation (Hardshrink at +-0.5); models with a nonzero
     count have several correct fp32 results and are left out of comparisons."""
@@ -257,20 +295,25 @@ def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
     B, F = Xf.shape
     counts = np.empty(len(hs), np.int32)
     with _rounding(rounding):
-        _check(_load().orc_value_ties(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(Xf), B,
+        c1 = _bias(b1, W1d.shape[0], "b1")
+        _check(_load().orc_value_ties(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(c1), _p(Xf), B,
                                       float(rel), _p(counts)), "value_ties")
     return counts
 
 
 def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,
-                 nthreads: int = 0, rounding: str = "exact") -> np.ndarray:
+                 nthreads: int = 0, rounding: str = "exact", b1=None,
+                 b2=None) -> np.ndarray:
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
     S, F = Xf.shape
     O = W2d.shape[0]
     loss = np.empty(len(hs), np.float64)
     with _rounding(rounding):
+        c1 = _bias(b1, W2d.shape[1], "b1")
+        c2 = _bias(b2, len(hs) * O, "b2")
         _check(_load().orc_dataset_loss(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d),
-                                        _p(Xf), _p(yi), S, chunk, _p(loss), nthreads),
+                                        _p(c1), _p(c2), _p(Xf), _p(yi), S, chunk, _p(loss),
+                                        nthreads),
                "dataset_loss")
     return loss

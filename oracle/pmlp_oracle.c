@@ -203,6 +203,27 @@ int orc_init_params(int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes
   return ORC_OK;
 }
 
+/* Biases from the same stream: tag 3 for b1 (idx = n, fan_in = F), tag 4
+ * for b2 (idx = m*O + o, fan_in = h_m). */
+int orc_init_biases(int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes,
+                    uint64_t seed, float* b1, float* b2) {
+  if (F < 1 || O < 1 || M < 1 || !hidden_sizes || !b1 || !b2) return ORC_EINVAL;
+  int64_t N = 0;
+  for (int m = 0; m < M; ++m) {
+    if (hidden_sizes[m] < 1) return ORC_EINVAL;
+    N += hidden_sizes[m];
+  }
+  uint64_t key = orc_splitmix64(seed);
+  float bound1 = (float)(1.0 / sqrt((double)F));
+  for (int64_t n = 0; n < N; ++n) b1[n] = orc_uniform_weight(key, 3, (uint64_t)n, bound1);
+  for (int m = 0; m < M; ++m) {
+    float bound2 = (float)(1.0 / sqrt((double)hidden_sizes[m]));
+    for (int o = 0; o < O; ++o)
+      b2[(int64_t)m * O + o] = orc_uniform_weight(key, 4, (uint64_t)((int64_t)m * O + o), bound2);
+  }
+  return ORC_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Operand rounding of the input-layer products.                            */
 /* ------------------------------------------------------------------------ */
@@ -275,18 +296,22 @@ static void orc_scratch_free(orc_scratch* s) {
 }
 
 /* Forward of one standalone MLP (Section 3, three-step procedure):
- *   Z = X W1^T   [B,h]      (input-to-hidden product)
- *   H = act(Z)              (hidden activation)
- *   L = H W2^T   [B,O]      (hidden-to-output product)
- * w1 is the model's [h,F] block, w2 its [O,h] block. */
+ *   Z = X W1^T (+ b1)   [B,h]   (input-to-hidden product)
+ *   H = act(Z)                  (hidden activation)
+ *   L = H W2^T (+ b2)   [B,O]   (hidden-to-output product)
+ * w1 is the model's [h,F] block, w2 its [O,h] block; the biases b1 [h] and
+ * b2 [O] (the paper drops them only to keep the explanation short) are
+ * optional (NULL: none). */
 static void orc_model_forward(const orc_scratch* s, int B, const float* X,
-                              const double* w1, const double* w2) {
+                              const double* w1, const double* w2, const double* b1,
+                              const double* b2) {
   const int F = s->F, O = s->O, h = s->h;
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
       double acc = 0.0;
       for (int f = 0; f < F; ++f)
         acc += orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]);
+      if (b1) acc += b1[j];
       s->Z[(int64_t)b * h + j] = acc;
       s->H[(int64_t)b * h + j] = orc_act(s->act, acc);
     }
@@ -294,6 +319,7 @@ static void orc_model_forward(const orc_scratch* s, int B, const float* X,
     for (int o = 0; o < O; ++o) {
       double acc = 0.0;
       for (int j = 0; j < h; ++j) acc += s->H[(int64_t)b * h + j] * w2[(int64_t)o * h + j];
+      if (b2) acc += b2[o];
       s->L[(int64_t)b * O + o] = acc;
     }
 }
@@ -326,7 +352,8 @@ static double orc_model_ce(const orc_scratch* s, int B, const int32_t* y) {
  *   dZ  = dH * act'(Z)
  *   dW1 = dZ^T X       [h,F]                                              */
 static void orc_model_backward(const orc_scratch* s, int B, const float* X,
-                               const double* w2, double* dw1, double* dw2) {
+                               const double* w2, double* dw1, double* dw2, double* db1,
+                               double* db2) {
   const int F = s->F, O = s->O, h = s->h;
   for (int o = 0; o < O; ++o)
     for (int j = 0; j < h; ++j) {
@@ -348,6 +375,19 @@ static void orc_model_backward(const orc_scratch* s, int B, const float* X,
         acc += orc_in(s->dZ[(int64_t)b * h + j]) * orc_in(X[(int64_t)b * F + f]);
       dw1[(int64_t)j * F + f] = acc;
     }
+  /* biases: db1 = sum_b dZ, db2 = sum_b G */
+  if (db1)
+    for (int j = 0; j < h; ++j) {
+      double acc = 0.0;
+      for (int b = 0; b < B; ++b) acc += s->dZ[(int64_t)b * h + j];
+      db1[j] = acc;
+    }
+  if (db2)
+    for (int o = 0; o < O; ++o) {
+      double acc = 0.0;
+      for (int b = 0; b < B; ++b) acc += s->G[(int64_t)b * O + o];
+      db2[o] = acc;
+    }
 }
 
 /* Kink allowance for piecewise-linear activations.  When |Z| lies within
@@ -356,7 +396,8 @@ static void orc_model_backward(const orc_scratch* s, int B, const float* X,
  * move by at most
  *   allow[j,f] = sum over such b of |dH[b,j]| * slope_jump * |X[b,f]|.     */
 static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
-                                 const double* w1, double* allow, double kink_rel) {
+                                 const double* w1, const double* b1, double* allow,
+                                 double kink_rel) {
   const int F = s->F, h = s->h;
   double jump = orc_kink_jump(s->act);
   for (int64_t i = 0; i < (int64_t)h * F; ++i) allow[i] = 0.0;
@@ -366,6 +407,7 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
       double mag = 0.0;
       for (int f = 0; f < F; ++f)
         mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
+      if (b1) mag += fabs(b1[j]);
       double z = s->Z[(int64_t)b * h + j];
       if (orc_kink_dist(s->act, z) <= kink_rel * mag) {
         double d = fabs(s->dH[(int64_t)b * h + j]) * jump;
@@ -378,7 +420,7 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
 /* Number of samples b and units j of one model whose Z lies within
  * rel * sum_f |x_f w_f| of a jump of the activation (Hardshrink at +-0.5). */
 static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
-                                    const double* w1, double rel) {
+                                    const double* w1, const double* b1, double rel) {
   if (s->act != 11) return 0;
   const int F = s->F, h = s->h;
   int32_t n = 0;
@@ -387,6 +429,7 @@ static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
       double mag = 0.0;
       for (int f = 0; f < F; ++f)
         mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
+      if (b1) mag += fabs(b1[j]);
       if (fabs(fabs(s->Z[(int64_t)b * h + j]) - 0.5) <= rel * mag) ++n;
     }
   return n;
@@ -517,8 +560,8 @@ int orc_max_threads(void) {
 /* Forward only: logits [B,M,O] (model-major inside each sample row), the
  * layout of the Scatter Add result Y[batch, model, out] of Section 3. */
 int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
-                const double* W1, const double* W2, const float* X, int32_t B,
-                double* logits, int nthreads) {
+                const double* W1, const double* W2, const double* b1, const double* b2,
+                const float* X, int32_t B, double* logits, int nthreads) {
   if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !logits) return ORC_EINVAL;
   int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
   if (!off) return ORC_ENOMEM;
@@ -536,7 +579,7 @@ int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_
       err = ORC_ENOMEM;
     } else {
       orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
-      orc_model_forward(&s, B, X, w1, w2);
+      orc_model_forward(&s, B, X, w1, w2, b1 ? b1 + off[m] : NULL, b2 ? b2 + (int64_t)m * O : NULL);
       for (int b = 0; b < B; ++b)
         for (int o = 0; o < O; ++o)
           logits[((int64_t)b * M + m) * O + o] = s.L[(int64_t)b * O + o];
@@ -555,8 +598,9 @@ int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_
  * in the bf16 operand mode the rounding-tie allowance with tie_rel, plus the
  * cancellation allowance of dH with cond_rel (0 switches it off). */
 int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
-                  const double* W1, const double* W2, const float* X, const int32_t* y,
-                  int32_t B, double* dW1, double* dW2, double* loss, double* allow_dW1,
+                  const double* W1, const double* W2, const double* b1, const double* b2,
+                  const float* X, const int32_t* y, int32_t B, double* dW1, double* dW2,
+                  double* db1, double* db2, double* loss, double* allow_dW1,
                   double kink_rel, double tie_rel, double cond_rel, int nthreads) {
   if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !y || !dW1 || !dW2 || !loss)
     return ORC_EINVAL;
@@ -580,12 +624,14 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
       err = ORC_ENOMEM;
     } else {
       orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
-      orc_model_forward(&s, B, X, w1, w2);
+      const double* bm1 = b1 ? b1 + off[m] : NULL;
+      orc_model_forward(&s, B, X, w1, w2, bm1, b2 ? b2 + (int64_t)m * O : NULL);
       loss[m] = orc_model_ce(&s, B, y);
-      orc_model_backward(&s, B, X, w2, g1, g2);
+      orc_model_backward(&s, B, X, w2, g1, g2, db1 ? db1 + off[m] : NULL,
+                         db2 ? db2 + (int64_t)m * O : NULL);
       orc_put(N, F, O, off[m], h, g1, g2, dW1, dW2);
       if (al) {
-        orc_model_kink_allow(&s, B, X, w1, al, kink_rel);
+        orc_model_kink_allow(&s, B, X, w1, bm1, al, kink_rel);
         if (orc_rounding) orc_model_tie_allow(&s, B, X, w2, al, tie_rel);
         if (cond_rel > 0.0) orc_model_cond_allow(&s, B, X, y, w2, al, cond_rel);
         memcpy(allow_dW1 + off[m] * F, al, sizeof(double) * (size_t)h * F);
@@ -609,10 +655,11 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
  * receives each model's loss on the last batch, before that batch's
  * update.  models/nmodels select a subset of the models (NULL: all).      */
 int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
-              const double* W1, const double* W2, const float* X, const int32_t* y,
+              const double* W1, const double* W2, const double* b1, const double* b2,
+              const float* X, const int32_t* y,
               int32_t nbatches, const int64_t* batch_off, const int32_t* batch_len,
               double lr, const double* lr_model, double* W1_out, double* W2_out,
-              double* loss_last,
+              double* b1_out, double* b2_out, double* loss_last,
               const int32_t* models, int32_t nmodels, int32_t* ties, double tie_rel,
               int nthreads) {
   if (orc_check(F, O, M, hs, acts) || nbatches < 0 || !W1 || !W2 || !X || !y ||
@@ -642,28 +689,40 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
     double* w2 = (double*)malloc(sizeof(double) * (size_t)h * O);
     double* g1 = (double*)malloc(sizeof(double) * (size_t)h * F);
     double* g2 = (double*)malloc(sizeof(double) * (size_t)h * O);
-    if (!w1 || !w2 || !g1 || !g2 || orc_scratch_alloc(&s, Bmax, h, F, O, acts[m])) {
+    /* the model's biases (updated in place) and their gradients */
+    double* c1 = b1 ? (double*)malloc(sizeof(double) * (size_t)h * 2) : NULL;
+    double* c2 = b2 ? (double*)malloc(sizeof(double) * (size_t)O * 2) : NULL;
+    if (!w1 || !w2 || !g1 || !g2 || (b1 && !c1) || (b2 && !c2) ||
+        orc_scratch_alloc(&s, Bmax, h, F, O, acts[m])) {
       err = ORC_ENOMEM;
     } else {
       orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
+      if (c1) memcpy(c1, b1 + off[m], sizeof(double) * (size_t)h);
+      if (c2) memcpy(c2, b2 + (int64_t)m * O, sizeof(double) * (size_t)O);
       double last = NAN;
       for (int k = 0; k < nbatches; ++k) {
         const float* Xb = X + batch_off[k] * F;
         const int32_t* yb = y + batch_off[k];
         const int B = batch_len[k];
-        orc_model_forward(&s, B, Xb, w1, w2);
+        orc_model_forward(&s, B, Xb, w1, w2, c1, c2);
         last = orc_model_ce(&s, B, yb);
-        if (ties) ties[m] += orc_model_value_ties(&s, B, Xb, w1, tie_rel);
-        orc_model_backward(&s, B, Xb, w2, g1, g2);
+        if (ties) ties[m] += orc_model_value_ties(&s, B, Xb, w1, c1, tie_rel);
+        orc_model_backward(&s, B, Xb, w2, g1, g2, c1 ? c1 + h : NULL, c2 ? c2 + O : NULL);
         const double lm = lr_model ? lr_model[m] : lr;
         for (int64_t t = 0; t < (int64_t)h * F; ++t) w1[t] -= lm * g1[t];
         for (int64_t t = 0; t < (int64_t)h * O; ++t) w2[t] -= lm * g2[t];
+        if (c1)
+          for (int j = 0; j < h; ++j) c1[j] -= lm * c1[h + j];
+        if (c2)
+          for (int o = 0; o < O; ++o) c2[o] -= lm * c2[O + o];
       }
       if (loss_last) loss_last[m] = last;
       orc_put(N, F, O, off[m], h, w1, w2, W1_out, W2_out);
+      if (c1 && b1_out) memcpy(b1_out + off[m], c1, sizeof(double) * (size_t)h);
+      if (c2 && b2_out) memcpy(b2_out + (int64_t)m * O, c2, sizeof(double) * (size_t)O);
     }
     orc_scratch_free(&s);
-    free(w1); free(w2); free(g1); free(g2);
+    free(w1); free(w2); free(g1); free(g2); free(c1); free(c2);
   }
   free(off);
   return err;
@@ -674,7 +733,8 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
  * its own model's activation): Z [B,N] = X W1^T and H [B,N] = act(Z),
  * both fp64, sample-major. */
 int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
-               const double* W1, const float* X, int32_t B, double* Z, double* H) {
+               const double* W1, const double* b1, const float* X, int32_t B, double* Z,
+               double* H) {
   if (F < 1 || M < 1 || !hs || !acts || !W1 || !X || B < 1 || !Z || !H) return ORC_EINVAL;
   int64_t N = 0;
   for (int m = 0; m < M; ++m) {
@@ -687,6 +747,7 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
       for (int b = 0; b < B; ++b) {
         double acc = 0.0;
         for (int f = 0; f < F; ++f) acc += orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]);
+        if (b1) acc += b1[n];
         Z[(int64_t)b * N + n] = acc;
         H[(int64_t)b * N + n] = orc_act(acts[m], acc);
       }
@@ -702,7 +763,8 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
  * then differs by the size of the jump; a comparison leaves such models out
  * (several results are correct for them). */
 int orc_value_ties(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
-                   const double* W1, const float* X, int32_t B, double rel, int32_t* counts) {
+                   const double* W1, const double* b1, const float* X, int32_t B, double rel,
+                   int32_t* counts) {
   if (F < 1 || M < 1 || !hs || !acts || !W1 || !X || B < 1 || !counts) return ORC_EINVAL;
   int64_t n = 0;
   for (int m = 0; m < M; ++m) {
@@ -717,6 +779,10 @@ int orc_value_ties(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
           acc += t;
           mag += fabs(t);
         }
+        if (b1) {
+          acc += b1[n];
+          mag += fabs(b1[n]);
+        }
         if (fabs(fabs(acc) - 0.5) <= rel * mag) counts[m] += 1;
       }
     }
@@ -727,8 +793,9 @@ int orc_value_ties(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
 /* Mean cross-entropy of every model over a whole sample set (no update),
  * evaluated in chunks of at most chunk samples. */
 int orc_dataset_loss(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
-                     const double* W1, const double* W2, const float* X, const int32_t* y,
-                     int64_t S, int32_t chunk, double* loss, int nthreads) {
+                     const double* W1, const double* W2, const double* b1, const double* b2,
+                     const float* X, const int32_t* y, int64_t S, int32_t chunk, double* loss,
+                     int nthreads) {
   if (orc_check(F, O, M, hs, acts) || S < 1 || chunk < 1 || !W1 || !W2 || !X || !y || !loss)
     return ORC_EINVAL;
   int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
@@ -750,7 +817,8 @@ int orc_dataset_loss(int32_t F, int32_t O, int32_t M, const int32_t* hs, const i
       double total = 0.0;
       for (int64_t s0 = 0; s0 < S; s0 += chunk) {
         int B = (int)((S - s0) < chunk ? (S - s0) : chunk);
-        orc_model_forward(&s, B, X + s0 * F, w1, w2);
+        orc_model_forward(&s, B, X + s0 * F, w1, w2, b1 ? b1 + off[m] : NULL,
+                          b2 ? b2 + (int64_t)m * O : NULL);
         total += orc_model_ce(&s, B, y + s0) * B;
       }
       loss[m] = total / (double)S;
