@@ -34,7 +34,9 @@
  * Optional operand rounding of the two input-layer products (Z = X W1^T and
  * dW1 = dZ^T X) emulates the bf16-in / fp32-accumulate variant: X, W1 and
  * dZ are first taken to fp32 and then to the nearest bfloat16 (ties to
- * even) before they are multiplied; everything else stays fp64.
+ * even) before they are multiplied; everything else stays fp64.  A hidden
+ * bias is the weight of a constant input 1, so in that variant it is rounded
+ * like W1, and db1 sums the rounded dZ.
  *
  * Parity pins (see tests/test_oracle_*.py): the Scatter Add worked example of
  * Section 3, the 4-1-2 + 4-2-2 packing example of Section 3, closed forms for
@@ -311,7 +313,7 @@ static void orc_model_forward(const orc_scratch* s, int B, const float* X,
       double acc = 0.0;
       for (int f = 0; f < F; ++f)
         acc += orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]);
-      if (b1) acc += b1[j];
+      if (b1) acc += orc_in(b1[j]);   /* the weight of a constant input 1 */
       s->Z[(int64_t)b * h + j] = acc;
       s->H[(int64_t)b * h + j] = orc_act(s->act, acc);
     }
@@ -379,7 +381,7 @@ static void orc_model_backward(const orc_scratch* s, int B, const float* X,
   if (db1)
     for (int j = 0; j < h; ++j) {
       double acc = 0.0;
-      for (int b = 0; b < B; ++b) acc += s->dZ[(int64_t)b * h + j];
+      for (int b = 0; b < B; ++b) acc += orc_in(s->dZ[(int64_t)b * h + j]);
       db1[j] = acc;
     }
   if (db2)
@@ -407,7 +409,7 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
       double mag = 0.0;
       for (int f = 0; f < F; ++f)
         mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
-      if (b1) mag += fabs(b1[j]);
+      if (b1) mag += fabs(orc_in(b1[j]));
       double z = s->Z[(int64_t)b * h + j];
       if (orc_kink_dist(s->act, z) <= kink_rel * mag) {
         double d = fabs(s->dH[(int64_t)b * h + j]) * jump;
@@ -429,7 +431,7 @@ static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
       double mag = 0.0;
       for (int f = 0; f < F; ++f)
         mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
-      if (b1) mag += fabs(b1[j]);
+      if (b1) mag += fabs(orc_in(b1[j]));
       if (fabs(fabs(s->Z[(int64_t)b * h + j]) - 0.5) <= rel * mag) ++n;
     }
   return n;
@@ -747,7 +749,7 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
       for (int b = 0; b < B; ++b) {
         double acc = 0.0;
         for (int f = 0; f < F; ++f) acc += orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]);
-        if (b1) acc += b1[n];
+        if (b1) acc += orc_in(b1[n]);
         Z[(int64_t)b * N + n] = acc;
         H[(int64_t)b * N + n] = orc_act(acts[m], acc);
       }
@@ -780,8 +782,8 @@ int orc_value_ties(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
           mag += fabs(t);
         }
         if (b1) {
-          acc += b1[n];
-          mag += fabs(b1[n]);
+          acc += orc_in(b1[n]);
+          mag += fabs(orc_in(b1[n]));
         }
         if (fabs(fabs(acc) - 0.5) <= rel * mag) counts[m] += 1;
       }

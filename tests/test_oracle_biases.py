@@ -120,3 +120,24 @@ def test_bias_init_follows_counter_definition(orc):
     for m in range(3):
         for o in range(O):
             assert b2[m, o] == draw(4, m * O + o, hs[m])
+
+
+def test_bf16_mode_treats_b1_as_a_weight_of_a_constant_input(orc):
+    """In the bf16 operand mode, b1 is the weight of an input fixed at 1: the
+    results equal those of the no-bias network with X extended by a column
+    of ones and W1 by the column b1."""
+    hs, acts, X, y, W1, W2, b1, b2 = _problem(6)
+    Xe = np.concatenate([X, np.ones((X.shape[0], 1), np.float32)], axis=1)
+    W1e = np.concatenate([W1, b1[:, None]], axis=1)
+    for rnd in ("exact", "bf16"):
+        got = orc.forward(hs, acts, W1, W2, X, b1=b1, b2=b2, rounding=rnd)
+        want = orc.forward(hs, acts, W1e, W2, Xe, rounding=rnd) + b2[None]
+        np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+        g = orc.gradients(hs, acts, W1, W2, X, y, b1=b1, b2=b2, rounding=rnd)
+        # the extended net's W1 gradient holds db1 in its last column (b2 adds
+        # the same shift to every logit of a model in both nets only when b2 = 0)
+        ge = orc.gradients(hs, acts, W1e, W2, Xe, y, rounding=rnd)
+        gz = orc.gradients(hs, acts, W1, W2, X, y, b1=b1, b2=np.zeros_like(b2), rounding=rnd)
+        np.testing.assert_allclose(gz[0], ge[0][:, :-1], rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(gz[4], ge[0][:, -1], rtol=1e-12, atol=1e-15)
+        assert g[4].shape == b1.shape
