@@ -63,7 +63,7 @@ def _load():
         lib.orc_forward.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, i32, P, C.c_int]
         lib.orc_gradients.restype = C.c_int
         lib.orc_gradients.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32,
-                                      P, P, P, P, P, P, dbl, dbl, dbl, C.c_int]
+                                      P, P, P, P, P, P, P, dbl, dbl, dbl, C.c_int]
         lib.orc_train.restype = C.c_int
         lib.orc_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32, P, P,
                                   dbl, P, P, P, P, P, P, P, i32, P, dbl, C.c_int]
@@ -194,8 +194,9 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     (cond_rel, about 4 units in the last fp32 place, times the excess).
 
     The gradient is that of sum_m L_m, so each model's slice is the gradient
-    of its own mean cross-entropy.  With biases b1 [N] and b2 [M, O] two more
-    items follow: db1 [N] and db2 [M, O]."""
+    of its own mean cross-entropy.  With biases b1 [N] and b2 [M, O] three more
+    items follow: db1 [N], db2 [M, O] and the allowance of db1 [N] (that of a
+    weight whose input is fixed at 1)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
     B, F = Xf.shape
@@ -208,15 +209,16 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     c1, c2 = _bias(b1, N, "b1"), _bias(b2, M * O, "b2")
     db1 = np.empty(N, np.float64) if c1 is not None else None
     db2 = np.empty((M, O), np.float64) if c2 is not None else None
+    allow_b = np.empty(N, np.float64) if (with_allowance and c1 is not None) else None
     with _rounding(rounding):
         _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                      _p(c2), _p(Xf), _p(yi), B, _p(dW1), _p(dW2), _p(db1),
-                                     _p(db2), _p(loss), _p(allow),
+                                     _p(db2), _p(loss), _p(allow), _p(allow_b),
                                      float(kink_rel), float(tie_rel), float(cond_rel),
                                      nthreads),
                "gradients")
     if c1 is not None or c2 is not None:
-        return dW1, dW2, loss, allow, db1, db2
+        return dW1, dW2, loss, allow, db1, db2, allow_b
     return dW1, dW2, loss, allow
 
 

@@ -399,10 +399,12 @@ static void orc_model_backward(const orc_scratch* s, int B, const float* X,
  *   allow[j,f] = sum over such b of |dH[b,j]| * slope_jump * |X[b,f]|.     */
 static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
                                  const double* w1, const double* b1, double* allow,
-                                 double kink_rel) {
+                                 double* allow_b, double kink_rel) {
   const int F = s->F, h = s->h;
   double jump = orc_kink_jump(s->act);
   for (int64_t i = 0; i < (int64_t)h * F; ++i) allow[i] = 0.0;
+  if (allow_b)
+    for (int j = 0; j < h; ++j) allow_b[j] = 0.0;
   if (jump == 0.0) return;
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
@@ -415,6 +417,7 @@ static void orc_model_kink_allow(const orc_scratch* s, int B, const float* X,
         double d = fabs(s->dH[(int64_t)b * h + j]) * jump;
         for (int f = 0; f < F; ++f)
           allow[(int64_t)j * F + f] += d * fabs(orc_in(X[(int64_t)b * F + f]));
+        if (allow_b) allow_b[j] += d;   /* the bias: an input fixed at 1 */
       }
     }
 }
@@ -448,7 +451,7 @@ static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
  * summed over b (nothing where dH does not cancel). */
 static void orc_model_cond_allow(const orc_scratch* s, int B, const float* X,
                                  const int32_t* y, const double* w2, double* allow,
-                                 double cond_rel) {
+                                 double* allow_b, double cond_rel) {
   const int F = s->F, O = s->O, h = s->h;
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
@@ -463,6 +466,7 @@ static void orc_model_cond_allow(const orc_scratch* s, int B, const float* X,
       const double d = cond_rel * excess * fabs(orc_act_deriv(s->act, s->Z[(int64_t)b * h + j]));
       for (int f = 0; f < F; ++f)
         allow[(int64_t)j * F + f] += d * fabs(orc_in(X[(int64_t)b * F + f]));
+      if (allow_b) allow_b[j] += d;
     }
 }
 
@@ -477,7 +481,8 @@ static void orc_model_cond_allow(const orc_scratch* s, int B, const float* X,
  * at most
  *   allow[j,f] += (the larger bfloat16 spacing next to dZ) * |X[b,f]|.     */
 static void orc_model_tie_allow(const orc_scratch* s, int B, const float* X,
-                                const double* w2, double* allow, double tie_rel) {
+                                const double* w2, double* allow, double* allow_b,
+                                double tie_rel) {
   const int F = s->F, O = s->O, h = s->h;
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
@@ -503,6 +508,7 @@ static void orc_model_tie_allow(const orc_scratch* s, int B, const float* X,
         const double gap = fmax(fabs((double)up) - ar, ar - fabs((double)dn));
         for (int f = 0; f < F; ++f)
           allow[(int64_t)j * F + f] += gap * fabs(orc_in(X[(int64_t)b * F + f]));
+        if (allow_b) allow_b[j] += gap;
       }
     }
 }
@@ -603,7 +609,8 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
                   const double* W1, const double* W2, const double* b1, const double* b2,
                   const float* X, const int32_t* y, int32_t B, double* dW1, double* dW2,
                   double* db1, double* db2, double* loss, double* allow_dW1,
-                  double kink_rel, double tie_rel, double cond_rel, int nthreads) {
+                  double* allow_db1, double kink_rel, double tie_rel, double cond_rel,
+                  int nthreads) {
   if (orc_check(F, O, M, hs, acts) || B < 1 || !W1 || !W2 || !X || !y || !dW1 || !dW2 || !loss)
     return ORC_EINVAL;
   int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (M + 1));
@@ -633,9 +640,10 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
                          db2 ? db2 + (int64_t)m * O : NULL);
       orc_put(N, F, O, off[m], h, g1, g2, dW1, dW2);
       if (al) {
-        orc_model_kink_allow(&s, B, X, w1, bm1, al, kink_rel);
-        if (orc_rounding) orc_model_tie_allow(&s, B, X, w2, al, tie_rel);
-        if (cond_rel > 0.0) orc_model_cond_allow(&s, B, X, y, w2, al, cond_rel);
+        double* ab = allow_db1 ? allow_db1 + off[m] : NULL;
+        orc_model_kink_allow(&s, B, X, w1, bm1, al, ab, kink_rel);
+        if (orc_rounding) orc_model_tie_allow(&s, B, X, w2, al, ab, tie_rel);
+        if (cond_rel > 0.0) orc_model_cond_allow(&s, B, X, y, w2, al, ab, cond_rel);
         memcpy(allow_dW1 + off[m] * F, al, sizeof(double) * (size_t)h * F);
       }
     }

@@ -57,7 +57,7 @@ def test_db2_closed_form_with_zero_output_weights(orc):
     so db2[m, o] = (B/O - #{b: y_b = o}) / B and db1 = 0."""
     hs, acts, X, y, W1, W2, b1, b2 = _problem(3)
     O, B = W2.shape[0], X.shape[0]
-    _, _, loss, _, db1, db2 = orc.gradients(hs, acts, W1, np.zeros_like(W2), X, y,
+    _, _, loss, _, db1, db2, _ = orc.gradients(hs, acts, W1, np.zeros_like(W2), X, y,
                                             b1=b1, b2=np.zeros_like(b2))
     want = (B / O - np.bincount(y, minlength=O)) / B
     np.testing.assert_allclose(db2, np.tile(want, (len(hs), 1)), rtol=0, atol=1e-15)
@@ -72,7 +72,7 @@ def test_bias_gradients_match_finite_differences(orc):
     unit_act = np.repeat(acts, hs)
     dist = np.where(unit_act == 11, np.abs(np.abs(Z) - 0.5), np.abs(Z))
     assert dist[:, np.isin(unit_act, (1, 5, 10, 11))].min() > 1e-3   # away from kinks
-    _, _, _, _, db1, db2 = orc.gradients(hs, acts, W1, W2, X, y, b1=b1, b2=b2)
+    _, _, _, _, db1, db2, _ = orc.gradients(hs, acts, W1, W2, X, y, b1=b1, b2=b2)
 
     def total(c1, c2):
         return orc.gradients(hs, acts, W1, W2, X, y, b1=c1, b2=c2, with_allowance=False)[2].sum()
@@ -141,3 +141,20 @@ def test_bf16_mode_treats_b1_as_a_weight_of_a_constant_input(orc):
         np.testing.assert_allclose(gz[0], ge[0][:, :-1], rtol=1e-12, atol=1e-15)
         np.testing.assert_allclose(gz[4], ge[0][:, -1], rtol=1e-12, atol=1e-15)
         assert g[4].shape == b1.shape
+
+
+def test_db1_allowance_is_that_of_a_constant_input(orc):
+    """The allowance of db1 equals the dW1 allowance of the extra column of
+    an equivalent network whose input carries a column of ones (b2 = 0)."""
+    rng = np.random.default_rng(8)
+    hs, acts, X, y, W1, W2, b1, b2 = _problem(8, M=6, hmax=5, F=3, O=2, B=6)
+    acts = np.array([1, 5, 10, 11, 1, 5], np.int32)
+    X[0] = [1.0, 1.0, 1.0]
+    W1[:, :] = 0.1
+    b1[:] = -0.3                      # Z[0] = 0 on every unit: kinks at 0 are hit
+    Xe = np.concatenate([X, np.ones((6, 1), np.float32)], axis=1)
+    W1e = np.concatenate([W1, b1[:, None]], axis=1)
+    g = orc.gradients(hs, acts, W1, W2, X, y, b1=b1, b2=np.zeros_like(b2))
+    ge = orc.gradients(hs, acts, W1e, W2, Xe, y)
+    np.testing.assert_allclose(g[6], ge[3][:, -1], rtol=1e-12, atol=1e-18)
+    assert g[6].max() > 0
