@@ -74,6 +74,10 @@ extern "C" {
 
 #define PMLP_NUM_ACTS 13
 
+#define PMLP_BIAS 1       /* pmlp_create_ex flag: hidden biases b1 [N] and output
+                             biases b2 [M, O] (Section 3 drops them only to keep
+                             the explanation short) */
+
 typedef struct pmlp* pmlp_t;
 
 /* Create a packed model of M MLPs with F inputs and O outputs each.
@@ -91,6 +95,18 @@ typedef struct pmlp* pmlp_t;
 int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M,
                 const int32_t* hidden_sizes, const int32_t* act_ids,
                 uint64_t seed);
+
+/* pmlp_create with flags (0 or PMLP_BIAS).  With PMLP_BIAS every model
+ * computes Z = X W1^T + b1 and logits = act(Z) W2^T + b2, trains b1 and b2
+ * by the same SGD (db1 = sum_b dZ, db2 = sum_b G), and the biases start
+ * uniform in (-1/sqrt(fan_in), +1/sqrt(fan_in)) from the same stream as the
+ * weights: tag 3 for b1 (idx = n, fan_in = F), tag 4 for b2 (idx = m*O + o,
+ * fan_in = h_m).  b1 is stored as the weight of a constant input 1, so in
+ * the PMLP_BF16_GEMM mode it is rounded with W1.  Unknown flags return
+ * PMLP_EINVAL. */
+int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M,
+                   const int32_t* hidden_sizes, const int32_t* act_ids,
+                   uint64_t seed, int32_t flags);
 
 /* Free the handle and every device buffer it owns (synchronises its
  * stream first).  A null handle is accepted. */
@@ -149,6 +165,13 @@ int pmlp_losses(pmlp_t h, float* out_host);
 int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev,
                    int32_t B, float* dW1_dev, float* dW2_dev);
 
+/* pmlp_gradients of a handle with biases, which also stores db1_dev [N]
+ * and db2_dev [M, O] (device, fp32).  PMLP_ESTATE for a handle without
+ * biases; null pointers return PMLP_EINVAL. */
+int pmlp_gradients_ex(pmlp_t h, const float* X_dev, const int32_t* y_dev,
+                      int32_t B, float* dW1_dev, float* dW2_dev,
+                      float* db1_dev, float* db2_dev);
+
 /* Hidden layer of the packed network: Z_dev [B, N] = X W1^T and
  * H_dev [B, N] = act_{model of n}(Z) (either pointer may be null).  A
  * view of the first two forward steps for inspection and testing. */
@@ -160,6 +183,12 @@ int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev,
  * may be null to skip that tensor. */
 int pmlp_get_params(pmlp_t h, float* W1_host, float* W2_host);
 int pmlp_set_params(pmlp_t h, const float* W1_host, const float* W2_host);
+
+/* Biases of a handle created with PMLP_BIAS (PMLP_ESTATE otherwise):
+ * b1_host [N], b2_host [M, O] (model-major), host memory, either may be
+ * null.  Synchronise the handle's stream. */
+int pmlp_get_biases(pmlp_t h, float* b1_host, float* b2_host);
+int pmlp_set_biases(pmlp_t h, const float* b1_host, const float* b2_host);
 
 /* Sizes of the packed model; any output pointer may be null. */
 int pmlp_info(pmlp_t h, int64_t* N, int32_t* M, int32_t* F, int32_t* O);

@@ -18,13 +18,13 @@ import numpy as np
 
 __all__ = [
     "PMLP_OK", "PMLP_EINVAL", "PMLP_ENOMEM", "PMLP_EDEVICE", "PMLP_ESTATE",
-    "PMLP_FP32", "PMLP_BF16_GEMM", "PMLP_NUM_KERNELS", "ACT_IDS", "PmlpError",
+    "PMLP_FP32", "PMLP_BF16_GEMM", "PMLP_BIAS", "PMLP_NUM_KERNELS", "ACT_IDS", "PmlpError",
     "library_path", "load_library", "pmlp_create", "pmlp_destroy", "pmlp_set_stream",
     "pmlp_set_precision", "pmlp_forward", "pmlp_train_step", "pmlp_train_step_lr",
     "pmlp_losses",
     "pmlp_gradients", "pmlp_hidden", "pmlp_get_params", "pmlp_set_params", "pmlp_info",
     "pmlp_set_profiling", "pmlp_kernel_time", "pmlp_profile_reset", "pmlp_kernel_name",
-    "pmlp_last_error", "PackedMLP",
+    "pmlp_last_error", "pmlp_gradients_ex", "pmlp_get_biases", "pmlp_set_biases", "PackedMLP",
 ]
 
 PMLP_OK = 0
@@ -34,6 +34,7 @@ PMLP_EDEVICE = -3
 PMLP_ESTATE = -4
 PMLP_FP32 = 0
 PMLP_BF16_GEMM = 1
+PMLP_BIAS = 1
 PMLP_NUM_KERNELS = 9
 
 ACT_IDS = {
@@ -68,6 +69,10 @@ def load_library():
     P, i32, i64, u64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_float
     sig = {
         "pmlp_create": [C.POINTER(P), i32, i32, i32, P, P, u64],
+        "pmlp_create_ex": [C.POINTER(P), i32, i32, i32, P, P, u64, i32],
+        "pmlp_gradients_ex": [P, P, P, i32, P, P, P, P],
+        "pmlp_get_biases": [P, P, P],
+        "pmlp_set_biases": [P, P, P],
         "pmlp_destroy": [P],
         "pmlp_set_stream": [P, P],
         "pmlp_set_precision": [P, i32],
@@ -126,16 +131,37 @@ def _ptr(x) -> Optional[int]:
 # --- raw C ABI (device pointers as integers) ------------------------------
 
 def pmlp_create(F: int, O: int, hidden_sizes: Sequence[int], act_ids: Sequence[int],
-                seed: int) -> int:
+                seed: int, flags: int = 0) -> int:
     hs = _host(hidden_sizes, np.int32)
     ac = _host(act_ids, np.int32)
     if hs.shape != ac.shape or hs.ndim != 1:
         raise ValueError("hidden_sizes and act_ids must be 1-D of equal length")
     h = C.c_void_p()
-    _check(load_library().pmlp_create(C.byref(h), int(F), int(O), int(hs.size),
-                                      hs.ctypes.data, ac.ctypes.data,
-                                      int(seed) & 0xFFFFFFFFFFFFFFFF), "pmlp_create")
+    _check(load_library().pmlp_create_ex(C.byref(h), int(F), int(O), int(hs.size),
+                                         hs.ctypes.data, ac.ctypes.data,
+                                         int(seed) & 0xFFFFFFFFFFFFFFFF, int(flags)),
+           "pmlp_create_ex")
     return h.value
+
+
+def pmlp_gradients_ex(h: int, X, y, B: int, dW1, dW2, db1, db2) -> None:
+    _check(load_library().pmlp_gradients_ex(h, _ptr(X), _ptr(y), int(B), _ptr(dW1), _ptr(dW2),
+                                            _ptr(db1), _ptr(db2)), "pmlp_gradients_ex")
+
+
+def pmlp_get_biases(h: int, N: int, M: int, O: int) -> Tuple[np.ndarray, np.ndarray]:
+    b1 = np.empty(N, np.float32)
+    b2 = np.empty((M, O), np.float32)
+    _check(load_library().pmlp_get_biases(h, b1.ctypes.data, b2.ctypes.data), "pmlp_get_biases")
+    return b1, b2
+
+
+def pmlp_set_biases(h: int, b1=None, b2=None) -> None:
+    c1 = None if b1 is None else _host(b1, np.float32)
+    c2 = None if b2 is None else _host(b2, np.float32)
+    _check(load_library().pmlp_set_biases(h, None if c1 is None else c1.ctypes.data,
+                                          None if c2 is None else c2.ctypes.data),
+           "pmlp_set_biases")
 
 
 def pmlp_destroy(h: int) -> None:
@@ -236,11 +262,13 @@ class PackedMLP:
     is enqueued on torch's current stream of that device."""
 
     def __init__(self, F: int, O: int, hidden_sizes: Sequence[int], act_ids: Sequence[int],
-                 seed: int = 0, precision: int = PMLP_FP32):
+                 seed: int = 0, precision: int = PMLP_FP32, biases: bool = False):
         import torch
         self._torch = torch
         self.device = torch.device("cuda", torch.cuda.current_device())
-        self.handle = pmlp_create(F, O, hidden_sizes, act_ids, seed)
+        self.biases = bool(biases)
+        self.handle = pmlp_create(F, O, hidden_sizes, act_ids, seed,
+                                  PMLP_BIAS if biases else 0)
         self.N, self.M, self.F, self.O = pmlp_info(self.handle)
         self.hidden_sizes = _host(hidden_sizes, np.int32)
         self.act_ids = _host(act_ids, np.int32)
@@ -311,8 +339,13 @@ class PackedMLP:
         dW1 = t.empty((self.N, self.F), dtype=t.float32, device=self.device)
         dW2 = t.empty((self.O, self.N), dtype=t.float32, device=self.device)
         self._stream()
-        pmlp_gradients(self.handle, X, y, B, dW1, dW2)
-        return dW1, dW2
+        if not self.biases:
+            pmlp_gradients(self.handle, X, y, B, dW1, dW2)
+            return dW1, dW2
+        db1 = t.empty(self.N, dtype=t.float32, device=self.device)
+        db2 = t.empty((self.M, self.O), dtype=t.float32, device=self.device)
+        pmlp_gradients_ex(self.handle, X, y, B, dW1, dW2, db1, db2)
+        return dW1, dW2, db1, db2
 
     def hidden(self, X):
         B = self._x(X)
@@ -331,6 +364,13 @@ class PackedMLP:
 
     def set_params(self, W1=None, W2=None) -> None:
         pmlp_set_params(self.handle, W1, W2)
+
+    def get_biases(self) -> Tuple[np.ndarray, np.ndarray]:
+        """b1 [N], b2 [M, O] of a handle made with biases=True."""
+        return pmlp_get_biases(self.handle, self.N, self.M, self.O)
+
+    def set_biases(self, b1=None, b2=None) -> None:
+        pmlp_set_biases(self.handle, b1, b2)
 
     def set_profiling(self, enable: bool) -> None:
         pmlp_set_profiling(self.handle, enable)

@@ -63,8 +63,10 @@ struct pmlp {
   std::vector<int32_t> hs, acts;
   std::vector<int64_t> seg_off;
 
-  float* W1 = nullptr;  // [Npad][F4] (+ slack)
+  float* W1 = nullptr;  // [Npad][F4] (+ slack); column bcol holds the hidden biases
   float* W2 = nullptr;  // [O][Npad]
+  int32_t bcol = -1;    // with biases: the column of the constant input 1 (F rounded to 4)
+  float* b2 = nullptr;  // with biases: output biases [M][O]
   int64_t* d_seg_off = nullptr;
   int32_t* d_act = nullptr;
   int32_t* d_mid = nullptr;   // [Npad] model of each hidden unit
@@ -105,6 +107,7 @@ namespace {
 void release(pmlp* h) {
   dfree(h->W1);
   dfree(h->W2);
+  dfree(h->b2);
   dfree(h->d_seg_off);
   dfree(h->d_act);
   dfree(h->d_mid);
@@ -276,7 +279,8 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
     if (int rc = ensure_workspace_bf16(h, Bp)) return rc;
     if (int rc = ensure_w1b(h)) return rc;
     if (int rc = run(h, KID_PACK_X, [&] {
-          return launch_pack_x_bf16(X, B, h->F, Bp, h->F4, h->Xp16, h->Xt16, h->stream);
+          return launch_pack_x_bf16(X, B, h->F, Bp, h->F4, h->bcol, h->Xp16, h->Xt16,
+                                    h->stream);
         }))
       return rc;
     GemmBfArgs g{};
@@ -294,7 +298,7 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
     return run(h, KID_GEMM_FWD, [&] { return launch_gemm_bf16(g, EPI_STORE, h->stream); });
   }
   if (int rc = run(h, KID_PACK_X, [&] {
-        return launch_pack_x(X, B, h->F, Bp, h->F4, h->Xp, h->Xt, h->stream);
+        return launch_pack_x(X, B, h->F, Bp, h->F4, h->bcol, h->Xp, h->Xt, h->stream);
       }))
     return rc;
   if (h->lds_kernels && fwd_lds_supported(Bp, h->F4)) {
@@ -325,7 +329,7 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
 // Full step: forward, loss, backward and either the SGD update (dW1 and
 // dW2 null) or gradient stores.
 int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const float* lrm,
-         float* dW1, float* dW2) {
+         float* dW1, float* dW2, float* db1 = nullptr, float* db2 = nullptr) {
   const int32_t Bp = pad_batch(B);
   if (int rc = use_device(h)) return rc;
   if (int rc = ensure_workspace(h, Bp)) return rc;
@@ -340,12 +344,14 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const f
   }
   if (int rc = run(h, KID_M3_FWD, [&] {
         return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act,
-                             h->d_tiles, h->ntiles, h->LG, (int64_t)Bp * h->O, h->O,
+                             h->d_tiles, h->ntiles, h->b2, h->LG, (int64_t)Bp * h->O, h->O,
                              h->stream);
       }))
     return rc;
   if (int rc = run(h, KID_CE, [&] {
+        // output biases: updated here (db2 = sum_b G), or their gradient stored
         return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, dW1 ? nullptr : lrm,
+                         dW1 ? (db2 ? h->b2 : nullptr) : h->b2, dW1 ? db2 : nullptr, lr,
                          h->stream);
       }))
     return rc;
@@ -368,6 +374,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const f
     b.O = h->O;
     b.lr = lr;
     b.lrm = lrm;
+    b.db1 = dW1 ? db1 : nullptr;
+    b.bcol = h->bcol;
     if (int rc = run(h, KID_BWD_FUSED, [&] { return launch_bwd_lds(b, h->stream); })) return rc;
     h->have_loss = true;
     return PMLP_OK;
@@ -394,6 +402,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const f
     g.lr = lr;
     g.lrm = lrm;
     g.mid = h->d_mid;
+    g.db1 = dW1 ? db1 : nullptr;
+    g.bcol = h->bcol;
     g.outb = dW1 ? nullptr : h->W1b;  // the update keeps the bf16 copy current
     g.ldob = bf16_ld(h->F4);
     if (int rc = run(h, KID_GEMM_BWD, [&] {
@@ -417,6 +427,8 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const f
   g.lr = lr;
   g.lrm = lrm;
   g.mid = h->d_mid;
+  g.db1 = dW1 ? db1 : nullptr;
+  g.bcol = h->bcol;
   if (int rc = run(h, KID_GEMM_BWD, [&] {
         return launch_gemm(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
       }))
@@ -462,8 +474,15 @@ extern "C" {
 
 int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes,
                 const int32_t* act_ids, uint64_t seed) {
+  return pmlp_create_ex(out, F, O, M, hidden_sizes, act_ids, seed, 0);
+}
+
+int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes,
+                   const int32_t* act_ids, uint64_t seed, int32_t flags) {
   if (!out) return fail(PMLP_EINVAL, "null output handle pointer");
   *out = nullptr;
+  if (flags & ~PMLP_BIAS) return fail(PMLP_EINVAL, "unknown flags");
+  const bool biases = (flags & PMLP_BIAS) != 0;
   if (F < 1) return fail(PMLP_EINVAL, "F must be >= 1");
   if (O < 2 || O > kMaxO) return fail(PMLP_EINVAL, "O must be in [2, 16]");
   if (M < 1) return fail(PMLP_EINVAL, "M must be >= 1");
@@ -476,12 +495,16 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
     N += hidden_sizes[m];
   }
   if (N > ((int64_t)1 << 31) - 1) return fail(PMLP_EINVAL, "total hidden units exceed 2^31-1");
-  const int32_t F4 = (F + 3) & ~3;
+  // With biases the input gets a constant 1 at column bcol = F rounded up
+  // to 4, whose weight is the hidden bias; rows are then 4 floats longer.
+  const int32_t bcol = biases ? (F + 3) & ~3 : -1;
+  const int32_t F4 = ((F + 3) & ~3) + (biases ? 4 : 0);
 
   pmlp* h = new (std::nothrow) pmlp();
   if (!h) return fail(PMLP_ENOMEM, "host allocation failed");
   h->F = F;
   h->F4 = F4;
+  h->bcol = bcol;
   h->O = O;
   h->M = M;
   h->N = N;
@@ -529,7 +552,8 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
       hipMalloc(&h->d_tiles, tiles.size() * sizeof(Tile3)) != hipSuccess ||
       hipMalloc(&h->loss, (size_t)M * sizeof(float)) != hipSuccess ||
       hipMalloc(&h->flag, 2 * sizeof(int32_t)) != hipSuccess ||
-      hipMalloc(&d_bound2, (size_t)M * sizeof(float)) != hipSuccess) {
+      hipMalloc(&d_bound2, (size_t)M * sizeof(float)) != hipSuccess ||
+      (biases && hipMalloc(&h->b2, (size_t)M * O * sizeof(float)) != hipSuccess)) {
     (void)hipGetLastError();
     dfree(d_bound2);
     return bail(fail(PMLP_ENOMEM, "device allocation failed for the packed parameters"));
@@ -550,6 +574,9 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* hid
     PMLP_HIP(hipMemset(h->flag, 0, 2 * sizeof(int32_t)));
     PMLP_HIP(launch_init_params(h->W1, N, F, F4, bound1, h->W2, Npad, O, h->d_mid, d_bound2,
                                 splitmix64_host(seed), nullptr));
+    if (biases)
+      PMLP_HIP(launch_init_biases(h->W1, N, F4, bcol, bound1, h->b2, M, O, d_bound2,
+                                  splitmix64_host(seed), nullptr));
     PMLP_HIP(hipStreamSynchronize(nullptr));
     return PMLP_OK;
   };
@@ -597,7 +624,7 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
   }
   return run(h, KID_M3_FWD, [&] {
     return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act, h->d_tiles,
-                         h->ntiles, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
+                         h->ntiles, h->b2, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
   });
 }
 
@@ -621,6 +648,45 @@ int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B
   if (int rc = check_batch(h, X_dev, B)) return rc;
   if (!y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null labels or gradient buffer");
   return step(h, X_dev, y_dev, B, 0.f, nullptr, dW1_dev, dW2_dev);
+}
+
+int pmlp_gradients_ex(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
+                      float* dW1_dev, float* dW2_dev, float* db1_dev, float* db2_dev) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null labels or gradient buffer");
+  if (h->bcol < 0) return fail(PMLP_ESTATE, "the handle was created without biases");
+  if (!db1_dev || !db2_dev) return fail(PMLP_EINVAL, "null bias gradient buffer");
+  return step(h, X_dev, y_dev, B, 0.f, nullptr, dW1_dev, dW2_dev, db1_dev, db2_dev);
+}
+
+int pmlp_get_biases(pmlp_t h, float* b1_host, float* b2_host) {
+  if (int rc = check_handle(h)) return rc;
+  if (h->bcol < 0) return fail(PMLP_ESTATE, "the handle was created without biases");
+  if (int rc = use_device(h)) return rc;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  if (b1_host)  // column bcol of W1
+    PMLP_HIP(hipMemcpy2D(b1_host, sizeof(float), h->W1 + h->bcol, (size_t)h->F4 * sizeof(float),
+                         sizeof(float), (size_t)h->N, hipMemcpyDeviceToHost));
+  if (b2_host)
+    PMLP_HIP(hipMemcpy(b2_host, h->b2, (size_t)h->M * h->O * sizeof(float),
+                       hipMemcpyDeviceToHost));
+  return PMLP_OK;
+}
+
+int pmlp_set_biases(pmlp_t h, const float* b1_host, const float* b2_host) {
+  if (int rc = check_handle(h)) return rc;
+  if (h->bcol < 0) return fail(PMLP_ESTATE, "the handle was created without biases");
+  if (int rc = use_device(h)) return rc;
+  PMLP_HIP(hipStreamSynchronize(h->stream));
+  if (b1_host) {
+    h->w1b_valid = false;
+    PMLP_HIP(hipMemcpy2D(h->W1 + h->bcol, (size_t)h->F4 * sizeof(float), b1_host, sizeof(float),
+                         sizeof(float), (size_t)h->N, hipMemcpyHostToDevice));
+  }
+  if (b2_host)
+    PMLP_HIP(hipMemcpy(h->b2, b2_host, (size_t)h->M * h->O * sizeof(float),
+                       hipMemcpyHostToDevice));
+  return PMLP_OK;
 }
 
 int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev, float* H_dev) {

@@ -141,6 +141,7 @@ __global__ __launch_bounds__(kBlock) void k_gemm_nt(GemmArgs a, int WQ) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           if (q + r < a.ncols) orow[q + r] = acc[i][j][r];
+          else if (q + r == a.bcol && a.db1) a.db1[p] = acc[i][j][r];
       }
     }
   }

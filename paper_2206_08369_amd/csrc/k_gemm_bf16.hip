@@ -291,6 +291,7 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             if (q + e < a.ncols) o[e] = v[e];
+            else if (q + e == a.bcol && a.db1) a.db1[p] = v[e];
         }
       }
       __syncthreads();

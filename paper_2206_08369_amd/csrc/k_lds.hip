@@ -304,6 +304,7 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (q + r < a.F) grow1[q + r] = acc[i][r];
+            else if (q + r == a.bcol && a.db1) a.db1[p] = acc[i][r];
         }
       }
     } else {

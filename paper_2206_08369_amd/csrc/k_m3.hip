@@ -65,7 +65,7 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
     const float* __restrict__ Zt, int Bp, int B, const float* __restrict__ W2, int64_t ldw,
     int O, const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
     const Tile3* __restrict__ tiles, int ntiles, int BW, int LG, int nbblk,
-    float* __restrict__ out, int64_t sm, int64_t sb) {
+    const float* __restrict__ b2, float* __restrict__ out, int64_t sm, int64_t sb) {
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
   const int tile = wv / nbblk;
@@ -111,6 +111,8 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
 #pragma unroll
         for (int o = 0; o < OM; ++o) acc[i][o] += __shfl_xor(acc[i][o], s);
     if (g == 0 && bvalid) {
+      // the output bias goes with the piece that starts the segment
+      const bool with_b2 = b2 && n == seg_off[m];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if (b + i >= B) continue;
@@ -118,8 +120,9 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
 #pragma unroll
         for (int o = 0; o < OM; ++o) {
           if (o >= O) continue;
-          if (t.atomic) unsafeAtomicAdd(dst + o, acc[i][o]);
-          else dst[o] = acc[i][o];
+          const float v = with_b2 ? acc[i][o] + b2[(int64_t)m * O + o] : acc[i][o];
+          if (t.atomic) unsafeAtomicAdd(dst + o, v);
+          else dst[o] = v;
         }
       }
     }
@@ -131,8 +134,8 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
 template <int OM>
 static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float* W2,
                             int64_t ldw, int32_t O, const int64_t* seg_off, const int32_t* act,
-                            const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
-                            int64_t sb, hipStream_t s) {
+                            const Tile3* tiles, int32_t ntiles, const float* b2, float* out,
+                            int64_t sm, int64_t sb, hipStream_t s) {
   int BW = 64;
   if (Bp < 64) BW = Bp <= 16 ? 16 : (Bp <= 32 ? 32 : 64);
   const int LG = BW / 4;
@@ -140,19 +143,19 @@ static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float*
   const int64_t waves = (int64_t)ntiles * nbblk;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
   k_m3_fwd<OM><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, BW,
-                                         LG, nbblk, out, sm, sb);
+                                         LG, nbblk, b2, out, sm, sb);
 }
 
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
-                         const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
-                         int64_t sb, hipStream_t s) {
+                         const Tile3* tiles, int32_t ntiles, const float* b2, float* out,
+                         int64_t sm, int64_t sb, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
-  if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
-  else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
-  else if (O <= 8) m3_fwd_dispatch<8>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
-  else if (O <= 10) m3_fwd_dispatch<10>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
-  else m3_fwd_dispatch<16>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, out, sm, sb, s);
+  if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
+  else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
+  else if (O <= 8) m3_fwd_dispatch<8>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
+  else if (O <= 10) m3_fwd_dispatch<10>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
+  else m3_fwd_dispatch<16>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
   return hipGetLastError();
 }
 

@@ -57,27 +57,53 @@ hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(kBlock) void k_init_b(float* __restrict__ W1, int64_t N, int F4,
+                                                   int bcol, float bound1,
+                                                   float* __restrict__ b2, int M, int O,
+                                                   const float* __restrict__ bound2,
+                                                   uint64_t key) {
+  const int64_t total = N + (int64_t)M * O;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    if (i < N) {
+      W1[i * F4 + bcol] = uniform_weight(key, 3, (uint64_t)i, bound1);
+    } else {
+      const int64_t j = i - N;  // counter m*O + o
+      b2[j] = uniform_weight(key, 4, (uint64_t)j, bound2[j / O]);
+    }
+  }
+}
+
+hipError_t launch_init_biases(float* W1, int64_t N, int32_t F4, int32_t bcol, float bound1,
+                              float* b2, int32_t M, int32_t O, const float* bound2,
+                              uint64_t key, hipStream_t s) {
+  k_init_b<<<grid_for(N + (int64_t)M * O), kBlock, 0, s>>>(W1, N, F4, bcol, bound1, b2, M, O,
+                                                           bound2, key);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // Batch packing: X [B][F] -> Xp [Bp][F4] and Xt [F4][Bp], zero padded.
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(kBlock) void k_pack_x(const float* __restrict__ X, int B, int F,
-                                                   int Bp, int F4, float* __restrict__ Xp,
+                                                   int Bp, int F4, int bcol,
+                                                   float* __restrict__ Xp,
                                                    float* __restrict__ Xt) {
   const int64_t total = (int64_t)Bp * F4;
   for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * kBlock) {
     const int b = (int)(i / F4);
     const int f = (int)(i - (int64_t)b * F4);
-    const float v = (b < B && f < F) ? X[(int64_t)b * F + f] : 0.f;
+    const float v = b < B ? (f < F ? X[(int64_t)b * F + f] : (f == bcol ? 1.f : 0.f)) : 0.f;
     Xp[i] = v;
     Xt[(int64_t)f * Bp + b] = v;
   }
 }
 
 hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
-                         float* Xp, float* Xt, hipStream_t s) {
-  k_pack_x<<<grid_for((int64_t)Bp * F4), kBlock, 0, s>>>(X, B, F, Bp, F4, Xp, Xt);
+                         int32_t bcol, float* Xp, float* Xt, hipStream_t s) {
+  k_pack_x<<<grid_for((int64_t)Bp * F4), kBlock, 0, s>>>(X, B, F, Bp, F4, bcol, Xp, Xt);
   return hipGetLastError();
 }
 
@@ -85,7 +111,8 @@ hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32
 // v_cvt_pk_bf16_f32); padding (b >= B, f >= F, and the row tails up to the
 // 64-element stride) is zero.
 __global__ __launch_bounds__(kBlock) void k_pack_x_bf16(const float* __restrict__ X, int B,
-                                                        int F, int Bp, int F4, int ldp, int ldt,
+                                                        int F, int Bp, int F4, int bcol,
+                                                        int ldp, int ldt,
                                                         unsigned short* __restrict__ Xp16,
                                                         unsigned short* __restrict__ Xt16) {
   const int64_t np = (int64_t)Bp * ldp, nt = (int64_t)F4 * ldt;
@@ -99,7 +126,8 @@ __global__ __launch_bounds__(kBlock) void k_pack_x_bf16(const float* __restrict_
       f = (int)((i - np) / ldt);
       b = (int)(i - np - (int64_t)f * ldt);
     }
-    const float v = (b < B && f < F) ? X[(int64_t)b * F + f] : 0.f;
+    const float v = (b < B && f < F4) ? (f < F ? X[(int64_t)b * F + f] : (f == bcol ? 1.f : 0.f))
+                                      : 0.f;
     const unsigned short u = __builtin_bit_cast(unsigned short, (__bf16)v);
     if (i < np) Xp16[i] = u;
     else Xt16[i - np] = u;
@@ -107,10 +135,11 @@ __global__ __launch_bounds__(kBlock) void k_pack_x_bf16(const float* __restrict_
 }
 
 hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
-                              unsigned short* Xp16, unsigned short* Xt16, hipStream_t s) {
+                              int32_t bcol, unsigned short* Xp16, unsigned short* Xt16,
+                              hipStream_t s) {
   const int ldp = bf16_ld(F4), ldt = bf16_ld(Bp);
   k_pack_x_bf16<<<grid_for((int64_t)Bp * ldp + (int64_t)F4 * ldt), kBlock, 0, s>>>(
-      X, B, F, Bp, F4, ldp, ldt, Xp16, Xt16);
+      X, B, F, Bp, F4, bcol, ldp, ldt, Xp16, Xt16);
   return hipGetLastError();
 }
 
@@ -161,12 +190,17 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
                                                int B, int O, float invB,
                                                float* __restrict__ loss,
                                                int32_t* __restrict__ flag,
-                                               const float* __restrict__ lrm) {
+                                               const float* __restrict__ lrm,
+                                               float* __restrict__ b2, float* __restrict__ db2,
+                                               float lr) {
   const int lane = threadIdx.x & 63;
   const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (m >= M) return;
   if (lrm && lane == 0 && !isfinite(lrm[m])) flag[1] = 1;
   float part = 0.f;
+  float gs[OM];  // this lane's share of db2 = sum_b G
+#pragma unroll
+  for (int o = 0; o < OM; ++o) gs[o] = 0.f;
   for (int b = lane; b < Bp; b += 64) {
     float* row = LG + ((int64_t)m * Bp + b) * O;
     if (b < B) {
@@ -191,7 +225,11 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
       part += lse - ly;
 #pragma unroll
       for (int o = 0; o < OM; ++o)
-        if (o < O) row[o] = (expf(l[o] - lse) - (o == yb ? 1.f : 0.f)) * invB;
+        if (o < O) {
+          const float g = (expf(l[o] - lse) - (o == yb ? 1.f : 0.f)) * invB;
+          row[o] = g;
+          gs[o] += g;
+        }
     } else {
       for (int o = 0; o < O; ++o) row[o] = 0.f;
     }
@@ -199,16 +237,29 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
 #pragma unroll
   for (int s = 32; s > 0; s >>= 1) part += __shfl_xor(part, s);
   if (lane == 0) loss[m] = part * invB;
+  if (b2) {
+    const float rate = lrm ? lrm[m] : lr;
+#pragma unroll
+    for (int o = 0; o < OM; ++o) {
+      float v = gs[o];
+      for (int s = 32; s > 0; s >>= 1) v += __shfl_xor(v, s);
+      if (lane == 0 && o < O) {
+        if (db2) db2[(int64_t)m * O + o] = v;
+        else b2[(int64_t)m * O + o] -= rate * v;
+      }
+    }
+  }
 }
 
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
-                     float* loss, int32_t* flag, const float* lrm, hipStream_t s) {
+                     float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
+                     float lr, hipStream_t s) {
   const unsigned blocks = (unsigned)((M + 3) / 4);
   const float invB = 1.0f / (float)B;
-  if (O <= 2) k_ce<2><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
-  else if (O <= 4) k_ce<4><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
-  else if (O <= 8) k_ce<8><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
-  else k_ce<16><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm);
+  if (O <= 2) k_ce<2><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm, b2, db2, lr);
+  else if (O <= 4) k_ce<4><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm, b2, db2, lr);
+  else if (O <= 8) k_ce<8><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm, b2, db2, lr);
+  else k_ce<16><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm, b2, db2, lr);
   return hipGetLastError();
 }
 

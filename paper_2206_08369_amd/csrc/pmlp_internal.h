@@ -54,6 +54,8 @@ struct GemmArgs {
   float lr;
   const float* lrm;    // EPI_SGD: per-model rates (null: lr for every row)
   const int32_t* mid;  // model of each row p (with lrm)
+  float* db1;          // EPI_GRAD: column bcol (the hidden bias) goes to db1[p]
+  int32_t bcol;
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
@@ -76,6 +78,8 @@ struct GemmBfArgs {
   float lr;
   const float* lrm;         // EPI_SGD: per-model rates (null: lr for every row)
   const int32_t* mid;       // model of each row p (with lrm)
+  float* db1;               // EPI_GRAD: column bcol (the hidden bias) goes to db1[p]
+  int32_t bcol;
   unsigned short* outb;     // EPI_SGD: also store bf16 of the updated values (or null)
   int64_t ldob;
 };
@@ -115,6 +119,8 @@ struct BwdArgs {
   int32_t Bp, F, F4, O;
   float lr;
   const float* lrm;  // per-model rates (null: lr for every row)
+  float* db1;        // gradient mode: column bcol (the hidden bias) goes to db1[p]
+  int32_t bcol;
 };
 bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O);
 hipError_t launch_bwd_lds(const BwdArgs& a, hipStream_t s);
@@ -123,8 +129,16 @@ hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float
                               float* W2, int64_t ldw, int32_t O, const int32_t* mid,
                               const float* bound2, uint64_t key, hipStream_t s);
 
+// Hidden biases into W1's column bcol (the weight of a constant input 1) and
+// output biases b2 [M][O]; bound2 is per model.
+hipError_t launch_init_biases(float* W1, int64_t N, int32_t F4, int32_t bcol, float bound1,
+                              float* b2, int32_t M, int32_t O, const float* bound2,
+                              uint64_t key, hipStream_t s);
+
+// Column bcol (>= F, or -1 for none) of the copies is 1 for the B real
+// samples: the constant input whose weight is the hidden bias.
 hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
-                         float* Xp, float* Xt, hipStream_t s);
+                         int32_t bcol, float* Xp, float* Xt, hipStream_t s);
 
 // bf16 copies of the batch (round to nearest even), zero padded:
 //   Xp16 [Bp][bf16_ld(F4)]  (operand of Z = X W1^T)
@@ -134,17 +148,21 @@ hipError_t launch_w1_to_bf16(const float* W1, int64_t Npad, int32_t F4, unsigned
                              int32_t ldb, hipStream_t s);
 
 hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
-                              unsigned short* Xp16, unsigned short* Xt16, hipStream_t s);
+                              int32_t bcol, unsigned short* Xp16, unsigned short* Xt16,
+                              hipStream_t s);
 
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
-                         const Tile3* tiles, int32_t ntiles, float* out, int64_t sm,
-                         int64_t sb, hipStream_t s);
+                         const Tile3* tiles, int32_t ntiles, const float* b2, float* out,
+                         int64_t sm, int64_t sb, hipStream_t s);
 
 // flag[0] is raised by a label outside [0, O), flag[1] by a non-finite
 // per-model rate in lrm (may be null).
+// With b2 set, db2[m][o] = sum_b G[m][b][o] is stored into db2 (gradient
+// mode) or applied as b2 -= lr_m db2 (the rate lrm[m], or lr).
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
-                     float* loss, int32_t* flag, const float* lrm, hipStream_t s);
+                     float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
+                     float lr, hipStream_t s);
 
 // M3 backward + activation derivative: dZ over Zt in place (fp32), or, with
 // dZ16 set, as bf16 into dZ16 [Npad][Bp] leaving Zt unchanged; then the W2

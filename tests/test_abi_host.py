@@ -90,3 +90,9 @@ def test_package_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(pm, "library_path", lambda: str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         pm.load_library()
+
+
+def test_create_rejects_unknown_flags(pm):
+    with pytest.raises(pm.PmlpError) as e:
+        pm.pmlp_create(3, 2, [1], [0], 0, flags=2)
+    assert e.value.code == pm.PMLP_EINVAL and "unknown flags" in str(e.value)
