@@ -70,6 +70,13 @@ CASES = {
     "f32_b32_o10": dict(M=25, hmax=200, F=32, O=10, B=29),
     "f140_b64": dict(M=12, hmax=64, F=140, O=2, B=64),
     "f12_b16": dict(M=40, hmax=30, F=12, O=2, B=16),
+    # the forward with the M3 epilogue: several segments inside one 16-unit
+    # tile, segments ending exactly on and just off tile edges, split
+    # segments, and the two-pass 256-sample tile
+    "fwd_mixed_b256": dict(hs=[3, 1, 1, 17, 16, 15, 600, 2, 1, 33, 1000, 5, 48, 1, 16, 513],
+                           F=20, O=2, B=256),
+    "fwd_mixed_o4": dict(hs=[3, 1, 1, 17, 16, 15, 600, 2, 1, 33, 1000, 5, 48, 1, 16, 513],
+                         F=36, O=4, B=120),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
