@@ -158,9 +158,13 @@ __device__ __forceinline__ void bwdl_load(f32x4& cz, f32x4 (&cg)[OM], const floa
 // One batch chunk of one tile row: dZ = (sum_o G W2) act'(Z) for the lane's
 // four samples, the dW2 partial sums, then the TQ x 4 MFMAs with the batch
 // operand from LDS.  A < 0: each lane dispatches on its own row's id.
-template <int TQ, int OM, int A>
-__device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ], float (&dw)[OM], const f32x4* qptr,
-                                           int qstride, const f32x4& cz, const f32x4 (&cg)[OM],
+// TAIL: four more columns (16 TQ .. 16 TQ + 3) by plain FMAs instead of a
+// 16-column MFMA block that would be three quarters padding; tptr points
+// at the lane's four LDS slots of those columns (rows 16 TQ + q, q < 4).
+template <int TQ, int OM, int A, bool TAIL>
+__device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ], float (&dw)[OM], float (&tacc)[4],
+                                           const f32x4* qptr, int qstride, const f32x4* tptr,
+                                           const f32x4& cz, const f32x4 (&cg)[OM],
                                            const float (&w2)[OM], int arow) {
   const float* g = (const float*)&cg[0];  // g[s*OM + o] = G[m][b+s][o]
   float dz[4];
@@ -184,6 +188,14 @@ __device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ], float (&dw)[OM], co
     for (int s = 0; s < 4; ++s)
       acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[s], dz[s], acc[i], 0, 0, 0);
   }
+  if (TAIL) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 x = tptr[q];  // X[b .. b+3][16 TQ + q]
+#pragma unroll
+      for (int s = 0; s < 4; ++s) tacc[q] = fmaf(dz[s], x[s], tacc[q]);
+    }
+  }
 }
 
 // All batch chunks of one tile.  Z and G chunks go through a ring of RING
@@ -191,11 +203,11 @@ __device__ __forceinline__ void bwdl_chunk(f32x4 (&acc)[TQ], float (&dw)[OM], co
 // past the end are clamped to the last chunk (redundant in-bounds loads) so
 // every pass issues the same loads and wait counts stay exact.  The loop is
 // instantiated per activation so that no activation switch sits inside it.
-template <int TQ, int OM, int RING, int A>
-__device__ __forceinline__ void bwdl_tile(f32x4 (&acc)[TQ], float (&dw)[OM], const f32x4* qbase,
-                                          int qstride, int nch, const float* zrow,
-                                          const float* grow, int lk, const float (&w2)[OM],
-                                          int arow) {
+template <int TQ, int OM, int RING, int A, bool TAIL>
+__device__ __forceinline__ void bwdl_tile(f32x4 (&acc)[TQ], float (&dw)[OM], float (&tacc)[4],
+                                          const f32x4* qbase, const f32x4* tbase, int qstride,
+                                          int nch, const float* zrow, const float* grow, int lk,
+                                          const float (&w2)[OM], int arow) {
   f32x4 zb[RING], gb[RING][OM];
 #pragma unroll
   for (int r = 0; r < RING - 1; ++r)
@@ -207,20 +219,23 @@ __device__ __forceinline__ void bwdl_tile(f32x4 (&acc)[TQ], float (&dw)[OM], con
       const int cl = c + RING - 1 < nch ? c + RING - 1 : nch - 1;
       bwdl_load<OM>(zb[(r + RING - 1) % RING], gb[(r + RING - 1) % RING], zrow, grow,
                     16 * cl + 4 * lk);
-      if (c < nch) bwdl_chunk<TQ, OM, A>(acc, dw, qbase + 64 * c, qstride, zb[r], gb[r], w2, arow);
+      if (c < nch)
+        bwdl_chunk<TQ, OM, A, TAIL>(acc, dw, tacc, qbase + 64 * c, qstride, tbase + 64 * c, zb[r],
+                                    gb[r], w2, arow);
     }
   }
 }
 
-template <int TQ, int OM, int RING, int NT>
+template <int TQ, int OM, int RING, int NT, bool TAIL>
 __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
   constexpr int NW = NT / 64;
+  constexpr int TB = TQ + (TAIL ? 1 : 0);  // column blocks held in LDS
   extern __shared__ float lds[];
   const int Bp = a.Bp;
   const int nch = Bp >> 4;
   const bool grad = a.dW1 != nullptr;
   // float4 slot ((i*nch + c)*64 + l) = Xt[16i + l%16][16c + 4(l/16) .. +3] (0 past F4)
-  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += NT) {
+  for (int slot = threadIdx.x; slot < TB * nch * 64; slot += NT) {
     const int l = slot & 63, rest = slot >> 6;
     const int i = rest / nch, c = rest - (rest / nch) * nch;
     const int row = 16 * i + (l & 15);
@@ -236,6 +251,8 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
   const int64_t tstride = (int64_t)gridDim.x * NW;
   const f32x4* qbase = (const f32x4*)lds + lane;  // + (i*nch + c)*64
   const int qstride = nch * 64;
+  // tail columns: the slots of lanes (q, lk), q < 4, of block TQ
+  const f32x4* tbase = (const f32x4*)lds + TQ * qstride + 16 * lk;  // + c*64 + q
   for (int64_t t = (int64_t)blockIdx.x * NW + wave; t < T; t += tstride) {
     const int64_t p = t * 16 + li;          // this lane's row; < Npad
     const int64_t pc = p < a.N ? p : a.N - 1;
@@ -258,8 +275,11 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
         w1v[i] = *(const f32x4*)(orow + q);
       }
     }
+    f32x4 w1t = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (TAIL && !grad) w1t = *(const f32x4*)(orow + 16 * TQ);
     f32x4 acc[TQ];
     float dw[OM];
+    float tacc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < TQ; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -269,20 +289,20 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
     const int a0 = __builtin_amdgcn_readfirstlane(arow);
     const int auni = __all(arow == a0) ? a0 : -1;
     switch (auni) {
-      case 0: bwdl_tile<TQ, OM, RING, 0>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 1: bwdl_tile<TQ, OM, RING, 1>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 2: bwdl_tile<TQ, OM, RING, 2>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 3: bwdl_tile<TQ, OM, RING, 3>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 4: bwdl_tile<TQ, OM, RING, 4>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 5: bwdl_tile<TQ, OM, RING, 5>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 6: bwdl_tile<TQ, OM, RING, 6>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 7: bwdl_tile<TQ, OM, RING, 7>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 8: bwdl_tile<TQ, OM, RING, 8>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 9: bwdl_tile<TQ, OM, RING, 9>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 10: bwdl_tile<TQ, OM, RING, 10>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 11: bwdl_tile<TQ, OM, RING, 11>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      case 12: bwdl_tile<TQ, OM, RING, 12>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
-      default: bwdl_tile<TQ, OM, RING, -1>(acc, dw, qbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 0: bwdl_tile<TQ, OM, RING, 0, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 1: bwdl_tile<TQ, OM, RING, 1, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 2: bwdl_tile<TQ, OM, RING, 2, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 3: bwdl_tile<TQ, OM, RING, 3, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 4: bwdl_tile<TQ, OM, RING, 4, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 5: bwdl_tile<TQ, OM, RING, 5, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 6: bwdl_tile<TQ, OM, RING, 6, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 7: bwdl_tile<TQ, OM, RING, 7, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 8: bwdl_tile<TQ, OM, RING, 8, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 9: bwdl_tile<TQ, OM, RING, 9, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 10: bwdl_tile<TQ, OM, RING, 10, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 11: bwdl_tile<TQ, OM, RING, 11, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      case 12: bwdl_tile<TQ, OM, RING, 12, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
+      default: bwdl_tile<TQ, OM, RING, -1, TAIL>(acc, dw, tacc, qbase, tbase, qstride, nch, zrow, grow, lk, w2, arow); break;
     }
     // dW2: combine the four lk lanes of the row; lanes lk == 0 write.
 #pragma unroll
@@ -291,6 +311,15 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
       dw[o] = v;
+    }
+    if (TAIL) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v = tacc[q];
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        tacc[q] = v;
+      }
     }
     if (grad) {
       if (p < a.N) {
@@ -306,6 +335,14 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
             if (q + r < a.F) grow1[q + r] = acc[i][r];
             else if (q + r == a.bcol && a.db1) a.db1[p] = acc[i][r];
         }
+        if (TAIL && lk == 0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int q = 16 * TQ + r;
+            if (q < a.F) grow1[q] = tacc[r];
+            else if (q == a.bcol && a.db1) a.db1[p] = tacc[r];
+          }
+        }
       }
     } else {
       // padded rows (p >= N) absorb the tail of the last tile
@@ -317,6 +354,8 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
         const int q = 16 * i + 4 * lk;
         if (q < a.F4) *(f32x4*)(orow + q) = w1v[i] - lr * acc[i];
       }
+      if (TAIL && lk == 0)
+        *(f32x4*)(orow + 16 * TQ) = w1t - lr * f32x4{tacc[0], tacc[1], tacc[2], tacc[3]};
     }
   }
 }
@@ -386,9 +425,13 @@ hipError_t launch_fwd_lds(const FwdLdsArgs& a0, hipStream_t s) {
   }
 }
 
+// Column blocks of 16 held in LDS (the last one is the four-column tail when
+// bwd_tail is set: F4 = 100, six MFMA blocks and four columns of FMAs).
 static int bwd_tq(int32_t F4) {
   return F4 <= 16 ? 1 : F4 <= 32 ? 2 : F4 <= 64 ? 4 : F4 <= 112 ? 7 : 8;
 }
+
+static bool bwd_tail(int32_t F4) { return F4 == 100; }
 
 static size_t bwd_lds_bytes(int32_t Bp, int32_t F4) { return (size_t)16 * bwd_tq(F4) * Bp * 4; }
 
@@ -398,15 +441,15 @@ bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O) {
          bwd_lds_bytes(Bp, F4) <= (size_t)d.lds_max;
 }
 
-template <int TQ, int OM>
+template <int TQ, int OM, bool TAIL = false>
 static hipError_t bwd_lds_go(const BwdArgs& a, size_t lds, hipStream_t s) {
   // One 16-row tile per wave; 12 waves per workgroup (3 per SIMD) when the
   // per-chunk G buffers are small, 8 otherwise; prefetch depth set by the
   // size of those buffers.
-  constexpr int RING = OM <= 2 ? 4 : (OM <= 4 ? 3 : 2);
+  constexpr int RING = OM <= 2 && !TAIL ? 4 : (OM <= 4 ? 3 : 2);
   constexpr int NT = OM <= 2 && TQ <= 7 ? 768 : 512;
   const int64_t T = (a.N + 15) / 16;
-  return launch_persistent(k_bwd_lds<TQ, OM, RING, NT>, NT, lds, T, s, a);
+  return launch_persistent(k_bwd_lds<TQ, OM, RING, NT, TAIL>, NT, lds, T, s, a);
 }
 
 template <int OM>
@@ -415,7 +458,10 @@ static hipError_t bwd_lds_by_f(const BwdArgs& a, size_t lds, hipStream_t s) {
     case 1: return bwd_lds_go<1, OM>(a, lds, s);
     case 2: return bwd_lds_go<2, OM>(a, lds, s);
     case 4: return bwd_lds_go<4, OM>(a, lds, s);
-    case 7: return bwd_lds_go<7, OM>(a, lds, s);
+    case 7:
+      if constexpr (OM == 2)
+        if (bwd_tail(a.F4)) return bwd_lds_go<6, OM, true>(a, lds, s);
+      return bwd_lds_go<7, OM>(a, lds, s);
     default: return bwd_lds_go<8, OM>(a, lds, s);
   }
 }
