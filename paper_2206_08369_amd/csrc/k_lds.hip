@@ -126,6 +126,127 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds(FwdLdsArgs a) {
   }
 }
 
+// Forward for narrow inputs and batches, where a tile is only a few MFMAs
+// and the kernel is bound by the W1 stream: the W1 strips of the wave's
+// next R-1 tiles are in flight while the current tile computes (a ring of
+// R strip buffers).  KC chunk registers cover the 16-wide chunks of K and
+// TRM scalar registers the 4/8/12-wide remainder; every tile issues the
+// same loads, so the wait counts stay exact.
+template <int KC, int TRM>
+struct FwdStrip {
+  f32x4 c[KC];
+  float t[TRM > 0 ? TRM : 1];
+};
+
+template <int KC, int TRM>
+__device__ __forceinline__ void fwd_ring_load(FwdStrip<KC, TRM>& st, const float* __restrict__ W1,
+                                             int64_t t, int64_t N, int K, int nch, int li,
+                                             int lk) {
+  int64_t p = t * 16 + li;
+  if (p > N - 1) p = N - 1;
+  const float* row = W1 + p * K;
+  const int clast = nch > 0 ? nch - 1 : 0;
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    int off = 16 * (c < clast ? c : clast) + 4 * lk;
+    if (off > K - 4) off = K - 4;
+    st.c[c] = *(const f32x4*)(row + off);
+  }
+#pragma unroll
+  for (int s = 0; s < TRM; ++s) {
+    int off = 16 * nch + 4 * s + lk;
+    if (off > K - 1) off = K - 1;
+    st.t[s] = row[off];
+  }
+}
+
+template <int TQ, int KC, int TRM>
+__device__ __forceinline__ void fwd_ring_tile(float* __restrict__ Zt, const FwdStrip<KC, TRM>& st,
+                                             const f32x4* qbase, const float* qtail, int64_t t,
+                                             int nch, int tr, int li, int lk) {
+  f32x4 acc[TQ];
+#pragma unroll
+  for (int i = 0; i < TQ; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    if (c < nch) {
+      // one LDS operand at a time; the four steps accumulate back to back
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) {
+        const f32x4 q = qbase[(i * nch + c) * 64];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[s], st.c[c][s], acc[i], 0, 0, 0);
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < TRM; ++s) {
+    if (s < tr) {
+#pragma unroll
+      for (int i = 0; i < TQ; ++i)
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(qtail[(i * tr + s) * 64], st.t[s], acc[i],
+                                                      0, 0, 0);
+    }
+  }
+  // Zt rows are padded to a multiple of 64, so every store is in bounds.
+  float* zrow = Zt + (t * 16 + li) * (int64_t)(16 * TQ) + 4 * lk;
+#pragma unroll
+  for (int i = 0; i < TQ; ++i) *(f32x4*)(zrow + 16 * i) = acc[i];
+}
+
+template <int TQ, int KC, int TRM, int R>
+__global__ __launch_bounds__(kLdsBlock) void k_fwd_lds_ring(FwdLdsArgs a) {
+  extern __shared__ float lds[];
+  const int K = a.K;
+  const int nch = K >> 4, tr = (K & 15) >> 2;
+  // full chunks: float4 slot ((i*nch + c)*64 + l) = Xp[16i + l%16][16c + 4(l/16) .. +3]
+  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / nch, c = rest - (rest / nch) * nch;
+    *(f32x4*)(lds + 4 * slot) =
+        *(const f32x4*)(a.Xp + (int64_t)(16 * i + (l & 15)) * K + 16 * c + 4 * (l >> 4));
+  }
+  // remainder: float slot T0 + (i*tr + s)*64 + l = Xp[16i + l%16][16nch + 4s + l/16]
+  const int T0 = TQ * nch * 256;
+  for (int slot = threadIdx.x; slot < TQ * tr * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / tr, s = rest - (rest / tr) * tr;
+    lds[T0 + slot] = a.Xp[(int64_t)(16 * i + (l & 15)) * K + 16 * nch + 4 * s + (l >> 4)];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t T = (a.N + 15) >> 4;
+  const int64_t tstride = (int64_t)gridDim.x * kLdsWaves;
+  const int64_t t0 = (int64_t)blockIdx.x * kLdsWaves + wave;
+  if (t0 >= T) return;
+  const f32x4* qbase = (const f32x4*)lds + lane;  // + (i*nch + c)*64
+  const float* qtail = lds + T0 + lane;            // + (i*tr + s)*64
+  // the wave's tiles are t0 + k*tstride; tiles past the end are clamped to
+  // the last one (loaded, never computed)
+  FwdStrip<KC, TRM> ring[R];
+#pragma unroll
+  for (int r = 0; r < R - 1; ++r) {
+    int64_t t = t0 + r * tstride;
+    if (t > T - 1) t = T - 1;
+    fwd_ring_load(ring[r], a.W1, t, a.N, K, nch, li, lk);
+  }
+  for (int64_t k0 = 0;; k0 += R) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int64_t t = t0 + (k0 + r) * tstride;
+      if (t >= T) return;
+      int64_t tn = t + (R - 1) * tstride;
+      if (tn > T - 1) tn = T - 1;
+      fwd_ring_load(ring[(r + R - 1) % R], a.W1, tn, a.N, K, nch, li, lk);
+      __builtin_amdgcn_sched_barrier(0);
+      fwd_ring_tile<TQ, KC, TRM>(a.Zt, ring[r], qbase, qtail, t, nch, tr, li, lk);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Fused backward: M3 backward + activation derivative + dW1 GEMM + both SGD
 // updates in one pass over Zt (dZ is never stored).
@@ -410,6 +531,16 @@ bool fwd_lds_supported(int32_t Bp, int32_t F4) {
   return tq_ok && F4 <= 16 * kKCMax + 12 && fwd_lds_bytes(Bp, F4) <= (size_t)d.lds_max;
 }
 
+// Narrow inputs and batches (K = 16 or 32, Bp <= 64): two chunk registers,
+// no remainder, four strips in flight; otherwise the one-tile-ahead kernel.
+template <int TQ>
+static hipError_t fwd_lds_go(const FwdLdsArgs& a, size_t lds, int64_t T, hipStream_t s) {
+  if constexpr (TQ <= 4)
+    if (a.K <= 32 && a.K % 16 == 0)
+      return launch_persistent(k_fwd_lds_ring<TQ, 2, 0, 4>, kLdsBlock, lds, T, s, a);
+  return launch_persistent(k_fwd_lds<TQ>, kLdsBlock, lds, T, s, a);
+}
+
 hipError_t launch_fwd_lds(const FwdLdsArgs& a0, hipStream_t s) {
   if (a0.N <= 0) return hipSuccess;
   if (!fwd_lds_supported(a0.Bp, a0.K)) return hipErrorInvalidValue;
@@ -417,11 +548,11 @@ hipError_t launch_fwd_lds(const FwdLdsArgs& a0, hipStream_t s) {
   const size_t lds = fwd_lds_bytes(a.Bp, a.K);
   const int64_t T = (a.N + 15) / 16;
   switch (a.Bp) {
-    case 16: return launch_persistent(k_fwd_lds<1>, kLdsBlock, lds, T, s, a);
-    case 32: return launch_persistent(k_fwd_lds<2>, kLdsBlock, lds, T, s, a);
-    case 64: return launch_persistent(k_fwd_lds<4>, kLdsBlock, lds, T, s, a);
-    case 128: return launch_persistent(k_fwd_lds<8>, kLdsBlock, lds, T, s, a);
-    default: return launch_persistent(k_fwd_lds<16>, kLdsBlock, lds, T, s, a);
+    case 16: return fwd_lds_go<1>(a, lds, T, s);
+    case 32: return fwd_lds_go<2>(a, lds, T, s);
+    case 64: return fwd_lds_go<4>(a, lds, T, s);
+    case 128: return fwd_lds_go<8>(a, lds, T, s);
+    default: return fwd_lds_go<16>(a, lds, T, s);
   }
 }
 
