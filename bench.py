@@ -66,6 +66,18 @@ def kernel_work(name, B, F, N, M, O, precision="fp32"):
     return "hbm", 0.0, 0.0
 
 
+def roofline_bound(bound, nbytes, flops, precision="fp32"):
+    """A matrix-core kernel is compute-bound only when its arithmetic
+    intensity (algorithmic flops per algorithmic byte) is above the ridge
+    point of its dtype (peak flops / peak HBM bandwidth); below it the HBM
+    roofline bounds it."""
+    if bound != "mfma" or not nbytes:
+        return bound
+    peak = PEAK_BF16_MFMA if precision == "bf16" else PEAK_FP32_MFMA
+    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+    return "mfma" if flops / nbytes >= ridge else "hbm"
+
+
 def traffic_key(kernel: str, workload: str, precision: str) -> str:
     return "%s/%s%s" % (kernel, workload, "" if precision == "fp32" else "+" + precision)
 
@@ -229,6 +241,7 @@ def main(argv=None):
                          "tflops": flops / (avg * 1e-3) / 1e12 if flops else None}
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
     bound, nbytes, flops = kernel_work(dom, w.B, w.F, N, M, w.O, args.precision)
+    bound = roofline_bound(bound, nbytes, flops, args.precision)
     avg_s = kernels[dom]["avg_ms"] * 1e-3
     if bound == "mfma":
         peak = PEAK_BF16_MFMA if args.precision == "bf16" else PEAK_FP32_MFMA
