@@ -5,6 +5,7 @@
 #include "pmlp.h"
 #include "pmlp_internal.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -72,6 +73,7 @@ struct pmlp {
   int32_t* d_mid = nullptr;   // [Npad] model of each hidden unit
   int32_t* d_actn = nullptr;  // [Npad] activation id of each hidden unit
   Tile3* d_tiles = nullptr;
+  int32_t* d_order = nullptr;  // tile indices, widest first
   int32_t ntiles = 0;
   bool has_split = false;
   float* loss = nullptr;   // [M]
@@ -113,6 +115,7 @@ void release(pmlp* h) {
   dfree(h->d_mid);
   dfree(h->d_actn);
   dfree(h->d_tiles);
+  dfree(h->d_order);
   dfree(h->loss);
   dfree(h->flag);
   dfree(h->Xp);
@@ -344,7 +347,7 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const f
   }
   if (int rc = run(h, KID_M3_FWD, [&] {
         return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act,
-                             h->d_tiles, h->ntiles, h->b2, h->LG, (int64_t)Bp * h->O, h->O,
+                             h->d_tiles, h->d_order, h->ntiles, h->b2, h->LG, (int64_t)Bp * h->O, h->O,
                              h->stream);
       }))
     return rc;
@@ -525,6 +528,12 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
   std::vector<Tile3> tiles;
   build_tiles(h->hs, tiles, h->has_split);
   h->ntiles = (int32_t)tiles.size();
+  // the M3 forward launches its waves widest tile first (ties in plan order),
+  // so the dispatcher schedules the longest work first
+  std::vector<int32_t> order(tiles.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (int32_t)i;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int32_t x, int32_t y) { return tiles[x].len > tiles[y].len; });
   std::vector<float> bound2((size_t)M);
   for (int32_t m = 0; m < M; ++m) bound2[m] = (float)(1.0 / std::sqrt((double)hidden_sizes[m]));
   const float bound1 = (float)(1.0 / std::sqrt((double)F));
@@ -550,6 +559,7 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
       hipMalloc(&h->d_mid, (size_t)Npad * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->d_actn, (size_t)Npad * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->d_tiles, tiles.size() * sizeof(Tile3)) != hipSuccess ||
+      hipMalloc(&h->d_order, order.size() * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&h->loss, (size_t)M * sizeof(float)) != hipSuccess ||
       hipMalloc(&h->flag, 2 * sizeof(int32_t)) != hipSuccess ||
       hipMalloc(&d_bound2, (size_t)M * sizeof(float)) != hipSuccess ||
@@ -569,6 +579,8 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
     PMLP_HIP(hipMemset(h->W1, 0, w1_bytes));
     PMLP_HIP(hipMemset(h->W2, 0, (size_t)O * Npad * sizeof(float)));
     PMLP_HIP(hipMemcpy(h->d_tiles, tiles.data(), tiles.size() * sizeof(Tile3),
+                       hipMemcpyHostToDevice));
+    PMLP_HIP(hipMemcpy(h->d_order, order.data(), order.size() * sizeof(int32_t),
                        hipMemcpyHostToDevice));
     PMLP_HIP(hipMemcpy(d_bound2, bound2.data(), (size_t)M * sizeof(float), hipMemcpyHostToDevice));
     PMLP_HIP(hipMemset(h->flag, 0, 2 * sizeof(int32_t)));
@@ -624,7 +636,7 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
   }
   return run(h, KID_M3_FWD, [&] {
     return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act, h->d_tiles,
-                         h->ntiles, h->b2, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
+                         h->d_order, h->ntiles, h->b2, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
   });
 }
 

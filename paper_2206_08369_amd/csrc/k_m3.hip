@@ -64,7 +64,8 @@ template <int OM>
 __global__ __launch_bounds__(kBlock) void k_m3_fwd(
     const float* __restrict__ Zt, int Bp, int B, const float* __restrict__ W2, int64_t ldw,
     int O, const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
-    const Tile3* __restrict__ tiles, int ntiles, int BW, int LG, int nbblk,
+    const Tile3* __restrict__ tiles, const int32_t* __restrict__ order, int ntiles, int BW,
+    int LG, int nbblk,
     const float* __restrict__ b2, float* __restrict__ out, int64_t sm, int64_t sb) {
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
@@ -77,7 +78,7 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
   const int b = bblk * BW + 4 * pp;
   const bool bvalid = b < Bp;
   const int bl = bvalid ? b : Bp - 4;  // lanes past the batch read a valid row, store nothing
-  const Tile3 t = tiles[tile];
+  const Tile3 t = tiles[__builtin_amdgcn_readfirstlane(order[tile])];
   const int64_t nend = t.n0 + t.len;
   int64_t n = t.n0;
   int m = t.m0;
@@ -131,10 +132,137 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
   }
 }
 
+// ---------------------------------------------------------------------------
+// M3 forward for wider output layers (O > 4).  For one model the product
+// with W2 followed by the scatter-add over its hidden units is a dense
+// contraction over those units,
+//   out[b][o] = sum_n act(Z[n][b]) W2[o][n],
+// which v_mfma_f32_16x16x4f32 takes four units at a time: A[b][k] =
+// act(Z[n0+k][b]) for 16 samples, B[k][o] = W2[o][n0+k] for 16 outputs (rows
+// o >= O are zero).  Lane (li, lk) supplies sample li and output li of unit
+// n0 + lk, and ends with out[4lk + r][li].  Per four units a lane loads one
+// Z value per 16-sample block and one weight (against O weights per unit and
+// 4 O running sums per lane in the scalar kernel); units past the segment
+// end are zero in both operands, so a model's sums never see another
+// model's values.  One wave per (tile of whole segments, 16 NBB samples).
+// ---------------------------------------------------------------------------
+
+template <int NBB, int A>
+__device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* __restrict__ Zt,
+                                               int Bp, int b0, const float* __restrict__ wrow,
+                                               bool orow_ok, int64_t nbeg, int64_t nend, int li,
+                                               int lk) {
+  // four-unit MFMA steps per pass, all loads first (loads in flight per lane:
+  // kUM (NBB + 1))
+  constexpr int kUM = NBB <= 2 ? 8 : 4;
+  for (int64_t n0 = nbeg; n0 < nend; n0 += 4 * kUM) {
+    float z[kUM][NBB];
+    float w[kUM];
+#pragma unroll
+    for (int u = 0; u < kUM; ++u) {
+      int64_t n = n0 + 4 * u + lk;
+      if (n > nend - 1) n = nend - 1;
+#pragma unroll
+      for (int i = 0; i < NBB; ++i) {
+        int b = b0 + 16 * i + li;
+        if (b > Bp - 1) b = Bp - 1;
+        z[u][i] = Zt[n * Bp + b];
+      }
+      w[u] = wrow[n];
+    }
+#pragma unroll
+    for (int u = 0; u < kUM; ++u) {
+      if (n0 + 4 * u >= nend) break;  // wave-uniform: the whole step is past the end
+      const bool in = n0 + 4 * u + lk < nend;
+      const float wv = in && orow_ok ? w[u] : 0.f;
+#pragma unroll
+      for (int i = 0; i < NBB; ++i) {
+        const float h = in ? act_fwd(A, z[u][i]) : 0.f;
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(h, wv, acc[i], 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <int NBB>
+__global__ __launch_bounds__(kBlock) void k_m3_fwd_mf(
+    const float* __restrict__ Zt, int Bp, int B, const float* __restrict__ W2, int64_t ldw,
+    int O, const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
+    const Tile3* __restrict__ tiles, const int32_t* __restrict__ order, int ntiles, int nbblk,
+    const float* __restrict__ b2,
+    float* __restrict__ out, int64_t sm, int64_t sb) {
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+  const int tile = wv / nbblk;
+  const int bblk = wv - tile * nbblk;
+  if (tile >= ntiles) return;
+  const int li = lane & 15, lk = lane >> 4;
+  const int b0 = bblk * 16 * NBB;
+  const bool orow_ok = li < O;
+  const float* wrow = W2 + (int64_t)(orow_ok ? li : O - 1) * ldw;
+  const Tile3 t = tiles[__builtin_amdgcn_readfirstlane(order[tile])];
+  const int64_t nend = t.n0 + t.len;
+  int64_t n = t.n0;
+  int m = t.m0;
+  while (n < nend) {
+    int64_t se = seg_off[m + 1];
+    if (se > nend) se = nend;
+    const int a = act[m];
+    f32x4 acc[NBB];
+#pragma unroll
+    for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    switch (a) {
+      case 0: fwd_segment_mf<NBB, 0>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 1: fwd_segment_mf<NBB, 1>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 2: fwd_segment_mf<NBB, 2>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 3: fwd_segment_mf<NBB, 3>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 4: fwd_segment_mf<NBB, 4>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 5: fwd_segment_mf<NBB, 5>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 6: fwd_segment_mf<NBB, 6>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 7: fwd_segment_mf<NBB, 7>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 8: fwd_segment_mf<NBB, 8>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 9: fwd_segment_mf<NBB, 9>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 10: fwd_segment_mf<NBB, 10>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 11: fwd_segment_mf<NBB, 11>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      default: fwd_segment_mf<NBB, 12>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+    }
+    if (orow_ok) {
+      // the output bias goes with the piece that starts the segment
+      const float bias = b2 && n == seg_off[m] ? b2[(int64_t)m * O + li] : 0.f;
+      float* dst = out + (int64_t)m * sm + li;
+#pragma unroll
+      for (int i = 0; i < NBB; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int b = b0 + 16 * i + 4 * lk + r;
+          if (b >= B) continue;
+          const float v = acc[i][r] + bias;
+          if (t.atomic) unsafeAtomicAdd(dst + (int64_t)b * sb, v);
+          else dst[(int64_t)b * sb] = v;
+        }
+    }
+    n = se;
+    ++m;
+  }
+}
+
+template <int NBB>
+static void m3_fwd_mf_dispatch(const float* Zt, int32_t Bp, int32_t B, const float* W2,
+                               int64_t ldw, int32_t O, const int64_t* seg_off,
+                               const int32_t* act, const Tile3* tiles, const int32_t* order, int32_t ntiles,
+                               const float* b2, float* out, int64_t sm, int64_t sb,
+                               hipStream_t s) {
+  const int nbblk = ceil_div_i(Bp, 16 * NBB);
+  const int64_t waves = (int64_t)ntiles * nbblk;
+  const unsigned blocks = (unsigned)((waves + 3) / 4);
+  k_m3_fwd_mf<NBB><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order,
+                                             ntiles, nbblk, b2, out, sm, sb);
+}
+
 template <int OM>
 static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float* W2,
                             int64_t ldw, int32_t O, const int64_t* seg_off, const int32_t* act,
-                            const Tile3* tiles, int32_t ntiles, const float* b2, float* out,
+                            const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
                             int64_t sm, int64_t sb, hipStream_t s) {
   int BW = 64;
   if (Bp < 64) BW = Bp <= 16 ? 16 : (Bp <= 32 ? 32 : 64);
@@ -142,20 +270,21 @@ static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float*
   const int nbblk = ceil_div_i(Bp, BW);
   const int64_t waves = (int64_t)ntiles * nbblk;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
-  k_m3_fwd<OM><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, BW,
-                                         LG, nbblk, b2, out, sm, sb);
+  k_m3_fwd<OM><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles,
+                                         BW, LG, nbblk, b2, out, sm, sb);
 }
 
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
-                         const Tile3* tiles, int32_t ntiles, const float* b2, float* out,
+                         const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
                          int64_t sm, int64_t sb, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
-  if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
-  else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
-  else if (O <= 8) m3_fwd_dispatch<8>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
-  else if (O <= 10) m3_fwd_dispatch<10>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
-  else m3_fwd_dispatch<16>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, ntiles, b2, out, sm, sb, s);
+  if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  // wider output layers: one MFMA per four units and 16 samples
+  else if (Bp <= 16) m3_fwd_mf_dispatch<1>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else if (Bp <= 32) m3_fwd_mf_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else m3_fwd_mf_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
   return hipGetLastError();
 }
 

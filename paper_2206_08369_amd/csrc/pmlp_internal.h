@@ -151,9 +151,10 @@ hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, 
                               int32_t bcol, unsigned short* Xp16, unsigned short* Xt16,
                               hipStream_t s);
 
+// order: tile indices in launch order (widest first).
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
-                         const Tile3* tiles, int32_t ntiles, const float* b2, float* out,
+                         const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
                          int64_t sm, int64_t sb, hipStream_t s);
 
 // flag[0] is raised by a label outside [0, O), flag[1] by a non-finite
