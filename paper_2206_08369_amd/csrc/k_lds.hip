@@ -481,6 +481,243 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused backward for wider output layers (O = 5 .. 16).  The gather of G by
+// model id and its products with W2 and with the hidden activations are,
+// for the units of one model, two small dense contractions per 16-sample
+// batch chunk, taken by v_mfma_f32_16x16x4f32:
+//   dH^T[b][n] = sum_o G[m][b][o] W2[o][n]     (K = o, ceil(O/4) steps)
+//   dW2[o][n] += sum_b G[m][b][o] act(Z[n][b]) (K = b, four steps)
+// Lane (li, lk) supplies G[m][16c + li][4j + lk] and W2[4j + lk][row li]
+// for the first and G[m][16c + 4lk + s][li] and act(Z[row li][16c + 4lk + s])
+// for the second; the first lands dH exactly where the lane holds its Z
+// values (row li, samples 4lk .. +3), the second leaves dW2[4lk + r][row li]
+// in the lane that updates it.  A tile whose rows belong to several models
+// repeats both products once per model with the other models' rows zeroed
+// in the W2 and activation operands; the G operand is shared by all 16
+// rows, so in such a tile non-finite G values (a diverged model, whose own
+// loss is already non-finite) are taken as zero rather than let them reach
+// the other models' rows.  Per chunk a lane holds 4 + 4 values
+// of G instead of 4 O, so the kernel keeps more waves in flight; the dW1
+// product, the W1 update and the batch in LDS are as in k_bwd_lds.
+// ---------------------------------------------------------------------------
+
+// G operands of one model for chunk c: g1[j] = G[mm][16c + li][4j + lk],
+// g2[s] = G[mm][16c + 4lk + s][li], read at the wave-uniform chunk base
+// gc = G + (mm Bp + 16c) O plus the lane's chunk-invariant offsets (outputs
+// past O clamped there, so every chunk issues the same loads, and their
+// values zeroed here).
+struct BwdmOffsets {
+  uint32_t o1[4], o2[4];
+  bool v1[4], v2;
+};
+
+__device__ __forceinline__ void bwdm_gload(float (&g1)[4], float (&g2)[4],
+                                           const float* __restrict__ gc, const BwdmOffsets& of) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float v = gc[of.o1[j]];
+    g1[j] = of.v1[j] ? v : 0.f;
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const float v = gc[of.o2[s]];
+    g2[s] = of.v2 ? v : 0.f;
+  }
+}
+
+// dH^T += G W2 and dW2 += G^T act(Z) for one model's rows of the tile.
+__device__ __forceinline__ void bwdm_products(f32x4& dh, f32x4& acc2, const float (&g1)[4],
+                                              const float (&g2)[4], const float (&wB)[4],
+                                              const float (&h)[4], bool mine, bool multi,
+                                              int JO) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (j < JO) {
+      const float g = multi && !isfinite(g1[j]) ? 0.f : g1[j];
+      dh = __builtin_amdgcn_mfma_f32_16x16x4f32(g, mine ? wB[j] : 0.f, dh, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const float g = multi && !isfinite(g2[s]) ? 0.f : g2[s];
+    acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(g, mine ? h[s] : 0.f, acc2, 0, 0, 0);
+  }
+}
+
+// All batch chunks of one tile.  Z and the G operands of the tile's first
+// model go through a ring of RING register buffers, RING-1 chunks ahead
+// (chunk indices past the end clamped to the last chunk); the G operands of
+// further models (tiles that span a segment boundary) are loaded in place.
+template <int TQ, int RING, int A>
+__device__ __forceinline__ void bwdm_tile(f32x4 (&acc)[TQ], f32x4& acc2, const f32x4* qbase,
+                                          int qstride, int nch, const float* zrow,
+                                          const float* __restrict__ G, int Bp, int O,
+                                          int m_first, int m_last, int m_row,
+                                          const float (&wB)[4], int arow, int li, int lk) {
+  const int JO = (O + 3) >> 2;
+  const bool multi = m_first != m_last;
+  const float* g0 = G + (int64_t)m_first * Bp * O;
+  BwdmOffsets of;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int o = 4 * j + lk;
+    of.o1[j] = (uint32_t)(li * O + (o < O ? o : O - 1));
+    of.v1[j] = o < O;
+    of.o2[j] = (uint32_t)((4 * lk + j) * O + (li < O ? li : O - 1));
+  }
+  of.v2 = li < O;
+  f32x4 zb[RING];
+  float g1b[RING][4], g2b[RING][4];
+#pragma unroll
+  for (int r = 0; r < RING - 1; ++r) {
+    const int c = r < nch ? r : nch - 1;
+    zb[r] = *(const f32x4*)(zrow + 16 * c + 4 * lk);
+    bwdm_gload(g1b[r], g2b[r], g0 + 16 * c * O, of);
+  }
+  for (int c0 = 0; c0 < nch; c0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) {
+      const int c = c0 + r;
+      const int cl = c + RING - 1 < nch ? c + RING - 1 : nch - 1;
+      const int rn = (r + RING - 1) % RING;
+      zb[rn] = *(const f32x4*)(zrow + 16 * cl + 4 * lk);
+      bwdm_gload(g1b[rn], g2b[rn], g0 + 16 * cl * O, of);
+      if (c < nch) {
+        float h[4], hp[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) h[s] = act_fwd_bwd(A >= 0 ? A : arow, zb[r][s], &hp[s]);
+        f32x4 dh = f32x4{0.f, 0.f, 0.f, 0.f};
+        bwdm_products(dh, acc2, g1b[r], g2b[r], wB, h, m_row == m_first, multi, JO);
+        for (int mm = m_first + 1; mm <= m_last; ++mm) {
+          float g1[4], g2[4];
+          bwdm_gload(g1, g2, G + ((int64_t)mm * Bp + 16 * c) * O, of);
+          bwdm_products(dh, acc2, g1, g2, wB, h, m_row == mm, multi, JO);
+        }
+        float dz[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) dz[s] = dh[s] * hp[s];
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+          const f32x4 q = qbase[i * qstride + 64 * c];
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[s], dz[s], acc[i], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+template <int TQ, int RING, int NT>
+__global__ __launch_bounds__(NT, TQ <= 2 ? 3 : 2) void k_bwd_mf(BwdArgs a) {
+  constexpr int NW = NT / 64;
+  extern __shared__ float lds[];
+  const int Bp = a.Bp, O = a.O;
+  const int nch = Bp >> 4;
+  const bool grad = a.dW1 != nullptr;
+  // float4 slot ((i*nch + c)*64 + l) = Xt[16i + l%16][16c + 4(l/16) .. +3] (0 past F4)
+  for (int slot = threadIdx.x; slot < TQ * nch * 64; slot += NT) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / nch, c = rest - (rest / nch) * nch;
+    const int row = 16 * i + (l & 15);
+    *(f32x4*)(lds + 4 * slot) =
+        row < a.F4 ? *(const f32x4*)(a.Xt + (int64_t)row * Bp + 16 * c + 4 * (l >> 4))
+                   : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t T = (a.N + 15) >> 4;
+  const int64_t tstride = (int64_t)gridDim.x * NW;
+  const f32x4* qbase = (const f32x4*)lds + lane;  // + (i*nch + c)*64
+  const int qstride = nch * 64;
+  for (int64_t t = (int64_t)blockIdx.x * NW + wave; t < T; t += tstride) {
+    const int64_t p = t * 16 + li;  // this lane's row; < Npad
+    const int64_t pc = p < a.N ? p : a.N - 1;
+    const int m_row = a.mid[pc];
+    const int arow = a.actn[pc];
+    const float lr = a.lrm ? a.lrm[m_row] : a.lr;
+    // models of the tile's rows: a contiguous range (segments are contiguous)
+    const int64_t plast = t * 16 + 15 < a.N ? t * 16 + 15 : a.N - 1;
+    const int m_first = __builtin_amdgcn_readfirstlane(a.mid[t * 16]);
+    const int m_last = __builtin_amdgcn_readfirstlane(a.mid[plast]);
+    // W2 operand of dH (rows 4j + lk) and old W2 of the update (rows 4lk + r)
+    float wB[4], w2u[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int o = 4 * j + lk;
+      wB[j] = o < O ? a.W2[(int64_t)o * a.ldw + pc] : 0.f;
+      const int ou = 4 * lk + j;
+      w2u[j] = ou < O ? a.W2[(int64_t)ou * a.ldw + pc] : 0.f;
+    }
+    const float* zrow = a.Zt + pc * Bp;
+    f32x4 w1v[TQ];
+    float* orow = a.W1 + p * a.F4;
+    if (!grad) {
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) {
+        int q = 16 * i + 4 * lk;
+        if (q > a.F4 - 4) q = a.F4 - 4;  // columns past F4 are never stored
+        w1v[i] = *(const f32x4*)(orow + q);
+      }
+    }
+    f32x4 acc[TQ], acc2 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < TQ; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int a0 = __builtin_amdgcn_readfirstlane(arow);
+    const int auni = __all(arow == a0) ? a0 : -1;
+#define PMLP_BWDM(AA)                                                                      \
+  bwdm_tile<TQ, RING, AA>(acc, acc2, qbase, qstride, nch, zrow, a.G, Bp, O, m_first, m_last, \
+                          m_row, wB, arow, li, lk)
+    switch (auni) {
+      case 0: PMLP_BWDM(0); break;
+      case 1: PMLP_BWDM(1); break;
+      case 2: PMLP_BWDM(2); break;
+      case 3: PMLP_BWDM(3); break;
+      case 4: PMLP_BWDM(4); break;
+      case 5: PMLP_BWDM(5); break;
+      case 6: PMLP_BWDM(6); break;
+      case 7: PMLP_BWDM(7); break;
+      case 8: PMLP_BWDM(8); break;
+      case 9: PMLP_BWDM(9); break;
+      case 10: PMLP_BWDM(10); break;
+      case 11: PMLP_BWDM(11); break;
+      case 12: PMLP_BWDM(12); break;
+      default: PMLP_BWDM(-1); break;
+    }
+#undef PMLP_BWDM
+    // lane (li, lk) holds dW2[4lk + r][row li]
+    if (grad) {
+      if (p < a.N) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (4 * lk + r < O) a.dW2[(int64_t)(4 * lk + r) * a.N + p] = acc2[r];
+        float* grow1 = a.dW1 + p * a.F;
+#pragma unroll
+        for (int i = 0; i < TQ; ++i) {
+          const int q = 16 * i + 4 * lk;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (q + r < a.F) grow1[q + r] = acc[i][r];
+            else if (q + r == a.bcol && a.db1) a.db1[p] = acc[i][r];
+        }
+      }
+    } else {
+      // padded rows (p >= N) absorb the tail of the last tile
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (4 * lk + r < O) a.W2[(int64_t)(4 * lk + r) * a.ldw + p] = w2u[r] - lr * acc2[r];
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) {
+        const int q = 16 * i + 4 * lk;
+        if (q < a.F4) *(f32x4*)(orow + q) = w1v[i] - lr * acc[i];
+      }
+    }
+  }
+}
+
 struct DevInfo {
   int cus = 0;
   int lds_max = 0;
@@ -568,8 +805,18 @@ static size_t bwd_lds_bytes(int32_t Bp, int32_t F4) { return (size_t)16 * bwd_tq
 
 bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O) {
   const DevInfo d = dev_info();
-  return F4 <= 128 && (O == 2 || O == 4 || O == 10) &&
+  return F4 <= 128 && (O == 2 || O == 4 || (O >= 5 && O <= 16)) &&
          bwd_lds_bytes(Bp, F4) <= (size_t)d.lds_max;
+}
+
+// Narrow inputs (two column blocks or fewer): workgroups of four waves and
+// at least three waves per SIMD (the batch copy is at most 32 KB, so several
+// workgroups share a CU); eight-wave workgroups otherwise.
+template <int TQ>
+static hipError_t bwd_mf_go(const BwdArgs& a, size_t lds, hipStream_t s) {
+  const int64_t T = (a.N + 15) / 16;
+  constexpr int NT = TQ <= 2 ? 256 : 512;
+  return launch_persistent(k_bwd_mf<TQ, 2, NT>, NT, lds, T, s, a);
 }
 
 template <int TQ, int OM, bool TAIL = false>
@@ -604,7 +851,14 @@ hipError_t launch_bwd_lds(const BwdArgs& a0, hipStream_t s) {
   const size_t lds = bwd_lds_bytes(a.Bp, a.F4);
   if (a.O == 2) return bwd_lds_by_f<2>(a, lds, s);
   if (a.O == 4) return bwd_lds_by_f<4>(a, lds, s);
-  return bwd_lds_by_f<10>(a, lds, s);
+  // O = 5 .. 16: the gather of G and the dW2 product on the matrix cores
+  switch (bwd_tq(a.F4)) {
+    case 1: return bwd_mf_go<1>(a, lds, s);
+    case 2: return bwd_mf_go<2>(a, lds, s);
+    case 4: return bwd_mf_go<4>(a, lds, s);
+    case 7: return bwd_mf_go<7>(a, lds, s);
+    default: return bwd_mf_go<8>(a, lds, s);
+  }
 }
 
 }  // namespace pmlpk
