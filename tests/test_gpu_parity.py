@@ -233,10 +233,14 @@ def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name, path):
 # Gradient isolation (Section 3) on the GPU
 # --------------------------------------------------------------------------
 
-def test_perturbing_one_model_leaves_the_others_bitwise(pm, torch):
+# (F, O, B): the scalar M3 kernels (O <= 4) and the matrix-core ones (O > 4)
+# with narrow and wide batches; "nan" makes model j diverge (its output
+# weights NaN), which must not reach the models sharing its tiles either.
+@pytest.mark.parametrize("F,O,B", [(9, 3, 40), (32, 10, 32), (20, 12, 70)])
+@pytest.mark.parametrize("kind", ["finite", "nan"])
+def test_perturbing_one_model_leaves_the_others_bitwise(pm, torch, F, O, B, kind):
     rng = np.random.default_rng(5)
     hs, acts = wl.random_models(rng, 40, 900)
-    F, O, B = 9, 3, 40
     X, y = wl.make_dataset(F, O, B, seed=8)
     net = make_net(pm, F, O, hs, acts, seed=15)
     W1, W2 = net.get_params()
@@ -247,8 +251,11 @@ def test_perturbing_one_model_leaves_the_others_bitwise(pm, torch):
     off = offsets(hs)
     j = 17
     P1, P2 = W1.copy(), W2.copy()
-    P1[off[j]:off[j + 1]] += 0.25
-    P2[:, off[j]:off[j + 1]] -= 0.5
+    if kind == "finite":
+        P1[off[j]:off[j + 1]] += 0.25
+        P2[:, off[j]:off[j + 1]] -= 0.5
+    else:
+        P2[:, off[j]:off[j + 1]] = np.nan
     net.set_params(P1, P2)
     lb = net.forward(Xd).cpu().numpy()
     gb = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
@@ -260,7 +267,10 @@ def test_perturbing_one_model_leaves_the_others_bitwise(pm, torch):
     assert np.array_equal(lossa[keep], lossb[keep])
     assert np.array_equal(ga[0][rows], gb[0][rows])
     assert np.array_equal(ga[1][:, rows], gb[1][:, rows])
-    assert not np.array_equal(la[:, j], lb[:, j])
+    if kind == "finite":
+        assert not np.array_equal(la[:, j], lb[:, j])
+    else:
+        assert np.isnan(lb[:, j]).all()
     net.close()
 
 
