@@ -8,6 +8,10 @@ result the packed method of Section 3 is constructed to reproduce exactly.
 `build()` compiles `pmlp_oracle.c` with gcc into `liboracle.so` next to
 this file; the wrappers below only marshal numpy arrays through ctypes.
 
+`head="mse"` (gradients, train, dataset_loss) replaces the softmax
+cross-entropy with the mean squared error against real targets y [B, O]
+(regression); the default `head="ce"` takes integer labels y [B].
+
 `rounding="bf16"` (forward, gradients, train, hidden, dataset_loss) emulates
 the bf16-in / fp32-accumulate variant of the two input-layer products: X,
 W1 and dZ go to fp32 and then to the nearest bfloat16 before they are
@@ -77,6 +81,8 @@ def _load():
         lib.orc_bf16_array.argtypes = [P, P, i64]
         lib.orc_value_ties.restype = C.c_int
         lib.orc_value_ties.argtypes = [i32, i32, P, P, P, P, P, i32, dbl, P]
+        lib.orc_set_head.restype = C.c_int
+        lib.orc_set_head.argtypes = [C.c_int]
         lib.orc_dataset_loss.restype = C.c_int
         lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i64,
                                          i32, P, C.c_int]
@@ -119,6 +125,31 @@ def _rounding(mode: str):
         yield
     finally:
         lib.orc_set_input_rounding(0)
+
+
+_HEADS = {"ce": 0, "mse": 1}
+
+
+@contextlib.contextmanager
+def _head(head: str):
+    if head not in _HEADS:
+        raise ValueError("head must be one of %s" % sorted(_HEADS))
+    lib = _load()
+    _check(lib.orc_set_head(_HEADS[head]), "set_head")
+    try:
+        yield
+    finally:
+        lib.orc_set_head(0)
+
+
+def _labels(y, head: str, O: int, S: int) -> np.ndarray:
+    """int32 labels [S] (ce) or float32 targets [S, O] (mse)."""
+    if head == "mse":
+        t = _c(y, np.float32)
+        if t.shape != (S, O):
+            raise ValueError("mse targets must be [%d, %d]" % (S, O))
+        return t
+    return _c(y, np.int32)
 
 
 def bf16_round(x) -> np.ndarray:
@@ -182,7 +213,8 @@ def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
 
 def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
               with_allowance: bool = True, nthreads: int = 0, rounding: str = "exact",
-              tie_rel: float = 1e-5, cond_rel: float = 2.4e-7, b1=None, b2=None):
+              tie_rel: float = 1e-5, cond_rel: float = 2.4e-7, b1=None, b2=None,
+              head: str = "ce"):
     """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
 
     allow_dW1 bounds what a correct fp32 evaluation may differ by where a
@@ -194,13 +226,14 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     (cond_rel, about 4 units in the last fp32 place, times the excess).
 
     The gradient is that of sum_m L_m, so each model's slice is the gradient
-    of its own mean cross-entropy.  With biases b1 [N] and b2 [M, O] three more
+    of its own mean cross-entropy (or, with head="mse", mean squared error).  With biases b1 [N] and b2 [M, O] three more
     items follow: db1 [N], db2 [M, O] and the allowance of db1 [N] (that of a
     weight whose input is fixed at 1)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
-    W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
+    W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     B, F = Xf.shape
     O, N = W2d.shape
+    yi = _labels(y, head, O, B)
     dW1 = np.empty((N, F), np.float64)
     dW2 = np.empty((O, N), np.float64)
     loss = np.empty(len(hs), np.float64)
@@ -210,7 +243,7 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     db1 = np.empty(N, np.float64) if c1 is not None else None
     db2 = np.empty((M, O), np.float64) if c2 is not None else None
     allow_b = np.empty(N, np.float64) if (with_allowance and c1 is not None) else None
-    with _rounding(rounding):
+    with _rounding(rounding), _head(head):
         _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                      _p(c2), _p(Xf), _p(yi), B, _p(dW1), _p(dW2), _p(db1),
                                      _p(db2), _p(loss), _p(allow), _p(allow_b),
@@ -225,7 +258,7 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
 def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
           lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0,
           rounding: str = "exact", return_ties: bool = False, tie_rel: float = 1e-6,
-          b1=None, b2=None):
+          b1=None, b2=None, head: str = "ce"):
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
@@ -236,9 +269,10 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     tie_rel * sum_f |x w| of a jump of the activation, at that step's
     weights; see value_ties)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
-    W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
+    W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     F = Xf.shape[1]
     O, N = W2d.shape
+    yi = _labels(y, head, O, Xf.shape[0])
     off = np.asarray([b[0] for b in batches], np.int64)
     ln = np.asarray([b[1] for b in batches], np.int32)
     if len(batches) and (off.min() < 0 or (off + ln).max() > Xf.shape[0]):
@@ -258,7 +292,7 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
         if lr_m.size != len(hs):
             raise ValueError("per-model lr needs one rate per model")
         lr = 0.0
-    with _rounding(rounding):
+    with _rounding(rounding), _head(head):
         _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                  _p(c2), _p(Xf), _p(yi), len(batches), _p(off), _p(ln),
                                  float(lr), _p(lr_m), _p(W1o), _p(W2o), _p(b1o), _p(b2o),
@@ -305,13 +339,14 @@ def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
 
 def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,
                  nthreads: int = 0, rounding: str = "exact", b1=None,
-                 b2=None) -> np.ndarray:
+                 b2=None, head: str = "ce") -> np.ndarray:
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
-    W1d, W2d, Xf, yi = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32), _c(y, np.int32)
+    W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     S, F = Xf.shape
     O = W2d.shape[0]
+    yi = _labels(y, head, O, S)
     loss = np.empty(len(hs), np.float64)
-    with _rounding(rounding):
+    with _rounding(rounding), _head(head):
         c1 = _bias(b1, W2d.shape[1], "b1")
         c2 = _bias(b2, len(hs) * O, "b2")
         _check(_load().orc_dataset_loss(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d),

@@ -19,8 +19,9 @@
  *   its rows of the packed W1 [N,F] and its columns of the packed W2 [O,N],
  *   runs the three-step forward of Section 3 (input-to-hidden product, hidden
  *   activation, hidden-to-output product; no biases, as Section 3 drops them),
- *   a softmax cross-entropy loss, back-propagation (Section 2.3, Section 3)
- *   and a plain SGD update, batch after batch, in fp64.
+ *   a softmax cross-entropy loss (or, for regression, a mean squared error
+ *   against real targets), back-propagation (Section 2.3, Section 3) and a
+ *   plain SGD update, batch after batch, in fp64.
  *
  *   Readings of points the paper leaves open (loss, optimizer, activation
  *   kink conventions, initialisation) are listed in the design notes and
@@ -347,6 +348,46 @@ static double orc_model_ce(const orc_scratch* s, int B, const int32_t* y) {
   return total / (double)B;
 }
 
+/* The loss head (both heads are per model, mean over the batch):
+ *   0  softmax cross-entropy with integer labels y [B] (classification);
+ *   1  mean squared error against real targets t [B,O] (regression, which
+ *      the paper names as the method's other use, Section 5):
+ *        L = 1/(B O) sum_b sum_o (L[b,o] - t[b,o])^2,
+ *        G = dLoss/dL = 2 (L - t) / (B O).
+ * The label argument of the entry points is an int32 [B] array under head
+ * 0 and a float32 [B,O] array under head 1. */
+static int orc_head = 0;
+
+int orc_set_head(int head) {
+  if (head != 0 && head != 1) return ORC_EINVAL;
+  orc_head = head;
+  return ORC_OK;
+}
+
+static double orc_model_mse(const orc_scratch* s, int B, const float* t) {
+  const int O = s->O;
+  const double inv = 1.0 / ((double)B * O);
+  double total = 0.0;
+  for (int b = 0; b < B; ++b)
+    for (int o = 0; o < O; ++o) {
+      const double d = s->L[(int64_t)b * O + o] - (double)t[(int64_t)b * O + o];
+      total += d * d;
+      s->G[(int64_t)b * O + o] = 2.0 * d * inv;
+    }
+  return total * inv;
+}
+
+/* The labels (or targets) of samples s0 .. of a label array. */
+static const void* orc_labels_at(const void* y, int64_t s0, int O) {
+  return orc_head == 1 ? (const void*)((const float*)y + s0 * O)
+                       : (const void*)((const int32_t*)y + s0);
+}
+
+static double orc_model_loss(const orc_scratch* s, int B, const void* y) {
+  return orc_head == 1 ? orc_model_mse(s, B, (const float*)y)
+                       : orc_model_ce(s, B, (const int32_t*)y);
+}
+
 /* Back-propagation of the loss through one model (chain rule of the three
  * forward steps):
  *   dW2 = G^T H        [O,h]
@@ -450,15 +491,25 @@ static int32_t orc_model_value_ties(const orc_scratch* s, int B, const float* X,
  *   allow[j,f] += cond_rel * (mag - 16 |dH|) * |act'(Z)| * |X[b,f]|
  * summed over b (nothing where dH does not cancel). */
 static void orc_model_cond_allow(const orc_scratch* s, int B, const float* X,
-                                 const int32_t* y, const double* w2, double* allow,
+                                 const void* yv, const double* w2, double* allow,
                                  double* allow_b, double cond_rel) {
   const int F = s->F, O = s->O, h = s->h;
+  const int32_t* y = (const int32_t*)yv;
+  const float* t = (const float*)yv;
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < h; ++j) {
       double mag = 0.0;
       for (int o = 0; o < O; ++o) {
-        const double g = s->G[(int64_t)b * O + o];
-        const double gh = o == y[b] ? g + 2.0 / B : g;   /* (p + [o == y]) / B */
+        double gh;
+        if (orc_head == 1) {
+          /* an fp32 G = 2 (L - t) / (B O) is off by a few ulp of
+           * 2 (|L| + |t|) / (B O) where L and t nearly cancel */
+          gh = 2.0 * (fabs(s->L[(int64_t)b * O + o]) + fabs((double)t[(int64_t)b * O + o])) /
+               ((double)B * O);
+        } else {
+          const double g = s->G[(int64_t)b * O + o];
+          gh = o == y[b] ? g + 2.0 / B : g;   /* (p + [o == y]) / B */
+        }
         mag += gh * fabs(w2[(int64_t)o * h + j]);
       }
       const double excess = mag - 16.0 * fabs(s->dH[(int64_t)b * h + j]);
@@ -607,7 +658,7 @@ int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_
  * cancellation allowance of dH with cond_rel (0 switches it off). */
 int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
                   const double* W1, const double* W2, const double* b1, const double* b2,
-                  const float* X, const int32_t* y, int32_t B, double* dW1, double* dW2,
+                  const float* X, const void* y, int32_t B, double* dW1, double* dW2,
                   double* db1, double* db2, double* loss, double* allow_dW1,
                   double* allow_db1, double kink_rel, double tie_rel, double cond_rel,
                   int nthreads) {
@@ -635,7 +686,7 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
       orc_take(N, F, O, off[m], h, W1, W2, w1, w2);
       const double* bm1 = b1 ? b1 + off[m] : NULL;
       orc_model_forward(&s, B, X, w1, w2, bm1, b2 ? b2 + (int64_t)m * O : NULL);
-      loss[m] = orc_model_ce(&s, B, y);
+      loss[m] = orc_model_loss(&s, B, y);
       orc_model_backward(&s, B, X, w2, g1, g2, db1 ? db1 + off[m] : NULL,
                          db2 ? db2 + (int64_t)m * O : NULL);
       orc_put(N, F, O, off[m], h, g1, g2, dW1, dW2);
@@ -666,7 +717,7 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
  * update.  models/nmodels select a subset of the models (NULL: all).      */
 int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
               const double* W1, const double* W2, const double* b1, const double* b2,
-              const float* X, const int32_t* y,
+              const float* X, const void* y,
               int32_t nbatches, const int64_t* batch_off, const int32_t* batch_len,
               double lr, const double* lr_model, double* W1_out, double* W2_out,
               double* b1_out, double* b2_out, double* loss_last,
@@ -712,10 +763,10 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
       double last = NAN;
       for (int k = 0; k < nbatches; ++k) {
         const float* Xb = X + batch_off[k] * F;
-        const int32_t* yb = y + batch_off[k];
+        const void* yb = orc_labels_at(y, batch_off[k], O);
         const int B = batch_len[k];
         orc_model_forward(&s, B, Xb, w1, w2, c1, c2);
-        last = orc_model_ce(&s, B, yb);
+        last = orc_model_loss(&s, B, yb);
         if (ties) ties[m] += orc_model_value_ties(&s, B, Xb, w1, c1, tie_rel);
         orc_model_backward(&s, B, Xb, w2, g1, g2, c1 ? c1 + h : NULL, c2 ? c2 + O : NULL);
         const double lm = lr_model ? lr_model[m] : lr;
@@ -800,11 +851,11 @@ int orc_value_ties(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
   return ORC_OK;
 }
 
-/* Mean cross-entropy of every model over a whole sample set (no update),
+/* Mean loss (the head's) of every model over a whole sample set (no update),
  * evaluated in chunks of at most chunk samples. */
 int orc_dataset_loss(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t* acts,
                      const double* W1, const double* W2, const double* b1, const double* b2,
-                     const float* X, const int32_t* y, int64_t S, int32_t chunk, double* loss,
+                     const float* X, const void* y, int64_t S, int32_t chunk, double* loss,
                      int nthreads) {
   if (orc_check(F, O, M, hs, acts) || S < 1 || chunk < 1 || !W1 || !W2 || !X || !y || !loss)
     return ORC_EINVAL;
@@ -829,7 +880,7 @@ int orc_dataset_loss(int32_t F, int32_t O, int32_t M, const int32_t* hs, const i
         int B = (int)((S - s0) < chunk ? (S - s0) : chunk);
         orc_model_forward(&s, B, X + s0 * F, w1, w2, b1 ? b1 + off[m] : NULL,
                           b2 ? b2 + (int64_t)m * O : NULL);
-        total += orc_model_ce(&s, B, y + s0) * B;
+        total += orc_model_loss(&s, B, orc_labels_at(y, s0, O)) * B;
       }
       loss[m] = total / (double)S;
     }

@@ -117,6 +117,21 @@ def make_dataset(F: int, O: int, S: int, seed: int,
     return np.ascontiguousarray(X), y
 
 
+def make_regression_dataset(F: int, O: int, S: int, seed: int,
+                            noise: float = 0.1) -> Tuple[np.ndarray, np.ndarray]:
+    """X ~ N(0,1) [S,F] fp32 and real targets Y [S,O] fp32 from the same
+    seeded linear teacher: Y = X T / sqrt(F) + eps, eps ~ N(0, noise^2)
+    (for the regression head; the paper names regression as the method's
+    other use but describes no regression data)."""
+    root = np.random.default_rng(seed)
+    teacher_rng = np.random.default_rng(root.bit_generator.seed_seq.spawn(1)[0])
+    X = root.standard_normal((S, F), dtype=np.float32)
+    T = teacher_rng.standard_normal((F, O))
+    eps = teacher_rng.standard_normal((S, O)) * noise
+    Y = (X.astype(np.float64) @ T / np.sqrt(F) + eps).astype(np.float32)
+    return np.ascontiguousarray(X), np.ascontiguousarray(Y)
+
+
 def workload_dataset(w: Workload, S: Optional[int] = None):
     return make_dataset(w.F, w.O, w.S if S is None else S, w.data_seed)
 
