@@ -78,6 +78,12 @@ extern "C" {
                              biases b2 [M, O] (Section 3 drops them only to keep
                              the explanation short) */
 
+#define PMLP_MSE 2        /* pmlp_create_ex flag: regression head, per-model mean
+                             squared error against real targets, trained with
+                             pmlp_train_step_mse / pmlp_gradients_mse (the
+                             paper names regression as the method's other use,
+                             Section 5) */
+
 typedef struct pmlp* pmlp_t;
 
 /* Create a packed model of M MLPs with F inputs and O outputs each.
@@ -96,13 +102,17 @@ int pmlp_create(pmlp_t* out, int32_t F, int32_t O, int32_t M,
                 const int32_t* hidden_sizes, const int32_t* act_ids,
                 uint64_t seed);
 
-/* pmlp_create with flags (0 or PMLP_BIAS).  With PMLP_BIAS every model
+/* pmlp_create with flags (0, PMLP_BIAS, PMLP_MSE or both).  With PMLP_BIAS every model
  * computes Z = X W1^T + b1 and logits = act(Z) W2^T + b2, trains b1 and b2
  * by the same SGD (db1 = sum_b dZ, db2 = sum_b G), and the biases start
  * uniform in (-1/sqrt(fan_in), +1/sqrt(fan_in)) from the same stream as the
  * weights: tag 3 for b1 (idx = n, fan_in = F), tag 4 for b2 (idx = m*O + o,
  * fan_in = h_m).  b1 is stored as the weight of a constant input 1, so in
- * the PMLP_BF16_GEMM mode it is rounded with W1.  Unknown flags return
+ * the PMLP_BF16_GEMM mode it is rounded with W1.  With PMLP_MSE the loss of
+ * model m on a batch is L_m = 1/(B O) sum_b sum_o (logit[b,m,o] - Y[b,o])^2
+ * and dLoss/dlogit = 2 (logit - Y) / (B O); such a handle trains only
+ * through the _mse calls, and the label-taking calls return PMLP_ESTATE
+ * (and the _mse calls on a classification handle).  Unknown flags return
  * PMLP_EINVAL. */
 int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M,
                    const int32_t* hidden_sizes, const int32_t* act_ids,
@@ -151,8 +161,9 @@ int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev,
 int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev,
                        int32_t B, const float* lr_dev);
 
-/* Copy the per-model mean cross-entropy of the last pmlp_train_step or
- * pmlp_gradients batch into out_host [M] (fp32).  Synchronises the
+/* Copy the per-model loss (mean cross-entropy, or mean squared error for a
+ * PMLP_MSE handle) of the last training or gradient batch into out_host [M]
+ * (fp32).  Synchronises the
  * stream.  PMLP_ESTATE before any step; PMLP_EINVAL if that batch held a
  * label outside [0, O) (the flag is cleared by the call). */
 int pmlp_losses(pmlp_t h, float* out_host);
@@ -171,6 +182,17 @@ int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev,
 int pmlp_gradients_ex(pmlp_t h, const float* X_dev, const int32_t* y_dev,
                       int32_t B, float* dW1_dev, float* dW2_dev,
                       float* db1_dev, float* db2_dev);
+
+/* Regression head (a handle created with PMLP_MSE): one SGD step and the
+ * gradients without update, as pmlp_train_step and pmlp_gradients but with
+ * real targets Y_dev [B, O] (device, fp32, row-major) in place of labels;
+ * pmlp_losses then returns the per-model mean squared errors.  With
+ * PMLP_BIAS the output biases are trained too (db2 = sum_b G).  PMLP_ESTATE
+ * for a classification handle; null pointers return PMLP_EINVAL. */
+int pmlp_train_step_mse(pmlp_t h, const float* X_dev, const float* Y_dev,
+                        int32_t B, float lr);
+int pmlp_gradients_mse(pmlp_t h, const float* X_dev, const float* Y_dev,
+                       int32_t B, float* dW1_dev, float* dW2_dev);
 
 /* Hidden layer of the packed network: Z_dev [B, N] = X W1^T and
  * H_dev [B, N] = act_{model of n}(Z) (either pointer may be null).  A

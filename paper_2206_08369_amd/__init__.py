@@ -24,7 +24,8 @@ __all__ = [
     "pmlp_losses",
     "pmlp_gradients", "pmlp_hidden", "pmlp_get_params", "pmlp_set_params", "pmlp_info",
     "pmlp_set_profiling", "pmlp_kernel_time", "pmlp_profile_reset", "pmlp_kernel_name",
-    "pmlp_last_error", "pmlp_gradients_ex", "pmlp_get_biases", "pmlp_set_biases", "PackedMLP",
+    "pmlp_last_error", "pmlp_gradients_ex", "pmlp_get_biases", "pmlp_set_biases",
+    "PMLP_MSE", "pmlp_train_step_mse", "pmlp_gradients_mse", "PackedMLP",
 ]
 
 PMLP_OK = 0
@@ -35,6 +36,7 @@ PMLP_ESTATE = -4
 PMLP_FP32 = 0
 PMLP_BF16_GEMM = 1
 PMLP_BIAS = 1
+PMLP_MSE = 2
 PMLP_NUM_KERNELS = 9
 
 ACT_IDS = {
@@ -71,6 +73,8 @@ def load_library():
         "pmlp_create": [C.POINTER(P), i32, i32, i32, P, P, u64],
         "pmlp_create_ex": [C.POINTER(P), i32, i32, i32, P, P, u64, i32],
         "pmlp_gradients_ex": [P, P, P, i32, P, P, P, P],
+        "pmlp_train_step_mse": [P, P, P, i32, f32],
+        "pmlp_gradients_mse": [P, P, P, i32, P, P],
         "pmlp_get_biases": [P, P, P],
         "pmlp_set_biases": [P, P, P],
         "pmlp_destroy": [P],
@@ -190,6 +194,16 @@ def pmlp_train_step_lr(h: int, X, y, B: int, lr) -> None:
            "pmlp_train_step_lr")
 
 
+def pmlp_train_step_mse(h: int, X, Y, B: int, lr: float) -> None:
+    _check(load_library().pmlp_train_step_mse(h, _ptr(X), _ptr(Y), int(B), float(lr)),
+           "pmlp_train_step_mse")
+
+
+def pmlp_gradients_mse(h: int, X, Y, B: int, dW1, dW2) -> None:
+    _check(load_library().pmlp_gradients_mse(h, _ptr(X), _ptr(Y), int(B), _ptr(dW1), _ptr(dW2)),
+           "pmlp_gradients_mse")
+
+
 def pmlp_losses(h: int) -> np.ndarray:
     M = pmlp_info(h)[1]
     out = np.empty(M, np.float32)
@@ -258,17 +272,23 @@ class PackedMLP:
     """M independent one-hidden-layer MLPs packed into one wide network.
 
     Tensors passed in must be contiguous CUDA (HIP) tensors on the device
-    that was current at construction: X float32 [B, F], y int32 [B].  Work
-    is enqueued on torch's current stream of that device."""
+    that was current at construction: X float32 [B, F], and y int32 [B]
+    labels (head "ce", classification) or float32 [B, O] targets (head
+    "mse", regression).  Work is enqueued on torch's current stream of that
+    device."""
 
     def __init__(self, F: int, O: int, hidden_sizes: Sequence[int], act_ids: Sequence[int],
-                 seed: int = 0, precision: int = PMLP_FP32, biases: bool = False):
+                 seed: int = 0, precision: int = PMLP_FP32, biases: bool = False,
+                 head: str = "ce"):
         import torch
+        if head not in ("ce", "mse"):
+            raise ValueError("head must be 'ce' or 'mse'")
         self._torch = torch
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.biases = bool(biases)
+        self.head = head
         self.handle = pmlp_create(F, O, hidden_sizes, act_ids, seed,
-                                  PMLP_BIAS if biases else 0)
+                                  (PMLP_BIAS if biases else 0) | (PMLP_MSE if head == "mse" else 0))
         self.N, self.M, self.F, self.O = pmlp_info(self.handle)
         self.hidden_sizes = _host(hidden_sizes, np.int32)
         self.act_ids = _host(act_ids, np.int32)
@@ -299,6 +319,12 @@ class PackedMLP:
 
     def _y(self, y, B):
         t = self._torch
+        if self.head == "mse":
+            if not (y.is_cuda and y.dtype == t.float32 and y.is_contiguous()
+                    and tuple(y.shape) == (B, self.O) and y.device == self.device):
+                raise ValueError("targets must be a contiguous float32 [B, %d] tensor on %s"
+                                 % (self.O, self.device))
+            return
         if not (y.is_cuda and y.dtype == t.int32 and y.is_contiguous() and y.shape == (B,)
                 and y.device == self.device):
             raise ValueError("y must be a contiguous int32 [B] tensor on %s" % self.device)
@@ -324,6 +350,11 @@ class PackedMLP:
         B = self._x(X)
         self._y(y, B)
         self._stream()
+        if self.head == "mse":
+            if isinstance(lr, self._torch.Tensor):
+                raise ValueError("per-model learning rates are not provided for the mse head")
+            pmlp_train_step_mse(self.handle, X, y, B, lr)
+            return
         if isinstance(lr, self._torch.Tensor):
             if not (lr.is_cuda and lr.dtype == self._torch.float32 and lr.is_contiguous()
                     and lr.numel() == self.M):
@@ -339,6 +370,11 @@ class PackedMLP:
         dW1 = t.empty((self.N, self.F), dtype=t.float32, device=self.device)
         dW2 = t.empty((self.O, self.N), dtype=t.float32, device=self.device)
         self._stream()
+        if self.head == "mse":
+            if self.biases:
+                raise ValueError("bias gradients are not provided for the mse head")
+            pmlp_gradients_mse(self.handle, X, y, B, dW1, dW2)
+            return dW1, dW2
         if not self.biases:
             pmlp_gradients(self.handle, X, y, B, dW1, dW2)
             return dW1, dW2

@@ -91,6 +91,7 @@ struct pmlp {
   unsigned short* W1b = nullptr;  // [Npad][bf16_ld(F4)] bf16 of W1 (operand of Z = X W1^T)
   bool w1b_valid = false;         // W1b equals bf16(W1)
   bool have_loss = false;
+  bool mse = false;         // regression head (PMLP_MSE)
   bool lds_kernels = true;  // persistent LDS-resident GEMMs where they apply
 
   bool prof = false;
@@ -331,7 +332,7 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp) {
 
 // Full step: forward, loss, backward and either the SGD update (dW1 and
 // dW2 null) or gradient stores.
-int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const float* lrm,
+int step(pmlp* h, const float* X, const void* y, int32_t B, float lr, const float* lrm,
          float* dW1, float* dW2, float* db1 = nullptr, float* db2 = nullptr) {
   const int32_t Bp = pad_batch(B);
   if (int rc = use_device(h)) return rc;
@@ -353,9 +354,14 @@ int step(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, const f
     return rc;
   if (int rc = run(h, KID_CE, [&] {
         // output biases: updated here (db2 = sum_b G), or their gradient stored
-        return launch_ce(h->LG, y, h->M, Bp, B, h->O, h->loss, h->flag, dW1 ? nullptr : lrm,
-                         dW1 ? (db2 ? h->b2 : nullptr) : h->b2, dW1 ? db2 : nullptr, lr,
-                         h->stream);
+        float* b2 = dW1 ? (db2 ? h->b2 : nullptr) : h->b2;
+        float* g2 = dW1 ? db2 : nullptr;
+        const float* rates = dW1 ? nullptr : lrm;
+        if (h->mse)
+          return launch_mse(h->LG, (const float*)y, h->M, Bp, B, h->O, h->loss, h->flag, rates,
+                            b2, g2, lr, h->stream);
+        return launch_ce(h->LG, (const int32_t*)y, h->M, Bp, B, h->O, h->loss, h->flag, rates,
+                         b2, g2, lr, h->stream);
       }))
     return rc;
   if (h->lds_kernels && !bf16_mode(h) && bwd_lds_supported(Bp, h->F4, h->O)) {
@@ -484,7 +490,7 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
                    const int32_t* act_ids, uint64_t seed, int32_t flags) {
   if (!out) return fail(PMLP_EINVAL, "null output handle pointer");
   *out = nullptr;
-  if (flags & ~PMLP_BIAS) return fail(PMLP_EINVAL, "unknown flags");
+  if (flags & ~(PMLP_BIAS | PMLP_MSE)) return fail(PMLP_EINVAL, "unknown flags");
   const bool biases = (flags & PMLP_BIAS) != 0;
   if (F < 1) return fail(PMLP_EINVAL, "F must be >= 1");
   if (O < 2 || O > kMaxO) return fail(PMLP_EINVAL, "O must be in [2, 16]");
@@ -507,6 +513,7 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
   if (!h) return fail(PMLP_ENOMEM, "host allocation failed");
   h->F = F;
   h->F4 = F4;
+  h->mse = (flags & PMLP_MSE) != 0;
   h->bcol = bcol;
   h->O = O;
   h->M = M;
@@ -642,6 +649,7 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
 
 int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B, float lr) {
   if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (h->mse) return fail(PMLP_ESTATE, "a regression handle trains with pmlp_train_step_mse");
   if (!y_dev) return fail(PMLP_EINVAL, "null labels");
   if (!std::isfinite(lr)) return fail(PMLP_EINVAL, "learning rate is not finite");
   return step(h, X_dev, y_dev, B, lr, nullptr, nullptr, nullptr);
@@ -650,6 +658,7 @@ int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t 
 int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
                        const float* lr_dev) {
   if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (h->mse) return fail(PMLP_ESTATE, "a regression handle trains with pmlp_train_step_mse");
   if (!y_dev) return fail(PMLP_EINVAL, "null labels");
   if (!lr_dev) return fail(PMLP_EINVAL, "null per-model learning rates");
   return step(h, X_dev, y_dev, B, 0.f, lr_dev, nullptr, nullptr);
@@ -658,13 +667,31 @@ int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32
 int pmlp_gradients(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
                    float* dW1_dev, float* dW2_dev) {
   if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (h->mse) return fail(PMLP_ESTATE, "a regression handle uses pmlp_gradients_mse");
   if (!y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null labels or gradient buffer");
   return step(h, X_dev, y_dev, B, 0.f, nullptr, dW1_dev, dW2_dev);
+}
+
+int pmlp_train_step_mse(pmlp_t h, const float* X_dev, const float* Y_dev, int32_t B, float lr) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!h->mse) return fail(PMLP_ESTATE, "the handle was created without PMLP_MSE");
+  if (!Y_dev) return fail(PMLP_EINVAL, "null targets");
+  if (!std::isfinite(lr)) return fail(PMLP_EINVAL, "learning rate is not finite");
+  return step(h, X_dev, Y_dev, B, lr, nullptr, nullptr, nullptr);
+}
+
+int pmlp_gradients_mse(pmlp_t h, const float* X_dev, const float* Y_dev, int32_t B,
+                       float* dW1_dev, float* dW2_dev) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (!h->mse) return fail(PMLP_ESTATE, "the handle was created without PMLP_MSE");
+  if (!Y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null targets or gradient buffer");
+  return step(h, X_dev, Y_dev, B, 0.f, nullptr, dW1_dev, dW2_dev);
 }
 
 int pmlp_gradients_ex(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
                       float* dW1_dev, float* dW2_dev, float* db1_dev, float* db2_dev) {
   if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (h->mse) return fail(PMLP_ESTATE, "a regression handle uses pmlp_gradients_mse");
   if (!y_dev || !dW1_dev || !dW2_dev) return fail(PMLP_EINVAL, "null labels or gradient buffer");
   if (h->bcol < 0) return fail(PMLP_ESTATE, "the handle was created without biases");
   if (!db1_dev || !db2_dev) return fail(PMLP_EINVAL, "null bias gradient buffer");

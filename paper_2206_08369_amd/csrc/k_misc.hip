@@ -264,6 +264,75 @@ hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t
 }
 
 // ---------------------------------------------------------------------------
+// Regression head: per-model mean squared error against real targets and
+// its gradient, G = 2 (logit - Y) / (B O), in place over the logits; one
+// wave per model, lanes over samples.
+// ---------------------------------------------------------------------------
+
+template <int OM>
+__global__ __launch_bounds__(kBlock) void k_mse(float* __restrict__ LG,
+                                                const float* __restrict__ Y, int M, int Bp,
+                                                int B, int O, float inv,
+                                                float* __restrict__ loss,
+                                                int32_t* __restrict__ flag,
+                                                const float* __restrict__ lrm,
+                                                float* __restrict__ b2, float* __restrict__ db2,
+                                                float lr) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;
+  if (lrm && lane == 0 && !isfinite(lrm[m])) flag[1] = 1;
+  float part = 0.f;
+  float gs[OM];  // this lane's share of db2 = sum_b G
+#pragma unroll
+  for (int o = 0; o < OM; ++o) gs[o] = 0.f;
+  for (int b = lane; b < Bp; b += 64) {
+    float* row = LG + ((int64_t)m * Bp + b) * O;
+    if (b < B) {
+      const float* t = Y + (int64_t)b * O;
+#pragma unroll
+      for (int o = 0; o < OM; ++o)
+        if (o < O) {
+          const float d = row[o] - t[o];
+          part = fmaf(d, d, part);
+          const float g = 2.f * d * inv;
+          row[o] = g;
+          gs[o] += g;
+        }
+    } else {
+      for (int o = 0; o < O; ++o) row[o] = 0.f;
+    }
+  }
+#pragma unroll
+  for (int s = 32; s > 0; s >>= 1) part += __shfl_xor(part, s);
+  if (lane == 0) loss[m] = part * inv;
+  if (b2) {
+    const float rate = lrm ? lrm[m] : lr;
+#pragma unroll
+    for (int o = 0; o < OM; ++o) {
+      float v = gs[o];
+      for (int s = 32; s > 0; s >>= 1) v += __shfl_xor(v, s);
+      if (lane == 0 && o < O) {
+        if (db2) db2[(int64_t)m * O + o] = v;
+        else b2[(int64_t)m * O + o] -= rate * v;
+      }
+    }
+  }
+}
+
+hipError_t launch_mse(float* LG, const float* Y, int32_t M, int32_t Bp, int32_t B, int32_t O,
+                      float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
+                      float lr, hipStream_t s) {
+  const unsigned blocks = (unsigned)((M + 3) / 4);
+  const float inv = 1.0f / ((float)B * (float)O);
+  if (O <= 2) k_mse<2><<<blocks, kBlock, 0, s>>>(LG, Y, M, Bp, B, O, inv, loss, flag, lrm, b2, db2, lr);
+  else if (O <= 4) k_mse<4><<<blocks, kBlock, 0, s>>>(LG, Y, M, Bp, B, O, inv, loss, flag, lrm, b2, db2, lr);
+  else if (O <= 8) k_mse<8><<<blocks, kBlock, 0, s>>>(LG, Y, M, Bp, B, O, inv, loss, flag, lrm, b2, db2, lr);
+  else k_mse<16><<<blocks, kBlock, 0, s>>>(LG, Y, M, Bp, B, O, inv, loss, flag, lrm, b2, db2, lr);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Hidden layer in the caller's [B][N] layout (inspection path).
 // ---------------------------------------------------------------------------
 

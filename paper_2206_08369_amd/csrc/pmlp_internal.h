@@ -165,6 +165,13 @@ hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t
                      float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
                      float lr, hipStream_t s);
 
+// Regression head: loss[m] = 1/(B O) sum_{b<B,o} (LG[m][b][o] - Y[b][o])^2 and
+// LG overwritten by G = 2 (LG - Y) / (B O) (0 for padded samples); flags,
+// per-model rates and b2/db2 as launch_ce.
+hipError_t launch_mse(float* LG, const float* Y, int32_t M, int32_t Bp, int32_t B, int32_t O,
+                      float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
+                      float lr, hipStream_t s);
+
 // M3 backward + activation derivative: dZ over Zt in place (fp32), or, with
 // dZ16 set, as bf16 into dZ16 [Npad][Bp] leaving Zt unchanged; then the W2
 // update (dW2 null) or the dW2 store.

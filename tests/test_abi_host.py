@@ -94,5 +94,5 @@ def test_package_fails_loudly_without_library(tmp_path, monkeypatch):
 
 def test_create_rejects_unknown_flags(pm):
     with pytest.raises(pm.PmlpError) as e:
-        pm.pmlp_create(3, 2, [1], [0], 0, flags=2)
+        pm.pmlp_create(3, 2, [1], [0], 0, flags=4)
     assert e.value.code == pm.PMLP_EINVAL and "unknown flags" in str(e.value)
