@@ -248,6 +248,196 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds_ring(FwdLdsArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Forward for wide batches on the bf16 matrix cores at fp32 accuracy.
+//
+// Every fp32 operand a is split into three bf16 pieces with round-to-nearest,
+//   a = a0 + a1 + a2 + r,  |a1| <= 2^-9 |a|,  |a2| <= 2^-18 |a|,  |r| <= 2^-27 |a|,
+// and a product a b is taken as the six piece products of magnitude up to
+// 2^-18 |a b| (a0 b0, a0 b1, a1 b0, a0 b2, a1 b1, a2 b0), each exact in the
+// fp32 accumulator.  The three products left out and the residuals add up
+// to a few times 2^-27 |a b|, below the rounding of one fp32 product
+// (2^-24), so the result carries the error of an fp32 dot product, while
+// six v_mfma_f32_16x16x32_bf16 (32 k values each) stand in for the eight
+// v_mfma_f32_16x16x4f32 of the same 32 k values at about a third of their
+// issue time.  The batch is split once per workgroup into three LDS planes
+// in MFMA-operand order (plane slot (i*NC + c)*64 + l holds the eight k
+// values 32c + 8(l/16) .. +7 of sample 16i + l%16); the W1 strips are split
+// in registers, each piece then serving all TQ sample tiles.  A wave takes
+// U tiles of 16 units at a time, so every LDS operand feeds U products.
+// The last K mod 32 columns (a multiple of 4) take fp32 MFMA steps as in
+// k_fwd_lds.  Operands above about 3.4e38 in magnitude would overflow the
+// first piece; weights and inputs of a network in training are far below.
+// ---------------------------------------------------------------------------
+
+static constexpr int kX3RemMax = 7;  // fp32 remainder steps: K mod 32 <= 28
+
+__device__ __forceinline__ void split3(const f32x4& a, const f32x4& b, bf16x8& p0, bf16x8& p1,
+                                       bf16x8& p2) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float x = j < 4 ? a[j] : b[j - 4];
+    const __bf16 h = (__bf16)x;
+    const float r1 = x - (float)h;
+    const __bf16 m = (__bf16)r1;
+    p0[j] = h;
+    p1[j] = m;
+    p2[j] = (__bf16)(r1 - (float)m);
+  }
+}
+
+// acc += a b for one 32-wide k chunk, smallest piece products first
+__device__ __forceinline__ f32x4 mfma_x3(const bf16x8& a0, const bf16x8& a1, const bf16x8& a2,
+                                         const bf16x8& b0, const bf16x8& b1, const bf16x8& b2,
+                                         f32x4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b0, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b2, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b0, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b1, acc, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc, 0, 0, 0);
+}
+
+template <int NC, int U>
+struct X3Strip {
+  f32x4 c[U][2 * NC];
+  float t[U][kX3RemMax];
+};
+
+// W1 rows (t*U + u)*16 + li: k = 32c + 8lk .. +7 per chunk and the
+// remainder values k = 32NC + 4s + lk (steps past rem repeat step 0).
+template <int NC, int U>
+__device__ __forceinline__ void x3_load(X3Strip<NC, U>& st, const float* __restrict__ W1,
+                                        int64_t t, int64_t N, int K, int rem, int li, int lk) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    int64_t p = (t * U + u) * 16 + li;
+    if (p > N - 1) p = N - 1;
+    const float* row = W1 + p * K;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      st.c[u][2 * c] = *(const f32x4*)(row + 32 * c + 8 * lk);
+      st.c[u][2 * c + 1] = *(const f32x4*)(row + 32 * c + 8 * lk + 4);
+    }
+#pragma unroll
+    for (int s = 0; s < kX3RemMax; ++s) {
+      int off = 32 * NC + 4 * (s < rem ? s : 0) + lk;
+      if (off > K - 1) off = K - 1;
+      st.t[u][s] = row[off];
+    }
+  }
+}
+
+template <int TQ, int NC, int U>
+__global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
+  extern __shared__ float lds[];
+  const int K = a.K;
+  const int rem = (K - 32 * NC) >> 2;
+  constexpr int PS = TQ * NC * 64;  // 16-byte slots per plane
+  bf16x8* planes = (bf16x8*)lds;
+  for (int slot = threadIdx.x; slot < PS; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / NC, c = rest - (rest / NC) * NC;
+    const float* src = a.Xp + (int64_t)(16 * i + (l & 15)) * K + 32 * c + 8 * (l >> 4);
+    bf16x8 p0, p1, p2;
+    split3(*(const f32x4*)src, *(const f32x4*)(src + 4), p0, p1, p2);
+    planes[slot] = p0;
+    planes[PS + slot] = p1;
+    planes[2 * PS + slot] = p2;
+  }
+  // remainder: float slot T0 + (i*rem + s)*64 + l = Xp[16i + l%16][32NC + 4s + l/16]
+  constexpr int T0 = 3 * PS * 4;
+  for (int slot = threadIdx.x; slot < TQ * rem * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / rem, s = rest - (rest / rem) * rem;
+    lds[T0 + slot] = a.Xp[(int64_t)(16 * i + (l & 15)) * K + 32 * NC + 4 * s + (l >> 4)];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t T = (a.N + 16 * U - 1) / (16 * U);
+  const int64_t tstride = (int64_t)gridDim.x * kLdsWaves;
+  int64_t t = (int64_t)blockIdx.x * kLdsWaves + wave;
+  if (t >= T) return;
+  const bf16x8* xq = planes + lane;  // + plane*PS + (i*NC + c)*64
+  const float* qtail = lds + T0 + lane;
+  // The strip of the next tile is loaded at the top of each tile and split
+  // at its end, so the products only read registers written by VALU
+  // instructions and no wait on memory falls inside the tile.
+  X3Strip<NC, U> nxt;
+  x3_load(nxt, a.W1, t, a.N, K, rem, li, lk);
+  bf16x8 w0[U][NC], w1[U][NC], w2[U][NC];
+  float wt[U][kX3RemMax];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      split3(nxt.c[u][2 * c], nxt.c[u][2 * c + 1], w0[u][c], w1[u][c], w2[u][c]);
+#pragma unroll
+    for (int s = 0; s < kX3RemMax; ++s) wt[u][s] = nxt.t[u][s];
+  }
+  for (; t < T; t += tstride) {
+    const int64_t tn = t + tstride < T ? t + tstride : t;
+    x3_load(nxt, a.W1, tn, a.N, K, rem, li, lk);
+    __builtin_amdgcn_sched_barrier(0);
+    // The six products of one accumulator issue back to back (the chained
+    // accumulator is forwarded instead of read back from VGPRs, which
+    // roughly halves the issue time of this MFMA); the LDS operands of the
+    // next chunk are read one chunk ahead.
+    bf16x8 xn0 = xq[0], xn1 = xq[PS], xn2 = xq[2 * PS];
+#pragma unroll
+    for (int i = 0; i < TQ; ++i) {
+      f32x4 acc[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // remainder operands of this sample tile, read before the chunks
+      float qt[kX3RemMax];
+      if (rem > 0) {
+#pragma unroll
+        for (int s = 0; s < kX3RemMax; ++s) qt[s] = qtail[(i * rem + (s < rem ? s : rem - 1)) * 64];
+      }
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const bf16x8 x0 = xn0, x1 = xn1, x2 = xn2;
+        if (i * NC + c + 1 < TQ * NC) {
+          const int o = (i * NC + c + 1) * 64;
+          xn0 = xq[o];
+          xn1 = xq[PS + o];
+          xn2 = xq[2 * PS + o];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          __builtin_amdgcn_sched_barrier(0);
+          acc[u] = mfma_x3(x0, x1, x2, w0[u][c], w1[u][c], w2[u][c], acc[u]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int s = 0; s < kX3RemMax; ++s) {
+        if (s < rem) {
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            acc[u] = __builtin_amdgcn_mfma_f32_16x16x4f32(qt[s], wt[u][s], acc[u], 0, 0, 0);
+        }
+      }
+      // Zt rows are padded to a multiple of 64, so every store is in bounds.
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        *(f32x4*)(a.Zt + ((t * U + u) * 16 + li) * (int64_t)(16 * TQ) + 16 * i + 4 * lk) = acc[u];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        split3(nxt.c[u][2 * c], nxt.c[u][2 * c + 1], w0[u][c], w1[u][c], w2[u][c]);
+#pragma unroll
+      for (int s = 0; s < kX3RemMax; ++s) wt[u][s] = nxt.t[u][s];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Fused backward: M3 backward + activation derivative + dW1 GEMM + both SGD
 // updates in one pass over Zt (dZ is never stored).
 //
@@ -770,11 +960,36 @@ bool fwd_lds_supported(int32_t Bp, int32_t F4) {
 
 // Narrow inputs and batches (K = 16 or 32, Bp <= 64): two chunk registers,
 // no remainder, four strips in flight; otherwise the one-tile-ahead kernel.
+// Batches of 128 and 256 samples: the bf16 three-piece kernel when its
+// three planes fit in LDS; two unit tiles per wave while the split strips
+// of both fit in registers (K < 128), one above.
+static size_t fwd_x3_bytes(int32_t Bp, int32_t K) {
+  return (size_t)3 * Bp * (K / 32) * 64 + (size_t)Bp * ((K % 32) / 4) * 16;
+}
+
+template <int TQ, int NC>
+static hipError_t fwd_x3_go(const FwdLdsArgs& a, hipStream_t s) {
+  constexpr int U = NC <= 3 ? 2 : 1;
+  const int64_t T = (a.N + 16 * U - 1) / (16 * U);
+  return launch_persistent(k_fwd_x3<TQ, NC, U>, kLdsBlock, fwd_x3_bytes(a.Bp, a.K), T, s, a);
+}
+
 template <int TQ>
 static hipError_t fwd_lds_go(const FwdLdsArgs& a, size_t lds, int64_t T, hipStream_t s) {
-  if constexpr (TQ <= 4)
+  if constexpr (TQ <= 4) {
     if (a.K <= 32 && a.K % 16 == 0)
       return launch_persistent(k_fwd_lds_ring<TQ, 2, 0, 4>, kLdsBlock, lds, T, s, a);
+  } else {
+    if (fwd_x3_bytes(a.Bp, a.K) <= (size_t)dev_info().lds_max) {
+      switch (a.K / 32) {
+        case 1: return fwd_x3_go<TQ, 1>(a, s);
+        case 2: return fwd_x3_go<TQ, 2>(a, s);
+        case 3: return fwd_x3_go<TQ, 3>(a, s);
+        case 4: if constexpr (TQ == 8) return fwd_x3_go<TQ, 4>(a, s); break;  // K <= 140
+        default: break;
+      }
+    }
+  }
   return launch_persistent(k_fwd_lds<TQ>, kLdsBlock, lds, T, s, a);
 }
 
