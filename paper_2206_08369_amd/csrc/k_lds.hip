@@ -271,18 +271,32 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds_ring(FwdLdsArgs a) {
 
 static constexpr int kX3RemMax = 7;  // fp32 remainder steps: K mod 32 <= 28
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// two values at a time: one packed conversion per piece, the pieces read
+// back as floats from the low and high halves
+__device__ __forceinline__ uint32_t bf16_pair(f32x2 v) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+__device__ __forceinline__ f32x2 bf16_pair_value(uint32_t p) {
+  return f32x2{__builtin_bit_cast(float, p << 16), __builtin_bit_cast(float, p & 0xffff0000u)};
+}
+
 __device__ __forceinline__ void split3(const f32x4& a, const f32x4& b, bf16x8& p0, bf16x8& p1,
                                        bf16x8& p2) {
+  uint32_t q0[4], q1[4], q2[4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float x = j < 4 ? a[j] : b[j - 4];
-    const __bf16 h = (__bf16)x;
-    const float r1 = x - (float)h;
-    const __bf16 m = (__bf16)r1;
-    p0[j] = h;
-    p1[j] = m;
-    p2[j] = (__bf16)(r1 - (float)m);
+  for (int j = 0; j < 4; ++j) {
+    const f32x2 x = j < 2 ? f32x2{a[2 * j], a[2 * j + 1]} : f32x2{b[2 * j - 4], b[2 * j - 3]};
+    q0[j] = bf16_pair(x);
+    const f32x2 r1 = x - bf16_pair_value(q0[j]);
+    q1[j] = bf16_pair(r1);
+    q2[j] = bf16_pair(r1 - bf16_pair_value(q1[j]));
   }
+  p0 = __builtin_bit_cast(bf16x8, q0);
+  p1 = __builtin_bit_cast(bf16x8, q1);
+  p2 = __builtin_bit_cast(bf16x8, q2);
 }
 
 // acc += a b for one 32-wide k chunk, smallest piece products first
@@ -297,16 +311,16 @@ __device__ __forceinline__ f32x4 mfma_x3(const bf16x8& a0, const bf16x8& a1, con
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc, 0, 0, 0);
 }
 
-template <int NC, int U>
+template <int NC, int U, int RM>
 struct X3Strip {
   f32x4 c[U][2 * NC];
-  float t[U][kX3RemMax];
+  float t[U][RM > 0 ? RM : 1];
 };
 
 // W1 rows (t*U + u)*16 + li: k = 32c + 8lk .. +7 per chunk and the
 // remainder values k = 32NC + 4s + lk (steps past rem repeat step 0).
-template <int NC, int U>
-__device__ __forceinline__ void x3_load(X3Strip<NC, U>& st, const float* __restrict__ W1,
+template <int NC, int U, int RM>
+__device__ __forceinline__ void x3_load(X3Strip<NC, U, RM>& st, const float* __restrict__ W1,
                                         int64_t t, int64_t N, int K, int rem, int li, int lk) {
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -319,7 +333,7 @@ __device__ __forceinline__ void x3_load(X3Strip<NC, U>& st, const float* __restr
       st.c[u][2 * c + 1] = *(const f32x4*)(row + 32 * c + 8 * lk + 4);
     }
 #pragma unroll
-    for (int s = 0; s < kX3RemMax; ++s) {
+    for (int s = 0; s < RM; ++s) {
       int off = 32 * NC + 4 * (s < rem ? s : 0) + lk;
       if (off > K - 1) off = K - 1;
       st.t[u][s] = row[off];
@@ -327,11 +341,13 @@ __device__ __forceinline__ void x3_load(X3Strip<NC, U>& st, const float* __restr
   }
 }
 
-template <int TQ, int NC, int U>
+// RM: the number of fp32 remainder steps when below kX3RemMax, else a
+// bound on the run-time number.
+template <int TQ, int NC, int U, int RM>
 __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
   extern __shared__ float lds[];
   const int K = a.K;
-  const int rem = (K - 32 * NC) >> 2;
+  const int rem = RM < kX3RemMax ? RM : (K - 32 * NC) >> 2;
   constexpr int PS = TQ * NC * 64;  // 16-byte slots per plane
   bf16x8* planes = (bf16x8*)lds;
   for (int slot = threadIdx.x; slot < PS; slot += kLdsBlock) {
@@ -346,9 +362,10 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
   }
   // remainder: float slot T0 + (i*rem + s)*64 + l = Xp[16i + l%16][32NC + 4s + l/16]
   constexpr int T0 = 3 * PS * 4;
+  const int rdiv = rem > 0 ? rem : 1;
   for (int slot = threadIdx.x; slot < TQ * rem * 64; slot += kLdsBlock) {
     const int l = slot & 63, rest = slot >> 6;
-    const int i = rest / rem, s = rest - (rest / rem) * rem;
+    const int i = rest / rdiv, s = rest - (rest / rdiv) * rdiv;
     lds[T0 + slot] = a.Xp[(int64_t)(16 * i + (l & 15)) * K + 32 * NC + 4 * s + (l >> 4)];
   }
   __syncthreads();
@@ -364,17 +381,17 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
   // The strip of the next tile is loaded at the top of each tile and split
   // at its end, so the products only read registers written by VALU
   // instructions and no wait on memory falls inside the tile.
-  X3Strip<NC, U> nxt;
+  X3Strip<NC, U, RM> nxt;
   x3_load(nxt, a.W1, t, a.N, K, rem, li, lk);
   bf16x8 w0[U][NC], w1[U][NC], w2[U][NC];
-  float wt[U][kX3RemMax];
+  float wt[U][RM > 0 ? RM : 1];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
 #pragma unroll
     for (int c = 0; c < NC; ++c)
       split3(nxt.c[u][2 * c], nxt.c[u][2 * c + 1], w0[u][c], w1[u][c], w2[u][c]);
 #pragma unroll
-    for (int s = 0; s < kX3RemMax; ++s) wt[u][s] = nxt.t[u][s];
+    for (int s = 0; s < RM; ++s) wt[u][s] = nxt.t[u][s];
   }
   for (; t < T; t += tstride) {
     const int64_t tn = t + tstride < T ? t + tstride : t;
@@ -391,10 +408,10 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
       // remainder operands of this sample tile, read before the chunks
-      float qt[kX3RemMax];
+      float qt[RM > 0 ? RM : 1];
       if (rem > 0) {
 #pragma unroll
-        for (int s = 0; s < kX3RemMax; ++s) qt[s] = qtail[(i * rem + (s < rem ? s : rem - 1)) * 64];
+        for (int s = 0; s < RM; ++s) qt[s] = qtail[(i * rem + (s < rem ? s : rem - 1)) * 64];
       }
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
@@ -413,7 +430,7 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
-      for (int s = 0; s < kX3RemMax; ++s) {
+      for (int s = 0; s < RM; ++s) {
         if (s < rem) {
 #pragma unroll
           for (int u = 0; u < U; ++u)
@@ -432,7 +449,7 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
       for (int c = 0; c < NC; ++c)
         split3(nxt.c[u][2 * c], nxt.c[u][2 * c + 1], w0[u][c], w1[u][c], w2[u][c]);
 #pragma unroll
-      for (int s = 0; s < kX3RemMax; ++s) wt[u][s] = nxt.t[u][s];
+      for (int s = 0; s < RM; ++s) wt[u][s] = nxt.t[u][s];
     }
   }
 }
@@ -971,7 +988,12 @@ template <int TQ, int NC>
 static hipError_t fwd_x3_go(const FwdLdsArgs& a, hipStream_t s) {
   constexpr int U = NC <= 3 ? 2 : 1;
   const int64_t T = (a.N + 16 * U - 1) / (16 * U);
-  return launch_persistent(k_fwd_x3<TQ, NC, U>, kLdsBlock, fwd_x3_bytes(a.Bp, a.K), T, s, a);
+  const size_t lds = fwd_x3_bytes(a.Bp, a.K);
+  switch ((a.K % 32) / 4) {
+    case 0: return launch_persistent(k_fwd_x3<TQ, NC, U, 0>, kLdsBlock, lds, T, s, a);
+    case 1: return launch_persistent(k_fwd_x3<TQ, NC, U, 1>, kLdsBlock, lds, T, s, a);
+    default: return launch_persistent(k_fwd_x3<TQ, NC, U, kX3RemMax>, kLdsBlock, lds, T, s, a);
+  }
 }
 
 template <int TQ>
