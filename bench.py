@@ -66,15 +66,47 @@ def kernel_work(name, B, F, N, M, O, precision="fp32"):
     return "hbm", 0.0, 0.0
 
 
-def roofline_bound(bound, nbytes, flops, precision="fp32"):
+LDS_BYTES = 160 * 1024        # per workgroup
+
+
+def padded_batch(B):
+    """Batch width of the LDS-resident kernels: 16, 32, 64, 128 or 256."""
+    return next((b for b in (16, 32, 64, 128, 256) if B <= b), None)
+
+
+def three_piece(name, B, F, O):
+    """True where the fp32 path runs the kernel's matrix products as six
+    bf16 products of three-piece operand splits (batches of 128 and 256
+    samples): the input-layer forward when its three LDS planes fit, the
+    fused backward for F4 = 52 or 100 and O = 2."""
+    bp, f4 = padded_batch(B), (F + 3) // 4 * 4
+    if bp not in (128, 256):
+        return False
+    if name == "gemm_fwd":
+        lds = 3 * bp * (f4 // 32) * 64 + bp * ((f4 % 32) // 4) * 16
+        return 32 <= f4 <= 140 and bp * f4 * 4 <= LDS_BYTES and lds <= LDS_BYTES
+    if name == "bwd_fused":
+        return O == 2 and f4 in (52, 100)
+    return False
+
+
+def mfma_peak(name, B, F, O, precision="fp32"):
+    """Matrix-core ceiling of one kernel in TFLOP/s of its own arithmetic:
+    the bf16 peak in the bf16 mode; in the fp32 path the fp32 peak, or a
+    sixth of the bf16 peak where each fp32 multiply-add is six bf16 ones."""
+    if precision == "bf16":
+        return PEAK_BF16_MFMA
+    return PEAK_BF16_MFMA / 6.0 if three_piece(name, B, F, O) else PEAK_FP32_MFMA
+
+
+def roofline_bound(bound, nbytes, flops, peak_tflops):
     """A matrix-core kernel is compute-bound only when its arithmetic
     intensity (algorithmic flops per algorithmic byte) is above the ridge
-    point of its dtype (peak flops / peak HBM bandwidth); below it the HBM
-    roofline bounds it."""
+    point of its matrix-core ceiling (peak flops / peak HBM bandwidth);
+    below it the HBM roofline bounds it."""
     if bound != "mfma" or not nbytes:
         return bound
-    peak = PEAK_BF16_MFMA if precision == "bf16" else PEAK_FP32_MFMA
-    ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+    ridge = peak_tflops * 1e12 / (PEAK_HBM_GBS * 1e9)
     return "mfma" if flops / nbytes >= ridge else "hbm"
 
 
@@ -241,10 +273,11 @@ def main(argv=None):
                          "tflops": flops / (avg * 1e-3) / 1e12 if flops else None}
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
     bound, nbytes, flops = kernel_work(dom, w.B, w.F, N, M, w.O, args.precision)
-    bound = roofline_bound(bound, nbytes, flops, args.precision)
+    mpeak = mfma_peak(dom, w.B, w.F, w.O, args.precision)
+    bound = roofline_bound(bound, nbytes, flops, mpeak)
     avg_s = kernels[dom]["avg_ms"] * 1e-3
     if bound == "mfma":
-        peak = PEAK_BF16_MFMA if args.precision == "bf16" else PEAK_FP32_MFMA
+        peak = mpeak
         achieved, unit = flops / avg_s / 1e12, "TFLOP/s"
     else:
         peak, achieved, unit = PEAK_HBM_GBS, nbytes / avg_s / 1e9, "GB/s"

@@ -250,14 +250,16 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds_ring(FwdLdsArgs a) {
 // ---------------------------------------------------------------------------
 // Forward for wide batches on the bf16 matrix cores at fp32 accuracy.
 //
-// Every fp32 operand a is split into three bf16 pieces with round-to-nearest,
-//   a = a0 + a1 + a2 + r,  |a1| <= 2^-9 |a|,  |a2| <= 2^-18 |a|,  |r| <= 2^-27 |a|,
-// and a product a b is taken as the six piece products of magnitude up to
-// 2^-18 |a b| (a0 b0, a0 b1, a1 b0, a0 b2, a1 b1, a2 b0), each exact in the
-// fp32 accumulator.  The three products left out and the residuals add up
-// to a few times 2^-27 |a b|, below the rounding of one fp32 product
-// (2^-24), so the result carries the error of an fp32 dot product, while
-// six v_mfma_f32_16x16x32_bf16 (32 k values each) stand in for the eight
+// Every fp32 operand a is split into three bf16 pieces, each the
+// round-to-nearest of what the previous ones leave:
+//   a = a0 + a1 + a2 exactly,  |a1| <= 2^-8 |a|,  |a2| <= 2^-16 |a|
+// (a has 24 significant bits, each piece takes 8; exact for normal a whose
+// last piece is not subnormal).  A product a b is taken as the six piece
+// products a0 b0, a0 b1, a1 b0, a0 b2, a1 b1, a2 b0, each exact in the fp32
+// accumulator; the three left out (a1 b2, a2 b1, a2 b2) are at most
+// 2^-23 |a b| together, two units of fp32 rounding and usually far less, so
+// the result carries the error of an fp32 dot product, while six
+// v_mfma_f32_16x16x32_bf16 (32 k values each) stand in for the eight
 // v_mfma_f32_16x16x4f32 of the same 32 k values at about a third of their
 // issue time.  The batch is split once per workgroup into three LDS planes
 // in MFMA-operand order (plane slot (i*NC + c)*64 + l holds the eight k
@@ -689,6 +691,224 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Fused backward with the dW1 product on the bf16 matrix cores at fp32
+// accuracy (the three-piece split of k_fwd_x3), for batches of 128 and 256
+// samples and O <= 4.  The batch goes through 32-sample chunks: lane
+// (li, lk) forms dZ of row li for the eight samples 32c + 8lk .. +7, splits
+// them into three bf16 pieces, and six v_mfma_f32_16x16x32_bf16 per column
+// block replace the eight fp32 steps of the same 32 samples.  The batch Xt
+// sits in LDS as three planes of pieces (slot (i*nc + c)*64 + l holds
+// Xt[16i + l%16][32c + 8(l/16) .. +7]); with TAIL the four columns past
+// 16 TQ have planes of their own (slot (c*4 + lk)*4 + q holds
+// Xt[16 TQ + q][32c + 8lk .. +7]) and take one more block of products in
+// which lanes li >= 4 supply zeros, so lane (li, 0) ends with those four
+// columns of row li.  The rest (gather of G, dW2, updates) is as in
+// k_bwd_lds.
+// ---------------------------------------------------------------------------
+
+template <int OM>
+__device__ __forceinline__ void bx3_load(f32x4 (&cz)[2], f32x4 (&cg)[2 * OM], const float* zrow,
+                                         const float* grow, int kofs) {
+  cz[0] = *(const f32x4*)(zrow + kofs);
+  cz[1] = *(const f32x4*)(zrow + kofs + 4);
+  // G[m][b .. b+7][0 .. OM-1] is 8*OM consecutive floats
+#pragma unroll
+  for (int v = 0; v < 2 * OM; ++v) cg[v] = *(const f32x4*)(grow + kofs * OM + 4 * v);
+}
+
+template <int TQ, int OM, int A, bool TAIL>
+__device__ __forceinline__ void bx3_chunk(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
+                                          const bf16x8* xq, int QS, int PS, const bf16x8* xt,
+                                          int TS,
+                                          bool tlane, const f32x4 (&cz)[2],
+                                          const f32x4 (&cg)[2 * OM], const float (&w2)[OM],
+                                          int arow) {
+  const float* g = (const float*)&cg[0];  // g[j*OM + o] = G[m][b+j][o]
+  float dz[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    float hp;
+    const float h = act_fwd_bwd(A >= 0 ? A : arow, cz[j >> 2][j & 3], &hp);
+    float dh = 0.f;
+#pragma unroll
+    for (int o = 0; o < OM; ++o) {
+      dh = fmaf(g[j * OM + o], w2[o], dh);
+      dw[o] = fmaf(g[j * OM + o], h, dw[o]);
+    }
+    dz[j] = dh * hp;
+    if (j == 3) __builtin_amdgcn_sched_barrier(0);  // four activations in flight at a time
+  }
+  bf16x8 d0, d1, d2;
+  split3(f32x4{dz[0], dz[1], dz[2], dz[3]}, f32x4{dz[4], dz[5], dz[6], dz[7]}, d0, d1, d2);
+  // the LDS operands of block i + 1 are read while block i multiplies
+  // (two blocks of pieces live at a time)
+  bf16x8 xn0 = xq[0], xn1 = xq[PS], xn2 = xq[2 * PS];
+#pragma unroll
+  for (int i = 0; i < TQ; ++i) {
+    const bf16x8 x0 = xn0, x1 = xn1, x2 = xn2;
+    if (i + 1 < TQ) {
+      xn0 = xq[(i + 1) * QS];
+      xn1 = xq[PS + (i + 1) * QS];
+      xn2 = xq[2 * PS + (i + 1) * QS];
+    } else if (TAIL) {
+      const bf16x8 zero = __builtin_bit_cast(bf16x8, f32x4{0.f, 0.f, 0.f, 0.f});
+      const bf16x8 t0 = xt[0], t1 = xt[TS], t2 = xt[2 * TS];
+      xn0 = tlane ? t0 : zero;
+      xn1 = tlane ? t1 : zero;
+      xn2 = tlane ? t2 : zero;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    acc[i] = mfma_x3(x0, x1, x2, d0, d1, d2, acc[i]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (TAIL) acc[TQ] = mfma_x3(xn0, xn1, xn2, d0, d1, d2, acc[TQ]);
+}
+
+template <int TQ, int OM, int RING, int A, bool TAIL>
+__device__ __forceinline__ void bx3_tile(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
+                                         const bf16x8* xq, int PS, const bf16x8* xt, int TS,
+                                         bool tlane, int nc, const float* zrow, const float* grow,
+                                         int lk, const float (&w2)[OM], int arow) {
+  f32x4 zb[RING][2], gb[RING][2 * OM];
+#pragma unroll
+  for (int r = 0; r < RING - 1; ++r)
+    bx3_load<OM>(zb[r], gb[r], zrow, grow, 32 * (r < nc ? r : nc - 1) + 8 * lk);
+  for (int c0 = 0; c0 < nc; c0 += RING) {
+#pragma unroll
+    for (int r = 0; r < RING; ++r) {
+      const int c = c0 + r;
+      const int cl = c + RING - 1 < nc ? c + RING - 1 : nc - 1;
+      bx3_load<OM>(zb[(r + RING - 1) % RING], gb[(r + RING - 1) % RING], zrow, grow,
+                   32 * cl + 8 * lk);
+      if (c < nc)
+        bx3_chunk<TQ, OM, A, TAIL>(acc, dw, xq + c * 64, nc * 64, PS, xt + c * 16, TS, tlane,
+                                   zb[r], gb[r], w2, arow);
+    }
+  }
+}
+
+template <int TQ, int OM, int RING, int NT, bool TAIL>
+__global__ __launch_bounds__(NT) void k_bwd_x3(BwdArgs a) {
+  constexpr int NW = NT / 64;
+  extern __shared__ float lds[];
+  const int Bp = a.Bp;
+  const int nc = Bp >> 5;
+  const bool grad = a.dW1 != nullptr;
+  const int PS = TQ * nc * 64;          // main slots per plane
+  const int TS = TAIL ? nc * 16 : 0;    // tail slots per plane
+  bf16x8* planes = (bf16x8*)lds;        // plane p: main at p*PS, tail at 3*PS + p*TS
+  for (int slot = threadIdx.x; slot < PS + TS; slot += NT) {
+    int row, col;
+    if (slot < PS) {
+      const int l = slot & 63, rest = slot >> 6;
+      const int i = rest / nc, c = rest - (rest / nc) * nc;
+      row = 16 * i + (l & 15);
+      col = 32 * c + 8 * (l >> 4);
+    } else {
+      const int s = slot - PS, q = s & 3, lk = (s >> 2) & 3, c = s >> 4;
+      row = 16 * TQ + q;
+      col = 32 * c + 8 * lk;
+    }
+    const float* src = a.Xt + (int64_t)row * Bp + col;
+    bf16x8 p0, p1, p2;
+    split3(*(const f32x4*)src, *(const f32x4*)(src + 4), p0, p1, p2);
+    const int base = slot < PS ? slot : 3 * PS + (slot - PS);
+    const int pstride = slot < PS ? PS : TS;
+    planes[base] = p0;
+    planes[base + pstride] = p1;
+    planes[base + 2 * pstride] = p2;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t T = (a.N + 15) >> 4;
+  const int64_t tstride = (int64_t)gridDim.x * NW;
+  const bf16x8* xq = planes + lane;                               // + (i*nc + c)*64
+  const bf16x8* xt = planes + 3 * PS + 4 * lk + (li & 3);         // + c*16
+  const bool tlane = li < 4;
+  for (int64_t t = (int64_t)blockIdx.x * NW + wave; t < T; t += tstride) {
+    const int64_t p = t * 16 + li;  // this lane's row; < Npad
+    const int64_t pc = p < a.N ? p : a.N - 1;
+    const int m = a.mid[pc];
+    const int arow = a.actn[pc];
+    const float lr = a.lrm ? a.lrm[m] : a.lr;
+    float w2[OM];
+#pragma unroll
+    for (int o = 0; o < OM; ++o) w2[o] = a.W2[(int64_t)o * a.ldw + pc];
+    const float* zrow = a.Zt + pc * Bp;
+    const float* grow = a.G + (int64_t)m * Bp * OM;
+    float* orow = a.W1 + p * a.F4;
+    f32x4 acc[TQ + 1];
+    float dw[OM];
+#pragma unroll
+    for (int i = 0; i <= TQ; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int o = 0; o < OM; ++o) dw[o] = 0.f;
+    const int a0 = __builtin_amdgcn_readfirstlane(arow);
+    const int auni = __all(arow == a0) ? a0 : -1;
+#define PMLP_BX3(AA) \
+  bx3_tile<TQ, OM, RING, AA, TAIL>(acc, dw, xq, PS, xt, TS, tlane, nc, zrow, grow, lk, w2, arow)
+    switch (auni) {
+      case 0: PMLP_BX3(0); break;
+      case 1: PMLP_BX3(1); break;
+      case 2: PMLP_BX3(2); break;
+      case 3: PMLP_BX3(3); break;
+      case 4: PMLP_BX3(4); break;
+      case 5: PMLP_BX3(5); break;
+      case 6: PMLP_BX3(6); break;
+      case 7: PMLP_BX3(7); break;
+      case 8: PMLP_BX3(8); break;
+      case 9: PMLP_BX3(9); break;
+      case 10: PMLP_BX3(10); break;
+      case 11: PMLP_BX3(11); break;
+      case 12: PMLP_BX3(12); break;
+      default: PMLP_BX3(-1); break;
+    }
+#undef PMLP_BX3
+#pragma unroll
+    for (int o = 0; o < OM; ++o) {
+      float v = dw[o];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      dw[o] = v;
+    }
+    if (grad) {
+      if (p < a.N) {
+        if (lk == 0)
+#pragma unroll
+          for (int o = 0; o < OM; ++o) a.dW2[(int64_t)o * a.N + p] = dw[o];
+        float* grow1 = a.dW1 + p * a.F;
+#pragma unroll
+        for (int i = 0; i <= TQ; ++i) {
+          if (i == TQ && (!TAIL || lk != 0)) continue;
+          const int q = 16 * i + 4 * lk;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (q + r < a.F) grow1[q + r] = acc[i][r];
+            else if (q + r == a.bcol && a.db1) a.db1[p] = acc[i][r];
+        }
+      }
+    } else {
+      // padded rows (p >= N) absorb the tail of the last tile; the W1
+      // strip is read here (other waves cover the latency) to keep the
+      // registers of the chunk loop free
+      f32x4 w1v[TQ + 1];
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) w1v[i] = *(const f32x4*)(orow + 16 * i + 4 * lk);
+      if (TAIL) w1v[TQ] = *(const f32x4*)(orow + 16 * TQ);
+      if (lk == 0)
+#pragma unroll
+        for (int o = 0; o < OM; ++o) a.W2[(int64_t)o * a.ldw + p] = w2[o] - lr * dw[o];
+#pragma unroll
+      for (int i = 0; i < TQ; ++i)
+        *(f32x4*)(orow + 16 * i + 4 * lk) = w1v[i] - lr * acc[i];
+      if (TAIL && lk == 0) *(f32x4*)(orow + 16 * TQ) = w1v[TQ] - lr * acc[TQ];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Fused backward for wider output layers (O = 5 .. 16).  The gather of G by
 // model id and its products with W2 and with the hidden activations are,
 // for the units of one model, two small dense contractions per 16-sample
@@ -1056,6 +1276,25 @@ static hipError_t bwd_mf_go(const BwdArgs& a, size_t lds, hipStream_t s) {
   return launch_persistent(k_bwd_mf<TQ, 2, NT>, NT, lds, T, s, a);
 }
 
+// Batches of 128 and 256 samples with F4 = 100 or 52 (six or three column
+// blocks and the four-column tail) and O = 2: the bf16 three-piece kernel.
+static size_t bwd_x3_bytes(int32_t Bp, int32_t F4) {
+  const int tq = F4 / 16, nc = Bp / 32;
+  return (size_t)3 * (tq * nc * 64 + (F4 % 16 ? nc * 16 : 0)) * 16;
+}
+
+static bool bwd_x3_shape(const BwdArgs& a) {
+  return (a.Bp == 128 || a.Bp == 256) && a.O == 2 && (a.F4 == 100 || a.F4 == 52) &&
+         bwd_x3_bytes(a.Bp, a.F4) <= (size_t)dev_info().lds_max;
+}
+
+static hipError_t bwd_x3_go(const BwdArgs& a, hipStream_t s) {
+  const int64_t T = (a.N + 15) / 16;
+  const size_t lds = bwd_x3_bytes(a.Bp, a.F4);
+  if (a.F4 == 100) return launch_persistent(k_bwd_x3<6, 2, 2, 512, true>, 512, lds, T, s, a);
+  return launch_persistent(k_bwd_x3<3, 2, 2, 512, true>, 512, lds, T, s, a);
+}
+
 template <int TQ, int OM, bool TAIL = false>
 static hipError_t bwd_lds_go(const BwdArgs& a, size_t lds, hipStream_t s) {
   // One 16-row tile per wave; 12 waves per workgroup (3 per SIMD) when the
@@ -1086,6 +1325,7 @@ hipError_t launch_bwd_lds(const BwdArgs& a0, hipStream_t s) {
   if (!bwd_lds_supported(a0.Bp, a0.F4, a0.O)) return hipErrorInvalidValue;
   const BwdArgs& a = a0;
   const size_t lds = bwd_lds_bytes(a.Bp, a.F4);
+  if (bwd_x3_shape(a)) return bwd_x3_go(a, s);
   if (a.O == 2) return bwd_lds_by_f<2>(a, lds, s);
   if (a.O == 4) return bwd_lds_by_f<4>(a, lds, s);
   // O = 5 .. 16: the gather of G and the dW2 product on the matrix cores
