@@ -77,6 +77,14 @@ CASES = {
                            F=20, O=2, B=256),
     "fwd_mixed_o4": dict(hs=[3, 1, 1, 17, 16, 15, 600, 2, 1, 33, 1000, 5, 48, 1, 16, 513],
                          F=36, O=4, B=120),
+    # the three-piece bf16 kernels: forward with no fp32 remainder (K = 64),
+    # with a run-time remainder (K = 40, 52), one or three 32-wide chunks;
+    # fused backward at F4 = 100 and 52 with zero-padded columns, for both
+    # 128- and 256-sample batches
+    "x3_f64_b256": dict(M=14, hmax=80, F=64, O=2, B=256),
+    "x3_f40_b200": dict(M=14, hmax=80, F=40, O=3, B=200),
+    "x3_f97_b100": dict(M=20, hmax=120, F=97, O=2, B=100),
+    "x3_f50_b256": dict(M=20, hmax=120, F=50, O=2, B=256),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
