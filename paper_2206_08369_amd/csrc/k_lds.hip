@@ -273,9 +273,6 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_lds_ring(FwdLdsArgs a) {
 
 static constexpr int kX3RemMax = 7;  // fp32 remainder steps: K mod 32 <= 28
 
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
 // two values at a time: one packed conversion per piece, the pieces read
 // back as floats from the low and high halves
 __device__ __forceinline__ uint32_t bf16_pair(f32x2 v) {

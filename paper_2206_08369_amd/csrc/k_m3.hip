@@ -139,10 +139,12 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
 //   out[b][o] = sum_n act(Z[n][b]) W2[o][n],
 // which v_mfma_f32_16x16x4f32 takes four units at a time: A[b][k] =
 // act(Z[n0+k][b]) for 16 samples, B[k][o] = W2[o][n0+k] for 16 outputs (rows
-// o >= O are zero).  Lane (li, lk) supplies sample li and output li of unit
-// n0 + lk, and ends with out[4lk + r][li].  Per four units a lane loads one
-// Z value per 16-sample block and one weight (against O weights per unit and
-// 4 O running sums per lane in the scalar kernel); units past the segment
+// o >= O are zero).  Lane (li, lk) supplies row li of each 16-sample block
+// and output li of unit n0 + lk, and ends with rows 4lk + r of the outputs;
+// with NBB blocks, row li of block i is sample NBB li + i of the wave's
+// range.  Per four units a lane loads NBB consecutive Z values (one vector
+// load) and one weight (against O weights per unit and 4 O running sums
+// per lane in the scalar kernel); units past the segment
 // end are zero in both operands, so a model's sums never see another
 // model's values.  One wave per (tile of whole segments, 16 NBB samples).
 // ---------------------------------------------------------------------------
@@ -153,8 +155,13 @@ __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* _
                                                bool orow_ok, int64_t nbeg, int64_t nend, int li,
                                                int lk) {
   // four-unit MFMA steps per pass, all loads first (loads in flight per lane:
-  // kUM (NBB + 1))
+  // 2 kUM).  Row li of block i is sample b0 + NBB li + i, so a lane's NBB
+  // values of one unit are one vector load and the 16 lanes of a unit read
+  // 64 NBB contiguous bytes of its row (a group past the batch reads the
+  // last NBB samples instead; their outputs are not stored).
   constexpr int kUM = NBB <= 2 ? 8 : 4;
+  int bl = b0 + NBB * li;
+  if (bl > Bp - NBB) bl = Bp - NBB;
   for (int64_t n0 = nbeg; n0 < nend; n0 += 4 * kUM) {
     float z[kUM][NBB];
     float w[kUM];
@@ -162,11 +169,17 @@ __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* _
     for (int u = 0; u < kUM; ++u) {
       int64_t n = n0 + 4 * u + lk;
       if (n > nend - 1) n = nend - 1;
+      const float* zp = Zt + n * Bp + bl;
+      if constexpr (NBB == 4) {
+        const f32x4 v = *(const f32x4*)zp;
 #pragma unroll
-      for (int i = 0; i < NBB; ++i) {
-        int b = b0 + 16 * i + li;
-        if (b > Bp - 1) b = Bp - 1;
-        z[u][i] = Zt[n * Bp + b];
+        for (int i = 0; i < 4; ++i) z[u][i] = v[i];
+      } else if constexpr (NBB == 2) {
+        const f32x2 v = *(const f32x2*)zp;
+        z[u][0] = v[0];
+        z[u][1] = v[1];
+      } else {
+        z[u][0] = zp[0];
       }
       w[u] = wrow[n];
     }
@@ -234,7 +247,7 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd_mf(
       for (int i = 0; i < NBB; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int b = b0 + 16 * i + 4 * lk + r;
+          const int b = b0 + NBB * (4 * lk + r) + i;
           if (b >= B) continue;
           const float v = acc[i][r] + bias;
           if (t.atomic) unsafeAtomicAdd(dst + (int64_t)b * sb, v);
