@@ -85,6 +85,7 @@ CASES = {
     "x3_f40_b200": dict(M=14, hmax=80, F=40, O=3, B=200),
     "x3_f97_b100": dict(M=20, hmax=120, F=97, O=2, B=100),
     "x3_f50_b256": dict(M=20, hmax=120, F=50, O=2, B=256),
+    "x3_tiny": dict(hs=[1, 2], F=97, O=2, B=129),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
