@@ -30,7 +30,9 @@ int fail(int code, const std::string& msg) {
       return fail(PMLP_EDEVICE, std::string(#expr) + " failed: " + hipGetErrorString(e_)); \
   } while (0)
 
-constexpr int64_t kTile3 = 512;      // M3 forward tile width (hidden units)
+constexpr int64_t kTile3 = 512;      // M3 forward tile width, largest (hidden units)
+constexpr int64_t kTile3Min = 32;    // smallest
+constexpr int64_t kTile3Count = 2048;  // tiles wanted to fill the chip
 constexpr int32_t kMaxBatch = 1 << 20;
 constexpr int32_t kMaxO = 16;
 
@@ -446,18 +448,27 @@ int step(pmlp* h, const float* X, const void* y, int32_t B, float lr, const floa
   return PMLP_OK;
 }
 
-// Tiles of the M3 forward: runs of whole segments up to kTile3 units wide;
+// Tiles of the M3 forward: runs of whole segments up to `cap` units wide;
 // a wider segment becomes two halves added with atomics onto zeroed logits.
 // Two additions onto zero give the same sum in either order, so the
-// forward is deterministic for every segment width.
-void build_tiles(const std::vector<int32_t>& hs, std::vector<Tile3>& tiles, bool& has_split) {
+// forward is deterministic for every segment width.  The cap is the power
+// of two in [kTile3Min, kTile3] nearest below N / kTile3Count, so that a
+// small pack still gives the M3 forward a few thousand waves.
+int64_t tile_cap(int64_t N) {
+  int64_t cap = kTile3;
+  while (cap > kTile3Min && cap * kTile3Count > N) cap >>= 1;
+  return cap;
+}
+
+void build_tiles(const std::vector<int32_t>& hs, int64_t cap, std::vector<Tile3>& tiles,
+                 bool& has_split) {
   tiles.clear();
   has_split = false;
   Tile3 cur{0, 0, 0, 0, 0};
   int64_t n = 0;
   for (size_t m = 0; m < hs.size(); ++m) {
     const int64_t w = hs[m];
-    if (w > kTile3) {
+    if (w > cap) {
       if (cur.len > 0) tiles.push_back(cur);
       cur.len = 0;
       const int64_t half = (w + 1) / 2;
@@ -465,7 +476,7 @@ void build_tiles(const std::vector<int32_t>& hs, std::vector<Tile3>& tiles, bool
       tiles.push_back(Tile3{n + half, (int32_t)(w - half), (int32_t)m, 1, 0});
       has_split = true;
     } else {
-      if (cur.len > 0 && cur.len + w > kTile3) {
+      if (cur.len > 0 && cur.len + w > cap) {
         tiles.push_back(cur);
         cur.len = 0;
       }
@@ -533,7 +544,7 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
       actn[n] = act_ids[m];
     }
   std::vector<Tile3> tiles;
-  build_tiles(h->hs, tiles, h->has_split);
+  build_tiles(h->hs, tile_cap(N), tiles, h->has_split);
   h->ntiles = (int32_t)tiles.size();
   // the M3 forward launches its waves widest tile first (ties in plan order),
   // so the dispatcher schedules the longest work first

@@ -243,9 +243,12 @@ def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name, path):
 # --------------------------------------------------------------------------
 
 # (F, O, B): the scalar M3 kernels (O <= 4) and the matrix-core ones (O > 4)
-# with narrow and wide batches; "nan" makes model j diverge (its output
-# weights NaN), which must not reach the models sharing its tiles either.
-@pytest.mark.parametrize("F,O,B", [(9, 3, 40), (32, 10, 32), (20, 12, 70)])
+# with narrow and wide batches, and the three-piece bf16 kernels (F4 = 100
+# and 52 with 256- and 128-sample batches); "nan" makes model j diverge (its
+# output weights NaN), which must not reach the models sharing its tiles
+# either.
+@pytest.mark.parametrize("F,O,B", [(9, 3, 40), (32, 10, 32), (20, 12, 70), (100, 2, 200),
+                                   (50, 2, 100)])
 @pytest.mark.parametrize("kind", ["finite", "nan"])
 def test_perturbing_one_model_leaves_the_others_bitwise(pm, torch, F, O, B, kind):
     rng = np.random.default_rng(5)
