@@ -344,7 +344,7 @@ def test_one_epoch(pm, orc, torch, wname, path):
 # models are independent).
 # --------------------------------------------------------------------------
 
-@pytest.mark.parametrize("wname", ["w10k_f100", "w10k_f32_o10", "w10k_f1000"])
+@pytest.mark.parametrize("wname", ["w10k_f100", "w10k_f32_o10", "w10k_f1000", "paper_10k"])
 def test_full_size_step_on_sampled_models(pm, orc, torch, wname):
     w = wl.WORKLOADS[wname]
     hs, acts = w.model_grid()
