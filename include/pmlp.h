@@ -129,7 +129,11 @@ int pmlp_set_stream(pmlp_t h, void* stream);
 
 /* Select the arithmetic of the two input-layer products (Section 3 step 1,
  * Z = X W1^T, and its gradient dW1 = dZ^T X) for all later calls:
- *   PMLP_FP32 (default): fp32 operands, fp32 accumulation.
+ *   PMLP_FP32 (default): fp32 operands, fp32 accumulation.  For batches
+ *     of 65 to 256 samples the products may run on the bf16 matrix cores
+ *     with every operand split exactly into three bf16 pieces and six piece
+ *     products accumulated in fp32; what that leaves out is at most 2^-23
+ *     of each product, the error of fp32 arithmetic (no operand is rounded).
  *   PMLP_BF16_GEMM: X, W1 and dZ are rounded to bf16 (nearest even) as
  *     the products read them and the products accumulate in fp32; the
  *     weights, Z, the activations, logits, loss, gradients of W2 and the
