@@ -698,7 +698,7 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
 // Xt[16i + l%16][32c + 8(l/16) .. +7]); with TAIL the four columns past
 // 16 TQ have planes of their own (slot (c*4 + lk)*4 + q holds
 // Xt[16 TQ + q][32c + 8lk .. +7]) and take one more block of products in
-// which lanes li >= 4 supply zeros, so lane (li, 0) ends with those four
+// which lanes li >= 4 read a zero slot, so lane (li, 0) ends with those four
 // columns of row li.  The rest (gather of G, dW2, updates) is as in
 // k_bwd_lds.
 // ---------------------------------------------------------------------------
@@ -717,7 +717,7 @@ template <int TQ, int OM, int A, bool TAIL>
 __device__ __forceinline__ void bx3_chunk(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
                                           const bf16x8* xq, int QS, int PS, const bf16x8* xt,
                                           int TS,
-                                          bool tlane, const f32x4 (&cz)[2],
+                                          const f32x4 (&cz)[2],
                                           const f32x4 (&cg)[2 * OM], const float (&w2)[OM],
                                           int arow) {
   const float* g = (const float*)&cg[0];  // g[j*OM + o] = G[m][b+j][o]
@@ -748,11 +748,9 @@ __device__ __forceinline__ void bx3_chunk(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
       xn1 = xq[PS + (i + 1) * QS];
       xn2 = xq[2 * PS + (i + 1) * QS];
     } else if (TAIL) {
-      const bf16x8 zero = __builtin_bit_cast(bf16x8, f32x4{0.f, 0.f, 0.f, 0.f});
-      const bf16x8 t0 = xt[0], t1 = xt[TS], t2 = xt[2 * TS];
-      xn0 = tlane ? t0 : zero;
-      xn1 = tlane ? t1 : zero;
-      xn2 = tlane ? t2 : zero;
+      xn0 = xt[0];
+      xn1 = xt[TS];
+      xn2 = xt[2 * TS];
     }
     __builtin_amdgcn_sched_barrier(0);
     acc[i] = mfma_x3(x0, x1, x2, d0, d1, d2, acc[i]);
@@ -764,7 +762,7 @@ __device__ __forceinline__ void bx3_chunk(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
 template <int TQ, int OM, int RING, int A, bool TAIL>
 __device__ __forceinline__ void bx3_tile(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
                                          const bf16x8* xq, int PS, const bf16x8* xt, int TS,
-                                         bool tlane, int nc, const float* zrow, const float* grow,
+                                         int tcs, int nc, const float* zrow, const float* grow,
                                          int lk, const float (&w2)[OM], int arow) {
   f32x4 zb[RING][2], gb[RING][2 * OM];
 #pragma unroll
@@ -778,8 +776,8 @@ __device__ __forceinline__ void bx3_tile(f32x4 (&acc)[TQ + 1], float (&dw)[OM],
       bx3_load<OM>(zb[(r + RING - 1) % RING], gb[(r + RING - 1) % RING], zrow, grow,
                    32 * cl + 8 * lk);
       if (c < nc)
-        bx3_chunk<TQ, OM, A, TAIL>(acc, dw, xq + c * 64, nc * 64, PS, xt + c * 16, TS, tlane,
-                                   zb[r], gb[r], w2, arow);
+        bx3_chunk<TQ, OM, A, TAIL>(acc, dw, xq + c * 64, nc * 64, PS, xt + c * tcs, TS, zb[r],
+                                   gb[r], w2, arow);
     }
   }
 }
@@ -815,6 +813,8 @@ __global__ __launch_bounds__(NT) void k_bwd_x3(BwdArgs a) {
     planes[base + pstride] = p1;
     planes[base + 2 * pstride] = p2;
   }
+  if (TAIL && threadIdx.x == 0)
+    planes[3 * PS + 3 * TS] = __builtin_bit_cast(bf16x8, f32x4{0.f, 0.f, 0.f, 0.f});
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -822,8 +822,11 @@ __global__ __launch_bounds__(NT) void k_bwd_x3(BwdArgs a) {
   const int64_t T = (a.N + 15) >> 4;
   const int64_t tstride = (int64_t)gridDim.x * NW;
   const bf16x8* xq = planes + lane;                               // + (i*nc + c)*64
-  const bf16x8* xt = planes + 3 * PS + 4 * lk + (li & 3);         // + c*16
+  // tail operands: lanes li < 4 read their slots (stride 16 per chunk, TS
+  // per plane), the others one zero slot past the tail planes (stride 0)
   const bool tlane = li < 4;
+  const bf16x8* xt = planes + (tlane ? 3 * PS + 4 * lk + li : 3 * PS + 3 * TS);
+  const int tcs = tlane ? 16 : 0, tps = tlane ? TS : 0;
   for (int64_t t = (int64_t)blockIdx.x * NW + wave; t < T; t += tstride) {
     const int64_t p = t * 16 + li;  // this lane's row; < Npad
     const int64_t pc = p < a.N ? p : a.N - 1;
@@ -845,7 +848,7 @@ __global__ __launch_bounds__(NT) void k_bwd_x3(BwdArgs a) {
     const int a0 = __builtin_amdgcn_readfirstlane(arow);
     const int auni = __all(arow == a0) ? a0 : -1;
 #define PMLP_BX3(AA) \
-  bx3_tile<TQ, OM, RING, AA, TAIL>(acc, dw, xq, PS, xt, TS, tlane, nc, zrow, grow, lk, w2, arow)
+  bx3_tile<TQ, OM, RING, AA, TAIL>(acc, dw, xq, PS, xt, tps, tcs, nc, zrow, grow, lk, w2, arow)
     switch (auni) {
       case 0: PMLP_BX3(0); break;
       case 1: PMLP_BX3(1); break;
@@ -1277,7 +1280,7 @@ static hipError_t bwd_mf_go(const BwdArgs& a, size_t lds, hipStream_t s) {
 // blocks and the four-column tail) and O = 2: the bf16 three-piece kernel.
 static size_t bwd_x3_bytes(int32_t Bp, int32_t F4) {
   const int tq = F4 / 16, nc = Bp / 32;
-  return (size_t)3 * (tq * nc * 64 + (F4 % 16 ? nc * 16 : 0)) * 16;
+  return (size_t)3 * (tq * nc * 64 + (F4 % 16 ? nc * 16 : 0)) * 16 + (F4 % 16 ? 16 : 0);
 }
 
 static bool bwd_x3_shape(const BwdArgs& a) {
