@@ -86,6 +86,9 @@ CASES = {
     "x3_f97_b100": dict(M=20, hmax=120, F=97, O=2, B=100),
     "x3_f50_b256": dict(M=20, hmax=120, F=50, O=2, B=256),
     "x3_tiny": dict(hs=[1, 2], F=97, O=2, B=129),
+    # widest forward shape of the three-piece kernel: four chunks, one unit
+    # tile per wave, three run-time remainder steps
+    "x3_f140_b128": dict(M=12, hmax=64, F=140, O=2, B=128),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
