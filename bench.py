@@ -283,7 +283,12 @@ def main(argv=None):
         peak, achieved, unit = PEAK_HBM_GBS, nbytes / avg_s / 1e9, "GB/s"
     roofline = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                 "frac": achieved / peak, "traffic": load_traffic(dom, w.name, args.precision),
-                "kernel": dom}
+                "kernel": dom,
+                # the kernel's matrix-core ceiling in TFLOP/s of fp32 work, which sets
+                # the ridge that chose `bound` (a sixth of the bf16 peak where the
+                # products run as six bf16 products of three-piece splits)
+                "mfma_ceiling": mpeak,
+                "three_piece": args.precision == "fp32" and three_piece(dom, w.B, w.F, w.O)}
 
     cpu = None
     if args.cpu_seconds > 0:
