@@ -12,6 +12,11 @@ this file; the wrappers below only marshal numpy arrays through ctypes.
 cross-entropy with the mean squared error against real targets y [B, O]
 (regression); the default `head="ce"` takes integer labels y [B].
 
+`mask` (forward, gradients, train, hidden, value_ties, dataset_loss) gives
+per-model input feature masks [M, F]: model m is trained on its own subset
+of the input columns (feature selection); its packed W1 block keeps zeros in
+the other columns.
+
 `rounding="bf16"` (forward, gradients, train, hidden, dataset_loss) emulates
 the bf16-in / fp32-accumulate variant of the two input-layer products: X,
 W1 and dZ go to fp32 and then to the nearest bfloat16 before they are
@@ -83,6 +88,12 @@ def _load():
         lib.orc_value_ties.argtypes = [i32, i32, P, P, P, P, P, i32, dbl, P]
         lib.orc_set_head.restype = C.c_int
         lib.orc_set_head.argtypes = [C.c_int]
+        lib.orc_set_branch.restype = C.c_int
+        lib.orc_set_branch.argtypes = [P, i64, dbl]
+        lib.orc_branch_conflicts.restype = i64
+        lib.orc_branch_conflicts.argtypes = []
+        lib.orc_set_feature_mask.restype = C.c_int
+        lib.orc_set_feature_mask.argtypes = [P]
         lib.orc_dataset_loss.restype = C.c_int
         lib.orc_dataset_loss.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i64,
                                          i32, P, C.c_int]
@@ -142,6 +153,54 @@ def _head(head: str):
         lib.orc_set_head(0)
 
 
+_last_conflicts = 0
+
+
+@contextlib.contextmanager
+def _branch(br, band: float, N: int):
+    """Branch choices at Hardshrink's jumps for the duration of one call
+    (see orc_set_branch in pmlp_oracle.c): br is [rows, N] with nonzero
+    where the checked result let the value pass; None gives none."""
+    global _last_conflicts
+    lib = _load()
+    a = None
+    if br is not None:
+        a = np.ascontiguousarray(np.asarray(br) != 0, dtype=np.uint8)
+        if a.ndim != 2 or a.shape[1] != N:
+            raise ValueError("branch choices must be [rows, %d]" % N)
+    _check(lib.orc_set_branch(_p(a), 0 if a is None else N, float(band)), "set_branch")
+    try:
+        yield
+    finally:
+        _last_conflicts = int(lib.orc_branch_conflicts())
+        lib.orc_set_branch(None, 0, 0.0)
+
+
+@contextlib.contextmanager
+def _fmask(mask, M: int, F: int):
+    """Per-model input feature masks [M, F] for the duration of one call
+    (nonzero: model m sees feature f; see orc_set_feature_mask in
+    pmlp_oracle.c); None: every model sees every feature."""
+    lib = _load()
+    a = None
+    if mask is not None:
+        a = np.ascontiguousarray(np.asarray(mask) != 0, dtype=np.uint8)
+        if a.shape != (M, F):
+            raise ValueError("feature masks must be [%d, %d]" % (M, F))
+    lib.orc_set_feature_mask(_p(a))
+    try:
+        yield
+    finally:
+        lib.orc_set_feature_mask(None)
+
+
+def branch_conflicts() -> int:
+    """Number of (sample, unit) pairs in the last call given branch choices
+    where the given side differs from the oracle's own outside the band
+    (a choice that is not among the correct results)."""
+    return _last_conflicts
+
+
 def _labels(y, head: str, O: int, S: int) -> np.ndarray:
     """int32 labels [S] (ce) or float32 targets [S, O] (mse)."""
     if head == "mse":
@@ -197,15 +256,17 @@ def init_biases(F: int, O: int, hidden_sizes, seed: int) -> Tuple[np.ndarray, np
 
 
 def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
-            rounding: str = "exact", b1=None, b2=None) -> np.ndarray:
-    """logits [B, M, O] in fp64; optional biases b1 [N] and b2 [M, O]."""
+            rounding: str = "exact", b1=None, b2=None, branch=None,
+            band: float = 1e-6, mask=None) -> np.ndarray:
+    """logits [B, M, O] in fp64; optional biases b1 [N] and b2 [M, O];
+    optional branch choices [B, N] at Hardshrink's jumps (see _branch)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     B, F = Xf.shape
     O, N = W2d.shape
     c1, c2 = _bias(b1, N, "b1"), _bias(b2, len(hs) * O, "b2")
     out = np.empty((B, len(hs), O), np.float64)
-    with _rounding(rounding):
+    with _rounding(rounding), _branch(branch, band, N), _fmask(mask, len(hs), F):
         _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                    _p(c2), _p(Xf), B, _p(out), nthreads), "forward")
     return out
@@ -214,7 +275,7 @@ def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
 def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
               with_allowance: bool = True, nthreads: int = 0, rounding: str = "exact",
               tie_rel: float = 1e-5, cond_rel: float = 2.4e-7, b1=None, b2=None,
-              head: str = "ce"):
+              head: str = "ce", branch=None, band: float = 1e-6, mask=None):
     """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
 
     allow_dW1 bounds what a correct fp32 evaluation may differ by where a
@@ -243,7 +304,7 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     db1 = np.empty(N, np.float64) if c1 is not None else None
     db2 = np.empty((M, O), np.float64) if c2 is not None else None
     allow_b = np.empty(N, np.float64) if (with_allowance and c1 is not None) else None
-    with _rounding(rounding), _head(head):
+    with _rounding(rounding), _head(head), _branch(branch, band, N), _fmask(mask, M, F):
         _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                      _p(c2), _p(Xf), _p(yi), B, _p(dW1), _p(dW2), _p(db1),
                                      _p(db2), _p(loss), _p(allow), _p(allow_b),
@@ -258,7 +319,7 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
 def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
           lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0,
           rounding: str = "exact", return_ties: bool = False, tie_rel: float = 1e-6,
-          b1=None, b2=None, head: str = "ce"):
+          b1=None, b2=None, head: str = "ce", branch=None, band: float = 1e-6, mask=None):
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
@@ -292,7 +353,7 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
         if lr_m.size != len(hs):
             raise ValueError("per-model lr needs one rate per model")
         lr = 0.0
-    with _rounding(rounding), _head(head):
+    with _rounding(rounding), _head(head), _branch(branch, band, N), _fmask(mask, len(hs), F):
         _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                  _p(c2), _p(Xf), _p(yi), len(batches), _p(off), _p(ln),
                                  float(lr), _p(lr_m), _p(W1o), _p(W2o), _p(b1o), _p(b2o),
@@ -306,23 +367,23 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
     return tuple(out)
 
 
-def hidden(hidden_sizes, act_ids, W1, X,
-           rounding: str = "exact", b1=None) -> Tuple[np.ndarray, np.ndarray]:
-    """Z = X W1^T and H = act(Z), both [B, N] fp64."""
+def hidden(hidden_sizes, act_ids, W1, X, rounding: str = "exact", b1=None,
+           branch=None, band: float = 1e-6, mask=None) -> Tuple[np.ndarray, np.ndarray]:
+    """Z = X W1^T and H = act(Z), both [B, N] fp64 (branch: see _branch)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
     B, F = Xf.shape
     N = int(hs.sum())
     Z = np.empty((B, N), np.float64)
     H = np.empty((B, N), np.float64)
-    with _rounding(rounding):
+    with _rounding(rounding), _branch(branch, band, N), _fmask(mask, len(hs), F):
         _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(_bias(b1, N, "b1")),
                                   _p(Xf), B, _p(Z), _p(H)), "hidden")
     return Z, H
 
 
 def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
-               rounding: str = "exact", b1=None) -> np.ndarray:
+               rounding: str = "exact", b1=None, mask=None) -> np.ndarray:
     """Per-model count of (sample, unit) pairs whose Z sits within rounding
     of a jump of its activation (Hardshrink at +-0.5); models with a nonzero
     count have several correct fp32 results and are left out of comparisons."""
@@ -330,7 +391,7 @@ def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
     W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
     B, F = Xf.shape
     counts = np.empty(len(hs), np.int32)
-    with _rounding(rounding):
+    with _rounding(rounding), _fmask(mask, len(hs), F):
         c1 = _bias(b1, W1d.shape[0], "b1")
         _check(_load().orc_value_ties(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(c1), _p(Xf), B,
                                       float(rel), _p(counts)), "value_ties")
@@ -339,14 +400,14 @@ def value_ties(hidden_sizes, act_ids, W1, X, rel: float = 1e-6,
 
 def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,
                  nthreads: int = 0, rounding: str = "exact", b1=None,
-                 b2=None, head: str = "ce") -> np.ndarray:
+                 b2=None, head: str = "ce", mask=None) -> np.ndarray:
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, W2d, Xf = _c(W1, np.float64), _c(W2, np.float64), _c(X, np.float32)
     S, F = Xf.shape
     O = W2d.shape[0]
     yi = _labels(y, head, O, S)
     loss = np.empty(len(hs), np.float64)
-    with _rounding(rounding), _head(head):
+    with _rounding(rounding), _head(head), _fmask(mask, len(hs), F):
         c1 = _bias(b1, W2d.shape[1], "b1")
         c2 = _bias(b2, len(hs) * O, "b2")
         _check(_load().orc_dataset_loss(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d),
@@ -354,3 +415,110 @@ def dataset_loss(hidden_sizes, act_ids, W1, W2, X, y, chunk: int = 1024,
                                         nthreads),
                "dataset_loss")
     return loss
+
+
+# --------------------------------------------------------------------------
+# Two hidden layers per model (Section 7, Figure 3).  h1 [M], h2 [M] hidden
+# sizes, one activation per model for both layers; packed W1 [N1, F],
+# W12 [K] (model m's [h2_m, h1_m] block row-major at offset K_m), W2 [O, N2].
+# --------------------------------------------------------------------------
+
+def _deep_lib():
+    lib = _load()
+    if not getattr(lib, "_deep_ready", False):
+        P = C.c_void_p
+        i32, u64, dbl = C.c_int32, C.c_uint64, C.c_double
+        lib.orc_deep_init.restype = C.c_int
+        lib.orc_deep_init.argtypes = [i32, i32, i32, P, P, u64, P, P, P]
+        lib.orc_deep_forward_all.restype = C.c_int
+        lib.orc_deep_forward_all.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, i32, P, C.c_int]
+        lib.orc_deep_gradients.restype = C.c_int
+        lib.orc_deep_gradients.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32, P, P, P,
+                                           P, P, P, P, dbl, dbl, dbl, C.c_int]
+        lib.orc_deep_train.restype = C.c_int
+        lib.orc_deep_train.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32, P, P, dbl,
+                                       P, P, P, P, P, i32, P, dbl, C.c_int]
+        lib._deep_ready = True
+    return lib
+
+
+def deep_sizes(h1, h2):
+    """(N1, N2, K): units of the two hidden layers and entries of all W12 blocks."""
+    a, b = np.asarray(h1, np.int64), np.asarray(h2, np.int64)
+    return int(a.sum()), int(b.sum()), int((a * b).sum())
+
+
+def deep_init(F: int, O: int, h1, h2, seed: int):
+    """W1 [N1, F], W12 [K], W2 [O, N2] (fp32) from the counter-based stream:
+    tags 1 (W1, fan_in F), 5 (W12, idx K_m + i h1_m + j, fan_in h1_m) and
+    2 (W2, idx o N2 + n, fan_in h2_m)."""
+    a, b = _c(h1, np.int32), _c(h2, np.int32)
+    N1, N2, K = deep_sizes(a, b)
+    W1 = np.empty((N1, F), np.float32)
+    W12 = np.empty(K, np.float32)
+    W2 = np.empty((O, N2), np.float32)
+    _check(_deep_lib().orc_deep_init(F, O, len(a), _p(a), _p(b), C.c_uint64(seed), _p(W1),
+                                     _p(W12), _p(W2)), "deep_init")
+    return W1, W12, W2
+
+
+def deep_forward(h1, h2, act_ids, W1, W12, W2, X, nthreads: int = 0) -> np.ndarray:
+    """logits [B, M, O] in fp64."""
+    a, b, ac = _c(h1, np.int32), _c(h2, np.int32), _c(act_ids, np.int32)
+    W1d, W12d, W2d, Xf = _c(W1, np.float64), _c(W12, np.float64), _c(W2, np.float64), _c(X, np.float32)
+    B, F = Xf.shape
+    O = W2d.shape[0]
+    out = np.empty((B, len(a), O), np.float64)
+    _check(_deep_lib().orc_deep_forward_all(F, O, len(a), _p(a), _p(b), _p(ac), _p(W1d), _p(W12d),
+                                            _p(W2d), _p(Xf), B, _p(out), nthreads), "deep_forward")
+    return out
+
+
+def deep_gradients(h1, h2, act_ids, W1, W12, W2, X, y, kink_rel: float = 1e-6,
+                   cond_rel: float = 2.4e-7, tie_rel: float = 1e-6, nthreads: int = 0):
+    """(dW1 [N1,F], dW12 [K], dW2 [O,N2], loss [M], allow_dW1, allow_dW12,
+    ties [M]) in fp64: gradients of sum_m L_m, the allowances of what a
+    correct fp32 evaluation may differ by (kink ties of either layer and the
+    cancellation of dH2 = G W2), and the count of Hardshrink value ties."""
+    a, b, ac = _c(h1, np.int32), _c(h2, np.int32), _c(act_ids, np.int32)
+    W1d, W12d, W2d, Xf = _c(W1, np.float64), _c(W12, np.float64), _c(W2, np.float64), _c(X, np.float32)
+    B, F = Xf.shape
+    O = W2d.shape[0]
+    N1, N2, K = deep_sizes(a, b)
+    yi = _c(y, np.int32)
+    dW1, dW12, dW2 = np.empty((N1, F)), np.empty(K), np.empty((O, N2))
+    loss = np.empty(len(a))
+    al1, al12 = np.empty((N1, F)), np.empty(K)
+    ties = np.empty(len(a), np.int32)
+    _check(_deep_lib().orc_deep_gradients(F, O, len(a), _p(a), _p(b), _p(ac), _p(W1d), _p(W12d),
+                                          _p(W2d), _p(Xf), _p(yi), B, _p(dW1), _p(dW12), _p(dW2),
+                                          _p(loss), _p(al1), _p(al12), _p(ties), float(kink_rel),
+                                          float(cond_rel), float(tie_rel), nthreads),
+           "deep_gradients")
+    return dW1, dW12, dW2, loss, al1, al12, ties
+
+
+def deep_train(h1, h2, act_ids, W1, W12, W2, X, y, batches, lr: float, models=None,
+               tie_rel: float = 1e-6, nthreads: int = 0):
+    """SGD over the (offset, length) batches: (W1', W12', W2', loss_last [M],
+    ties [M]) in fp64; with a model subset the other entries are NaN."""
+    a, b, ac = _c(h1, np.int32), _c(h2, np.int32), _c(act_ids, np.int32)
+    W1d, W12d, W2d, Xf = _c(W1, np.float64), _c(W12, np.float64), _c(W2, np.float64), _c(X, np.float32)
+    F = Xf.shape[1]
+    O = W2d.shape[0]
+    N1, N2, K = deep_sizes(a, b)
+    yi = _c(y, np.int32)
+    off = np.asarray([t[0] for t in batches], np.int64)
+    ln = np.asarray([t[1] for t in batches], np.int32)
+    if len(batches) and (off.min() < 0 or (off + ln).max() > Xf.shape[0]):
+        raise ValueError("batch outside the sample arrays")
+    W1o, W12o, W2o = np.full((N1, F), np.nan), np.full(K, np.nan), np.full((O, N2), np.nan)
+    loss = np.full(len(a), np.nan)
+    ties = np.zeros(len(a), np.int32)
+    sel = None if models is None else _c(models, np.int32)
+    _check(_deep_lib().orc_deep_train(F, O, len(a), _p(a), _p(b), _p(ac), _p(W1d), _p(W12d),
+                                      _p(W2d), _p(Xf), _p(yi), len(batches), _p(off), _p(ln),
+                                      float(lr), _p(W1o), _p(W12o), _p(W2o), _p(loss), _p(sel),
+                                      0 if sel is None else len(sel), _p(ties), float(tie_rel),
+                                      nthreads), "deep_train")
+    return W1o, W12o, W2o, loss, ties

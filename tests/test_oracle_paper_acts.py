@@ -130,3 +130,74 @@ def test_training_counts_ties_at_each_step(orc):
     W1a, W2a, _ = orc.train(hs, acts, W1, W2, X, y, batches[:1], 0.1)
     want = want + orc.value_ties(hs, acts, W1a, X[6:])
     assert list(ties) == list(want) and ties[0] >= 1 and ties[1] == 0
+
+
+# --------------------------------------------------------------------------
+# Branch choices at Hardshrink's jumps.  At a value tie several results are
+# correct; a checked result names the side it took and the oracle follows it
+# inside the tie band only.  Pinned against other activations and against
+# PyTorch autograd, not against the oracle's own formulas.
+# --------------------------------------------------------------------------
+
+def _tied_single_unit():
+    """One unit, w = 0.5, inputs 1, 2, 3, -1: Z = 0.5 (a tie), 1, 1.5, -0.5 (a tie)."""
+    X = np.array([[1.0], [2.0], [3.0], [-1.0]], np.float32)
+    W1 = np.array([[0.5]])
+    W2 = np.array([[0.8], [-0.3]])
+    y = np.array([0, 1, 1, 0], np.int32)
+    return np.array([1], np.int32), X, W1, W2, y
+
+
+def test_forced_pass_at_every_tie_equals_the_identity_activation(orc):
+    hs, X, W1, W2, y = _tied_single_unit()
+    br = np.ones((4, 1), np.uint8)                       # every sample passes
+    g = orc.gradients(hs, [HARDSHRINK], W1, W2, X, y, branch=br)
+    assert orc.branch_conflicts() == 0
+    ident = orc.gradients(hs, [0], W1, W2, X, y)         # identity everywhere
+    for a, b in zip(g[:3], ident[:3]):
+        np.testing.assert_array_equal(a, b)
+    _, H = orc.hidden(hs, [HARDSHRINK], W1, X, branch=br)
+    np.testing.assert_array_equal(H[:, 0], [0.5, 1.0, 1.5, -0.5])
+
+
+def test_forced_zero_at_the_ties_equals_the_unforced_oracle(orc):
+    hs, X, W1, W2, y = _tied_single_unit()
+    br = np.array([[0], [1], [1], [0]], np.uint8)        # the oracle's own sides
+    a = orc.gradients(hs, [HARDSHRINK], W1, W2, X, y, branch=br)
+    assert orc.branch_conflicts() == 0
+    b = orc.gradients(hs, [HARDSHRINK], W1, W2, X, y)
+    for u, v in zip(a[:3], b[:3]):
+        np.testing.assert_array_equal(u, v)
+
+
+def test_forced_branches_match_torch_autograd(orc):
+    """Sample 0 passes, sample 3 is zeroed: the same as PyTorch's Hardshrink
+    with threshold 0.499 on sample 0 and 0.501 on sample 3 (a threshold
+    moved across the tie, everything else unchanged)."""
+    hs, X, W1, W2, y = _tied_single_unit()
+    br = np.array([[1], [1], [1], [0]], np.uint8)
+    dW1, dW2, loss, _ = orc.gradients(hs, [HARDSHRINK], W1, W2, X, y, branch=br)
+    w1 = torch.tensor(W1, requires_grad=True)
+    w2 = torch.tensor(W2, requires_grad=True)
+    z = torch.tensor(X, dtype=torch.float64) @ w1.T                       # [4, 1]
+    lam = torch.tensor([[0.499], [0.5], [0.5], [0.501]], dtype=torch.float64)
+    h = torch.where(z.abs() > lam, z, torch.zeros_like(z))
+    logits = h @ w2.T
+    ce = torch.nn.functional.cross_entropy(logits, torch.tensor(y, dtype=torch.long))
+    ce.backward()
+    np.testing.assert_allclose(dW1, w1.grad.numpy(), rtol=1e-14)
+    np.testing.assert_allclose(dW2, w2.grad.numpy(), rtol=1e-14)
+    assert loss[0] == pytest.approx(ce.item(), rel=1e-14)
+
+
+def test_a_choice_outside_the_band_is_counted_and_ignored(orc):
+    hs, X, W1, W2, y = _tied_single_unit()
+    br = np.array([[0], [0], [1], [0]], np.uint8)        # sample 1 (Z = 1) is no tie
+    a = orc.gradients(hs, [HARDSHRINK], W1, W2, X, y, branch=br)
+    assert orc.branch_conflicts() == 1
+    b = orc.gradients(hs, [HARDSHRINK], W1, W2, X, y)
+    np.testing.assert_array_equal(a[0], b[0])
+    # in training, rows are offsets into the sample arrays: batch (2, 2)
+    # reads rows 2 and 3 only
+    orc.train(hs, [HARDSHRINK], W1, W2, X, y, [(2, 2)], 0.1, branch=br)
+    assert orc.branch_conflicts() == 0
