@@ -118,13 +118,53 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M,
                    const int32_t* hidden_sizes, const int32_t* act_ids,
                    uint64_t seed, int32_t flags);
 
+/* A pack of M MLPs with two hidden layers each (Section 7, Figure 3: the
+ * packing extended to deeper MLPs, where a second-layer unit sums only the
+ * first-layer units of its own model).  Model m maps F inputs through h1[m]
+ * units, then h2[m] units, both with activation act_ids[m], to O outputs:
+ *   Z1 = X W1^T, H1 = act(Z1), Z2 = H1 W12_m^T, H2 = act(Z2),
+ *   logits = M3 of H2 with W2 (Section 3)
+ * and trains, like every pack, by independent per-model softmax
+ * cross-entropy and plain SGD.  Parameters (pmlp_get_params_deep):
+ *   W1  [N1, F]  rows of the N1 = sum h1 first-layer units, model-major;
+ *   W12 [K]      model m's block [h2[m], h1[m]] row-major at offset
+ *                K_m = sum over earlier models of h1 h2 (K = the total);
+ *   W2  [O, N2]  columns of the N2 = sum h2 second-layer units.
+ * Initial values: W1 as pmlp_create (tag 1, fan_in F); W12 uniform with
+ * bound 1/sqrt(h1[m]) from the same stream with tag 5 and idx = the packed
+ * position; W2 with tag 2, idx = o*N2 + n, bound 1/sqrt(h2[m]).
+ * Such a handle takes pmlp_forward, pmlp_train_step, pmlp_losses,
+ * pmlp_nonfinite, pmlp_info (N = N1), pmlp_set_stream, profiling and the
+ * _deep calls below; the other calls, the PMLP_BF16_GEMM mode, biases,
+ * masks and the regression head return PMLP_ESTATE.  Arguments as for
+ * pmlp_create (h2[m] >= 1). */
+int pmlp_create_deep(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* h1,
+                     const int32_t* h2, const int32_t* act_ids, uint64_t seed);
+
+/* Gradients of sum_m L_m of a two-hidden-layer pack on one batch without an
+ * update (device, fp32): dW1_dev [N1, F], dW12_dev [K], dW2_dev [O, N2].
+ * Records the batch losses.  PMLP_ESTATE for a one-layer handle. */
+int pmlp_gradients_deep(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
+                        float* dW1_dev, float* dW12_dev, float* dW2_dev);
+
+/* Parameters of a two-hidden-layer pack to / from host memory in the
+ * layout above (any pointer may be null).  Synchronous. */
+int pmlp_get_params_deep(pmlp_t h, float* W1_host, float* W12_host, float* W2_host);
+int pmlp_set_params_deep(pmlp_t h, const float* W1_host, const float* W12_host,
+                         const float* W2_host);
+
+/* N2 (second-layer units) and K (entries of all W12 blocks) of a
+ * two-hidden-layer pack; PMLP_ESTATE for a one-layer handle. */
+int pmlp_info_deep(pmlp_t h, int64_t* N2, int64_t* K);
+
 /* Free the handle and every device buffer it owns (synchronises its
  * stream first).  A null handle is accepted. */
 int pmlp_destroy(pmlp_t h);
 
 /* Launch all later work on `stream` (a hipStream_t, passed as void*;
  * null selects the null stream).  The stream must belong to the device
- * the handle was created on. */
+ * the handle was created on; a stream of another device returns
+ * PMLP_EINVAL and the handle keeps its stream. */
 int pmlp_set_stream(pmlp_t h, void* stream);
 
 /* Select the arithmetic of the two input-layer products (Section 3 step 1,
@@ -204,11 +244,46 @@ int pmlp_gradients_mse(pmlp_t h, const float* X_dev, const float* Y_dev,
 int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev,
                 float* H_dev);
 
+/* Number of (step, model) pairs whose loss was not finite (NaN or
+ * infinite: a diverged model) since the last call or since creation, into
+ * *count_host; the count is then cleared.  Synchronises the stream.  The
+ * models train independently (Section 3), so a diverged model changes
+ * nothing for the others and the steps go on; this is how a caller learns
+ * that one diverged without reading every loss.  Null count_host returns
+ * PMLP_EINVAL. */
+int pmlp_nonfinite(pmlp_t h, int32_t* count_host);
+
 /* Copy the parameters to / from host memory in the layout above
  * (W1_host [N, F], W2_host [O, N], fp32).  Synchronous.  Either pointer
  * may be null to skip that tensor. */
 int pmlp_get_params(pmlp_t h, float* W1_host, float* W2_host);
 int pmlp_set_params(pmlp_t h, const float* W1_host, const float* W2_host);
+
+/* Parameters of some of the models (model selection in the pool of trained
+ * MLPs, Section 7; also a cheap hand-off of a sample of models to a
+ * checker): models_host [count] model indices (host, each in [0, M), any
+ * order, repeats allowed); with R = the sum of their hidden sizes,
+ * W1_host [R, F] receives their W1 rows and W2_host [O, R] their W2
+ * columns, model after model in the given order (the layout of a pack of
+ * just those models).  Either output may be null.  Synchronous.  Bad
+ * indices return PMLP_EINVAL before any copy. */
+int pmlp_get_models(pmlp_t h, const int32_t* models_host, int32_t count, float* W1_host,
+                    float* W2_host);
+
+/* Per-model input feature masks (feature selection, Section 7: each model
+ * may see its own subset of the input features).  mask_host [M, F] (host,
+ * row-major, one byte per entry): model m sees feature f where
+ * mask_host[m*F + f] != 0 and is then trained as the MLP whose whole input
+ * is those features.  The weights of the features a model does not see are
+ * set to zero now and held there: every later pmlp_set_params zeroes them
+ * again, every SGD step leaves them at zero and pmlp_gradients[_ex|_mse]
+ * returns zero for them; no step makes an extra pass over W1 for it (the
+ * dW1 product's epilogue drops their gradient).  Biases are never masked.
+ * Z = X W1^T then sums over the seen features only, as long as the unseen
+ * features of X are finite (they meet zero weights).  A null mask_host
+ * removes the masks (the zeroed weights stay zero until set or trained).
+ * Synchronises the stream.  The initial weights keep fan_in = F. */
+int pmlp_set_feature_mask(pmlp_t h, const uint8_t* mask_host);
 
 /* Biases of a handle created with PMLP_BIAS (PMLP_ESTATE otherwise):
  * b1_host [N], b2_host [M, O] (model-major), host memory, either may be
@@ -225,11 +300,28 @@ int pmlp_info(pmlp_t h, int64_t* N, int32_t* M, int32_t* F, int32_t* O);
  * PMLP_NUM_KERNELS-1, names from pmlp_kernel_name), the summed duration
  * in milliseconds and the number of launches since the last reset;
  * pmlp_profile_reset clears the totals. */
-#define PMLP_NUM_KERNELS 9
+#define PMLP_NUM_KERNELS 10
 int pmlp_set_profiling(pmlp_t h, int32_t enable);
 int pmlp_kernel_time(pmlp_t h, int32_t k, double* total_ms, int64_t* launches);
 int pmlp_profile_reset(pmlp_t h);
 const char* pmlp_kernel_name(int32_t k);
+
+/* The kernel that role k (as in pmlp_kernel_name) ran at its last launch
+ * on this handle, and the arithmetic of its matrix products, as chosen by
+ * the library for the shapes it was given: *name receives a library-owned
+ * string ("" before the first launch), *arith one of
+ *   PMLP_ARITH_NONE  no matrix products (memory and vector ALU work),
+ *   PMLP_ARITH_FP32  fp32 matrix-core products,
+ *   PMLP_ARITH_X3    fp32 products as six bf16 products of three-piece
+ *                    operand splits (fp32 accuracy),
+ *   PMLP_ARITH_BF16  bf16 operands, fp32 accumulation.
+ * Either pointer may be null.  Lets a caller price a kernel against the
+ * ceiling of the arithmetic it really ran. */
+#define PMLP_ARITH_NONE 0
+#define PMLP_ARITH_FP32 1
+#define PMLP_ARITH_X3 2
+#define PMLP_ARITH_BF16 3
+int pmlp_kernel_variant(pmlp_t h, int32_t k, const char** name, int32_t* arith);
 
 /* Message describing the last failure on the calling thread (a
  * library-owned string, valid until the next failing call on it). */

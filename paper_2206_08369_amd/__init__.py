@@ -25,7 +25,11 @@ __all__ = [
     "pmlp_gradients", "pmlp_hidden", "pmlp_get_params", "pmlp_set_params", "pmlp_info",
     "pmlp_set_profiling", "pmlp_kernel_time", "pmlp_profile_reset", "pmlp_kernel_name",
     "pmlp_last_error", "pmlp_gradients_ex", "pmlp_get_biases", "pmlp_set_biases",
-    "PMLP_MSE", "pmlp_train_step_mse", "pmlp_gradients_mse", "PackedMLP",
+    "PMLP_MSE", "pmlp_train_step_mse", "pmlp_gradients_mse", "pmlp_nonfinite",
+    "pmlp_set_feature_mask", "pmlp_get_models", "pmlp_create_deep", "pmlp_gradients_deep",
+    "pmlp_get_params_deep", "pmlp_set_params_deep", "pmlp_info_deep", "pmlp_kernel_variant",
+    "PMLP_ARITH_NONE", "PMLP_ARITH_FP32", "PMLP_ARITH_X3", "PMLP_ARITH_BF16", "PackedMLP",
+    "DeepPackedMLP",
 ]
 
 PMLP_OK = 0
@@ -37,7 +41,7 @@ PMLP_FP32 = 0
 PMLP_BF16_GEMM = 1
 PMLP_BIAS = 1
 PMLP_MSE = 2
-PMLP_NUM_KERNELS = 9
+PMLP_NUM_KERNELS = 10
 
 ACT_IDS = {
     "identity": 0, "relu": 1, "tanh": 2, "sigmoid": 3, "elu": 4, "leaky_relu": 5,
@@ -92,6 +96,15 @@ def load_library():
         "pmlp_set_profiling": [P, i32],
         "pmlp_kernel_time": [P, i32, C.POINTER(C.c_double), C.POINTER(i64)],
         "pmlp_profile_reset": [P],
+        "pmlp_nonfinite": [P, C.POINTER(i32)],
+        "pmlp_set_feature_mask": [P, P],
+        "pmlp_get_models": [P, P, i32, P, P],
+        "pmlp_create_deep": [C.POINTER(P), i32, i32, i32, P, P, P, u64],
+        "pmlp_gradients_deep": [P, P, P, i32, P, P, P],
+        "pmlp_get_params_deep": [P, P, P, P],
+        "pmlp_set_params_deep": [P, P, P, P],
+        "pmlp_info_deep": [P, C.POINTER(i64), C.POINTER(i64)],
+        "pmlp_kernel_variant": [P, i32, C.POINTER(C.c_char_p), C.POINTER(i32)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -220,6 +233,12 @@ def pmlp_hidden(h: int, X, B: int, Z=None, H=None) -> None:
     _check(load_library().pmlp_hidden(h, _ptr(X), int(B), _ptr(Z), _ptr(H)), "pmlp_hidden")
 
 
+def pmlp_nonfinite(h: int) -> int:
+    n = C.c_int32()
+    _check(load_library().pmlp_nonfinite(h, C.byref(n)), "pmlp_nonfinite")
+    return n.value
+
+
 def pmlp_get_params(h: int) -> Tuple[np.ndarray, np.ndarray]:
     N, _, F, O = pmlp_info(h)
     W1 = np.empty((N, F), np.float32)
@@ -244,6 +263,84 @@ def pmlp_set_params(h: int, W1: Optional[np.ndarray], W2: Optional[np.ndarray]) 
            "pmlp_set_params")
 
 
+def pmlp_get_models(h: int, models, hidden_sizes) -> Tuple[np.ndarray, np.ndarray]:
+    """W1 rows [R, F] and W2 columns [O, R] of the given models, in order."""
+    _, _, F, O = pmlp_info(h)
+    idx = _host(models, np.int32)
+    hs = np.asarray(hidden_sizes, np.int64)
+    ok = (idx >= 0) & (idx < hs.size)
+    if not ok.all():   # the library rejects the list before copying anything
+        _check(load_library().pmlp_get_models(h, idx.ctypes.data, int(idx.size), None, None),
+               "pmlp_get_models")
+    R = int(hs[idx].sum())
+    W1 = np.empty((R, F), np.float32)
+    W2 = np.empty((O, R), np.float32)
+    _check(load_library().pmlp_get_models(h, idx.ctypes.data, int(idx.size), W1.ctypes.data,
+                                          W2.ctypes.data), "pmlp_get_models")
+    return W1, W2
+
+
+def pmlp_create_deep(F: int, O: int, h1: Sequence[int], h2: Sequence[int],
+                     act_ids: Sequence[int], seed: int) -> int:
+    a, b, ac = _host(h1, np.int32), _host(h2, np.int32), _host(act_ids, np.int32)
+    if not (a.shape == b.shape == ac.shape and a.ndim == 1):
+        raise ValueError("h1, h2 and act_ids must be 1-D of equal length")
+    h = C.c_void_p()
+    _check(load_library().pmlp_create_deep(C.byref(h), int(F), int(O), int(a.size), a.ctypes.data,
+                                           b.ctypes.data, ac.ctypes.data,
+                                           int(seed) & 0xFFFFFFFFFFFFFFFF), "pmlp_create_deep")
+    return h.value
+
+
+def pmlp_gradients_deep(h: int, X, y, B: int, dW1, dW12, dW2) -> None:
+    _check(load_library().pmlp_gradients_deep(h, _ptr(X), _ptr(y), int(B), _ptr(dW1), _ptr(dW12),
+                                              _ptr(dW2)), "pmlp_gradients_deep")
+
+
+def pmlp_info_deep(h: int) -> Tuple[int, int]:
+    n2, k = C.c_int64(), C.c_int64()
+    _check(load_library().pmlp_info_deep(h, C.byref(n2), C.byref(k)), "pmlp_info_deep")
+    return n2.value, k.value
+
+
+def pmlp_get_params_deep(h: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    N1, _, F, O = pmlp_info(h)
+    N2, K = pmlp_info_deep(h)
+    W1 = np.empty((N1, F), np.float32)
+    W12 = np.empty(K, np.float32)
+    W2 = np.empty((O, N2), np.float32)
+    _check(load_library().pmlp_get_params_deep(h, W1.ctypes.data, W12.ctypes.data, W2.ctypes.data),
+           "pmlp_get_params_deep")
+    return W1, W12, W2
+
+
+def pmlp_set_params_deep(h: int, W1=None, W12=None, W2=None) -> None:
+    N1, _, F, O = pmlp_info(h)
+    N2, K = pmlp_info_deep(h)
+    arrs = []
+    for a, shape, what in ((W1, (N1, F), "W1"), (W12, (K,), "W12"), (W2, (O, N2), "W2")):
+        if a is None:
+            arrs.append(None)
+            continue
+        c = _host(a, np.float32)
+        if c.shape != shape:
+            raise ValueError("%s must be %s" % (what, shape))
+        arrs.append(c)
+    _check(load_library().pmlp_set_params_deep(h, *[None if c is None else c.ctypes.data
+                                                    for c in arrs]), "pmlp_set_params_deep")
+
+
+def pmlp_set_feature_mask(h: int, mask: Optional[np.ndarray]) -> None:
+    if mask is None:
+        _check(load_library().pmlp_set_feature_mask(h, None), "pmlp_set_feature_mask")
+        return
+    _, M, F, _ = pmlp_info(h)
+    a = np.ascontiguousarray(np.asarray(mask) != 0, dtype=np.uint8)
+    if a.shape != (M, F):
+        raise ValueError("feature masks must be [M, F] = [%d, %d]" % (M, F))
+    _check(load_library().pmlp_set_feature_mask(h, a.ctypes.data), "pmlp_set_feature_mask")
+
+
 def pmlp_info(h: int) -> Tuple[int, int, int, int]:
     N, M, F, O = C.c_int64(), C.c_int32(), C.c_int32(), C.c_int32()
     _check(load_library().pmlp_info(h, C.byref(N), C.byref(M), C.byref(F), C.byref(O)),
@@ -260,6 +357,17 @@ def pmlp_kernel_time(h: int, k: int) -> Tuple[float, int]:
     _check(load_library().pmlp_kernel_time(h, int(k), C.byref(ms), C.byref(n)),
            "pmlp_kernel_time")
     return ms.value, n.value
+
+
+PMLP_ARITH_NONE, PMLP_ARITH_FP32, PMLP_ARITH_X3, PMLP_ARITH_BF16 = 0, 1, 2, 3
+
+
+def pmlp_kernel_variant(h: int, k: int) -> Tuple[str, int]:
+    """(kernel name, PMLP_ARITH_*) of role k's last launch."""
+    name, arith = C.c_char_p(), C.c_int32()
+    _check(load_library().pmlp_kernel_variant(h, int(k), C.byref(name), C.byref(arith)),
+           "pmlp_kernel_variant")
+    return (name.value or b"").decode(), arith.value
 
 
 def pmlp_profile_reset(h: int) -> None:
@@ -395,11 +503,24 @@ class PackedMLP:
     def losses(self) -> np.ndarray:
         return pmlp_losses(self.handle)
 
+    def nonfinite_count(self) -> int:
+        """(step, model) pairs with a non-finite loss since the last call."""
+        return pmlp_nonfinite(self.handle)
+
     def get_params(self) -> Tuple[np.ndarray, np.ndarray]:
         return pmlp_get_params(self.handle)
 
+    def get_models(self, models) -> Tuple[np.ndarray, np.ndarray]:
+        """W1 [R, F] and W2 [O, R] of the given models (R: their hidden units)."""
+        return pmlp_get_models(self.handle, models, self.hidden_sizes)
+
     def set_params(self, W1=None, W2=None) -> None:
         pmlp_set_params(self.handle, W1, W2)
+
+    def set_feature_mask(self, mask) -> None:
+        """Per-model input feature masks [M, F] (nonzero: the model sees the
+        feature), or None to remove them."""
+        pmlp_set_feature_mask(self.handle, mask)
 
     def get_biases(self) -> Tuple[np.ndarray, np.ndarray]:
         """b1 [N], b2 [M, O] of a handle made with biases=True."""
@@ -416,5 +537,48 @@ class PackedMLP:
         return {pmlp_kernel_name(k): pmlp_kernel_time(self.handle, k)
                 for k in range(PMLP_NUM_KERNELS)}
 
+    def kernel_variants(self):
+        """{kernel role: (kernel name, PMLP_ARITH_*)} of the last launches."""
+        return {pmlp_kernel_name(k): pmlp_kernel_variant(self.handle, k)
+                for k in range(PMLP_NUM_KERNELS)}
+
     def profile_reset(self) -> None:
         pmlp_profile_reset(self.handle)
+
+
+class DeepPackedMLP(PackedMLP):
+    """M independent MLPs with two hidden layers each (h1[m] then h2[m]
+    units, one activation per model), packed as one network.  Takes the
+    forward, train_step, losses and nonfinite_count calls of PackedMLP;
+    gradients and parameters carry the hidden-to-hidden blocks W12."""
+
+    def __init__(self, F: int, O: int, h1: Sequence[int], h2: Sequence[int],
+                 act_ids: Sequence[int], seed: int = 0):
+        import torch
+        self._torch = torch
+        self.device = torch.device("cuda", torch.cuda.current_device())
+        self.biases = False
+        self.head = "ce"
+        self.handle = pmlp_create_deep(F, O, h1, h2, act_ids, seed)
+        self.N, self.M, self.F, self.O = pmlp_info(self.handle)
+        self.N2, self.K = pmlp_info_deep(self.handle)
+        self.hidden_sizes = _host(h1, np.int32)
+        self.hidden_sizes2 = _host(h2, np.int32)
+        self.act_ids = _host(act_ids, np.int32)
+
+    def gradients(self, X, y):
+        B = self._x(X)
+        self._y(y, B)
+        t = self._torch
+        dW1 = t.empty((self.N, self.F), dtype=t.float32, device=self.device)
+        dW12 = t.empty(max(self.K, 1), dtype=t.float32, device=self.device)
+        dW2 = t.empty((self.O, self.N2), dtype=t.float32, device=self.device)
+        self._stream()
+        pmlp_gradients_deep(self.handle, X, y, B, dW1, dW12, dW2)
+        return dW1, dW12[:self.K], dW2
+
+    def get_params(self):
+        return pmlp_get_params_deep(self.handle)
+
+    def set_params(self, W1=None, W12=None, W2=None) -> None:
+        pmlp_set_params_deep(self.handle, W1, W12, W2)

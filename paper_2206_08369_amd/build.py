@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libpmlp.so")
-SOURCES = ("k_misc.hip", "k_gemm.hip", "k_gemm_bf16.hip", "k_m3.hip", "k_lds.hip", "api.hip")
+SOURCES = ("k_misc.hip", "k_gemm.hip", "k_gemm_bf16.hip", "k_m3.hip", "k_lds.hip", "k_deep.hip",
+           "api.hip")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

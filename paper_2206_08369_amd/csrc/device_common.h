@@ -44,6 +44,45 @@ inline unsigned grid_for(int64_t n) {
 }
 
 // ---------------------------------------------------------------------------
+// Counter-based draws for the initial weights: splitmix64 (Steele, Lea and
+// Flood, OOPSLA 2014) of key ^ (tag << 60) ^ idx, whose top 24 bits give
+// u in [0, 1); the weight is (2u - 1) * bound with one fp32 rounding.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ float uniform_weight(uint64_t key, uint64_t tag, uint64_t idx,
+                                                float bound) {
+  const uint64_t r = splitmix64(key ^ (tag << 60) ^ idx);
+  const int32_t k = (int32_t)(r >> 40);                             // 24 random bits
+  const float c = (float)(2 * k - 16777216) * 5.9604644775390625e-08f;  // exact: (2u - 1)
+  return c * bound;                                                // one rounding
+}
+
+// ---------------------------------------------------------------------------
+// Per-model input feature masks (feature selection, Section 7): bit q of
+// word fm[m * fmw + q / 32] is 1 when model m sees input column q (columns
+// from F on, padding and the bias column, always 1).  A masked weight is
+// held at zero by zeroing its gradient wherever the dW1 product is stored
+// or applied, so Z = X W1^T needs no mask.  fm null: no masks.
+// ---------------------------------------------------------------------------
+
+// v with the entries of columns q .. q+3 (q a multiple of 4) that model m
+// does not see set to zero.
+__device__ __forceinline__ f32x4 fmask4(const uint32_t* __restrict__ fm, int fmw, int m, int q,
+                                        f32x4 v) {
+  if (!fm) return v;
+  const uint32_t bits = fm[(int64_t)m * fmw + (q >> 5)] >> (q & 31);
+  return f32x4{(bits & 1u) ? v[0] : 0.f, (bits & 2u) ? v[1] : 0.f, (bits & 4u) ? v[2] : 0.f,
+               (bits & 8u) ? v[3] : 0.f};
+}
+
+// ---------------------------------------------------------------------------
 // Activations (Section 3, last paragraph: one activation per contiguous
 // portion of the hidden layer; the list of Section 4.2).  Ids as in
 // include/pmlp.h.

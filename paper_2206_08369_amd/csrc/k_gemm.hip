@@ -127,21 +127,26 @@ __global__ __launch_bounds__(kBlock) void k_gemm_nt(GemmArgs a, int WQ) {
     if (p >= a.NP) continue;
     float* orow = a.out + p * a.ldo;
     const float lr = (EPI == EPI_SGD && a.lrm) ? a.lrm[a.mid[p]] : a.lr;
+    const int mrow = (EPI != EPI_STORE && a.fmask) ? a.mid[p] : 0;
 #pragma unroll
     for (int i = 0; i < TQ; ++i) {
       const int q = q0 + 16 * i + 4 * lk;
       if (q >= a.NQ) continue;
       if (EPI == EPI_STORE) {
         *(f32x4*)(orow + q) = acc[i][j];
-      } else if (EPI == EPI_SGD) {
+        continue;
+      }
+      // masked features: zero gradient, so their weights stay 0
+      const f32x4 g = fmask4(a.fmask, a.fmw, mrow, q, acc[i][j]);
+      if (EPI == EPI_SGD) {
         f32x4 w = *(f32x4*)(orow + q);
-        w -= lr * acc[i][j];
+        w -= lr * g;
         *(f32x4*)(orow + q) = w;
       } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (q + r < a.ncols) orow[q + r] = acc[i][j][r];
-          else if (q + r == a.bcol && a.db1) a.db1[p] = acc[i][j][r];
+          if (q + r < a.ncols) orow[q + r] = g[r];
+          else if (q + r == a.bcol && a.db1) a.db1[p] = g[r];
       }
     }
   }
@@ -160,6 +165,7 @@ static void gemm_dispatch(const GemmArgs& a, int epi, int WQ, hipStream_t s) {
 }
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s) {
+  note_variant("k_gemm_nt", kArithFp32);
   if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
   if (a.NQ <= 16) gemm_dispatch<1, 8>(a, epi, 1, s);
   else if (a.NQ <= 32) gemm_dispatch<2, 8>(a, epi, 1, s);

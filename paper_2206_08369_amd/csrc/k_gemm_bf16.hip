@@ -271,14 +271,17 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
 #pragma unroll
       for (int pass = 0; pass < 32 * LPR / 64; ++pass) {
         const int r = pass * (64 / LPR) + lane / LPR, c4 = 4 * (lane % LPR);
-        const f32x4 v = *(const f32x4*)(scr + r * LDT + c4);
+        const f32x4 v0 = *(const f32x4*)(scr + r * LDT + c4);
         const int64_t p = pb + r;
         const int q = qb + c4;
         if (p >= a.NP || q >= a.NQ) continue;
         float* o = a.out + p * a.ldo + q;
         const float lr = (EPI == EPI_SGD && a.lrm) ? a.lrm[a.mid[p]] : a.lr;
+        // masked features: zero gradient, so their weights stay 0
+        const f32x4 v =
+            (EPI != EPI_STORE && a.fmask) ? fmask4(a.fmask, a.fmw, a.mid[p], q, v0) : v0;
         if (EPI == EPI_STORE) {
-          *(f32x4*)o = v;
+          *(f32x4*)o = v0;
         } else if (EPI == EPI_SGD) {
           f32x4 w = *(f32x4*)o;
           w -= lr * v;
@@ -337,6 +340,7 @@ hipError_t gemm_bf_p(const GemmBfArgs& a, int epi, hipStream_t s) {
 }
 
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
+  note_variant("k_gemm_bf", kArithBf16);
   if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
   if (!gemm_bf16_args_ok(a)) return hipErrorInvalidValue;
   // q tile no wider than needed for small q; 256 x 256 tiles otherwise (the

@@ -648,6 +648,15 @@ __global__ __launch_bounds__(NT) void k_bwd_lds(BwdArgs a) {
         tacc[q] = v;
       }
     }
+    if (a.fmask) {  // masked features: zero gradient, so their weights stay 0
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) acc[i] = fmask4(a.fmask, a.fmw, m, 16 * i + 4 * lk, acc[i]);
+      if (TAIL) {
+        const f32x4 t = fmask4(a.fmask, a.fmw, m, 16 * TQ, f32x4{tacc[0], tacc[1], tacc[2], tacc[3]});
+#pragma unroll
+        for (int q = 0; q < 4; ++q) tacc[q] = t[q];
+      }
+    }
     if (grad) {
       if (p < a.N) {
         if (lk == 0)
@@ -872,6 +881,11 @@ __global__ __launch_bounds__(NT) void k_bwd_x3(BwdArgs a) {
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
       dw[o] = v;
+    }
+    if (a.fmask) {  // masked features: zero gradient, so their weights stay 0
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) acc[i] = fmask4(a.fmask, a.fmw, m, 16 * i + 4 * lk, acc[i]);
+      if (TAIL) acc[TQ] = fmask4(a.fmask, a.fmw, m, 16 * TQ, acc[TQ]);
     }
     if (grad) {
       if (p < a.N) {
@@ -1115,6 +1129,11 @@ __global__ __launch_bounds__(NT, TQ <= 2 ? 3 : 2) void k_bwd_mf(BwdArgs a) {
       default: PMLP_BWDM(-1); break;
     }
 #undef PMLP_BWDM
+    if (a.fmask) {  // masked features: zero gradient, so their weights stay 0
+#pragma unroll
+      for (int i = 0; i < TQ; ++i)
+        acc[i] = fmask4(a.fmask, a.fmw, m_row, 16 * i + 4 * lk, acc[i]);
+    }
     // lane (li, lk) holds dW2[4lk + r][row li]
     if (grad) {
       if (p < a.N) {
@@ -1209,6 +1228,7 @@ static hipError_t fwd_x3_go(const FwdLdsArgs& a, hipStream_t s) {
   constexpr int U = NC <= 3 ? 2 : 1;
   const int64_t T = (a.N + 16 * U - 1) / (16 * U);
   const size_t lds = fwd_x3_bytes(a.Bp, a.K);
+  note_variant("k_fwd_x3", kArithX3);
   switch ((a.K % 32) / 4) {
     case 0: return launch_persistent(k_fwd_x3<TQ, NC, U, 0>, kLdsBlock, lds, T, s, a);
     case 1: return launch_persistent(k_fwd_x3<TQ, NC, U, 1>, kLdsBlock, lds, T, s, a);
@@ -1219,8 +1239,10 @@ static hipError_t fwd_x3_go(const FwdLdsArgs& a, hipStream_t s) {
 template <int TQ>
 static hipError_t fwd_lds_go(const FwdLdsArgs& a, size_t lds, int64_t T, hipStream_t s) {
   if constexpr (TQ <= 4) {
-    if (a.K <= 32 && a.K % 16 == 0)
+    if (a.K <= 32 && a.K % 16 == 0) {
+      note_variant("k_fwd_lds_ring", kArithFp32);
       return launch_persistent(k_fwd_lds_ring<TQ, 2, 0, 4>, kLdsBlock, lds, T, s, a);
+    }
   } else {
     if (fwd_x3_bytes(a.Bp, a.K) <= (size_t)dev_info().lds_max) {
       switch (a.K / 32) {
@@ -1232,6 +1254,7 @@ static hipError_t fwd_lds_go(const FwdLdsArgs& a, size_t lds, int64_t T, hipStre
       }
     }
   }
+  note_variant("k_fwd_lds", kArithFp32);
   return launch_persistent(k_fwd_lds<TQ>, kLdsBlock, lds, T, s, a);
 }
 
@@ -1273,6 +1296,7 @@ template <int TQ>
 static hipError_t bwd_mf_go(const BwdArgs& a, size_t lds, hipStream_t s) {
   const int64_t T = (a.N + 15) / 16;
   constexpr int NT = TQ <= 2 ? 256 : 512;
+  note_variant("k_bwd_mf", kArithFp32);
   return launch_persistent(k_bwd_mf<TQ, 2, NT>, NT, lds, T, s, a);
 }
 
@@ -1291,6 +1315,7 @@ static bool bwd_x3_shape(const BwdArgs& a) {
 static hipError_t bwd_x3_go(const BwdArgs& a, hipStream_t s) {
   const int64_t T = (a.N + 15) / 16;
   const size_t lds = bwd_x3_bytes(a.Bp, a.F4);
+  note_variant("k_bwd_x3", kArithX3);
   if (a.F4 == 100) return launch_persistent(k_bwd_x3<6, 2, 2, 512, true>, 512, lds, T, s, a);
   return launch_persistent(k_bwd_x3<3, 2, 2, 512, true>, 512, lds, T, s, a);
 }
@@ -1303,6 +1328,7 @@ static hipError_t bwd_lds_go(const BwdArgs& a, size_t lds, hipStream_t s) {
   constexpr int RING = OM <= 2 && !TAIL ? 4 : (OM <= 4 ? 3 : 2);
   constexpr int NT = OM <= 2 && TQ <= 7 ? 768 : 512;
   const int64_t T = (a.N + 15) / 16;
+  note_variant("k_bwd_lds", kArithFp32);
   return launch_persistent(k_bwd_lds<TQ, OM, RING, NT, TAIL>, NT, lds, T, s, a);
 }
 

@@ -292,6 +292,7 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
                          const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
                          int64_t sm, int64_t sb, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
+  note_variant(O <= 4 ? "k_m3_fwd" : "k_m3_fwd_mf", O <= 4 ? kArithNone : kArithFp32);
   if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
   else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
   // wider output layers: one MFMA per four units and 16 samples
@@ -477,6 +478,7 @@ hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2,
                          int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
                          const int32_t* act, const float* G, float lr, const float* lrm,
                          float* dW2, hipStream_t s) {
+  note_variant("k_m3_bwd", kArithNone);
   if (O <= 2) m3_bwd_dispatch<2>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
   else if (O <= 4) m3_bwd_dispatch<4>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
   else if (O <= 8) m3_bwd_dispatch<8>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);

@@ -5,24 +5,9 @@
 namespace pmlpk {
 
 // ---------------------------------------------------------------------------
-// Initialisation: counter-based splitmix64 draws (Steele, Lea and Flood,
-// OOPSLA 2014), U(-bound, bound) with bound = 1/sqrt(fan_in).
+// Initialisation: U(-bound, bound) with bound = 1/sqrt(fan_in), from the
+// counter-based draws of device_common.h.
 // ---------------------------------------------------------------------------
-
-__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
-  uint64_t z = x + 0x9E3779B97F4A7C15ull;
-  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-  return z ^ (z >> 31);
-}
-
-__device__ __forceinline__ float uniform_weight(uint64_t key, uint64_t tag, uint64_t idx,
-                                                float bound) {
-  const uint64_t r = splitmix64(key ^ (tag << 60) ^ idx);
-  const int32_t k = (int32_t)(r >> 40);                             // 24 random bits
-  const float c = (float)(2 * k - 16777216) * 5.9604644775390625e-08f;  // exact: (2u - 1)
-  return c * bound;                                                // one rounding
-}
 
 __global__ __launch_bounds__(kBlock) void k_init_w1(float* __restrict__ W1, int64_t N, int F,
                                                     int F4, float bound, uint64_t key) {
@@ -53,6 +38,12 @@ hipError_t launch_init_params(float* W1, int64_t N, int32_t F, int32_t F4, float
                               float* W2, int64_t ldw, int32_t O, const int32_t* mid,
                               const float* bound2, uint64_t key, hipStream_t s) {
   k_init_w1<<<grid_for(N * F4), kBlock, 0, s>>>(W1, N, F, F4, bound1, key);
+  k_init_w2<<<grid_for(N * O), kBlock, 0, s>>>(W2, N, ldw, O, mid, bound2, key);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_w2(float* W2, int64_t N, int64_t ldw, int32_t O, const int32_t* mid,
+                          const float* bound2, uint64_t key, hipStream_t s) {
   k_init_w2<<<grid_for(N * O), kBlock, 0, s>>>(W2, N, ldw, O, mid, bound2, key);
   return hipGetLastError();
 }
@@ -103,6 +94,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_x(const float* __restrict__ X, 
 
 hipError_t launch_pack_x(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
                          int32_t bcol, float* Xp, float* Xt, hipStream_t s) {
+  note_variant("k_pack_x", kArithNone);
   k_pack_x<<<grid_for((int64_t)Bp * F4), kBlock, 0, s>>>(X, B, F, Bp, F4, bcol, Xp, Xt);
   return hipGetLastError();
 }
@@ -137,6 +129,7 @@ __global__ __launch_bounds__(kBlock) void k_pack_x_bf16(const float* __restrict_
 hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, int32_t F4,
                               int32_t bcol, unsigned short* Xp16, unsigned short* Xt16,
                               hipStream_t s) {
+  note_variant("k_pack_x_bf16", kArithNone);
   const int ldp = bf16_ld(F4), ldt = bf16_ld(Bp);
   k_pack_x_bf16<<<grid_for((int64_t)Bp * ldp + (int64_t)F4 * ldt), kBlock, 0, s>>>(
       X, B, F, Bp, F4, bcol, ldp, ldt, Xp16, Xt16);
@@ -157,6 +150,7 @@ __global__ __launch_bounds__(kBlock) void k_w1_to_bf16(const float* __restrict__
 
 hipError_t launch_w1_to_bf16(const float* W1, int64_t Npad, int32_t F4, unsigned short* W1b,
                              int32_t ldb, hipStream_t s) {
+  note_variant("k_w1_to_bf16", kArithNone);
   const int64_t total = Npad * ldb;
   k_w1_to_bf16<<<grid_for(total), kBlock, 0, s>>>(W1, total, F4, ldb, W1b);
   return hipGetLastError();
@@ -169,8 +163,31 @@ __global__ __launch_bounds__(kBlock) void k_fill(float* __restrict__ p, int64_t 
 }
 
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s) {
+  note_variant("k_fill", kArithNone);
   if (n <= 0) return hipSuccess;
   k_fill<<<grid_for(n), kBlock, 0, s>>>(p, n, v);
+  return hipGetLastError();
+}
+
+// Zero the weights of the input features a model does not see (run when
+// the masks or the weights are set; the SGD steps then keep them at zero).
+__global__ __launch_bounds__(kBlock) void k_apply_fmask(float* __restrict__ W1, int64_t total,
+                                                        int F4, const int32_t* __restrict__ mid,
+                                                        const uint32_t* __restrict__ fm,
+                                                        int fmw) {
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int64_t n = i / F4;
+    const int q = (int)(i - n * F4);
+    if (!((fm[(int64_t)mid[n] * fmw + (q >> 5)] >> (q & 31)) & 1u)) W1[i] = 0.f;
+  }
+}
+
+hipError_t launch_apply_fmask(float* W1, int64_t Npad, int32_t F4, const int32_t* mid,
+                              const uint32_t* fmask, int32_t fmw, hipStream_t s) {
+  const int64_t total = Npad * F4;
+  if (total <= 0 || !fmask) return hipSuccess;
+  k_apply_fmask<<<grid_for(total), kBlock, 0, s>>>(W1, total, F4, mid, fmask, fmw);
   return hipGetLastError();
 }
 
@@ -181,7 +198,8 @@ hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s) {
 //   LG[m][b][:] (logits) -> G = (softmax - onehot(y_b)) / B,  G = 0 for b >= B
 //   loss[m] = mean_b (logsumexp - logit_y)
 // A label outside [0, O) raises flag[0]; a non-finite per-model rate (lrm,
-// may be null) raises flag[1].
+// may be null) raises flag[1]; every model whose loss is not finite adds one
+// to flag[2].
 // ---------------------------------------------------------------------------
 
 template <int OM>
@@ -236,7 +254,10 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
   }
 #pragma unroll
   for (int s = 32; s > 0; s >>= 1) part += __shfl_xor(part, s);
-  if (lane == 0) loss[m] = part * invB;
+  if (lane == 0) {
+    loss[m] = part * invB;
+    if (!isfinite(part)) atomicAdd(flag + 2, 1);
+  }
   if (b2) {
     const float rate = lrm ? lrm[m] : lr;
 #pragma unroll
@@ -254,6 +275,7 @@ __global__ __launch_bounds__(kBlock) void k_ce(float* __restrict__ LG,
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
                      float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
                      float lr, hipStream_t s) {
+  note_variant("k_ce", kArithNone);
   const unsigned blocks = (unsigned)((M + 3) / 4);
   const float invB = 1.0f / (float)B;
   if (O <= 2) k_ce<2><<<blocks, kBlock, 0, s>>>(LG, y, M, Bp, B, O, invB, loss, flag, lrm, b2, db2, lr);
@@ -305,7 +327,10 @@ __global__ __launch_bounds__(kBlock) void k_mse(float* __restrict__ LG,
   }
 #pragma unroll
   for (int s = 32; s > 0; s >>= 1) part += __shfl_xor(part, s);
-  if (lane == 0) loss[m] = part * inv;
+  if (lane == 0) {
+    loss[m] = part * inv;
+    if (!isfinite(part)) atomicAdd(flag + 2, 1);
+  }
   if (b2) {
     const float rate = lrm ? lrm[m] : lr;
 #pragma unroll
@@ -323,6 +348,7 @@ __global__ __launch_bounds__(kBlock) void k_mse(float* __restrict__ LG,
 hipError_t launch_mse(float* LG, const float* Y, int32_t M, int32_t Bp, int32_t B, int32_t O,
                       float* loss, int32_t* flag, const float* lrm, float* b2, float* db2,
                       float lr, hipStream_t s) {
+  note_variant("k_mse", kArithNone);
   const unsigned blocks = (unsigned)((M + 3) / 4);
   const float inv = 1.0f / ((float)B * (float)O);
   if (O <= 2) k_mse<2><<<blocks, kBlock, 0, s>>>(LG, Y, M, Bp, B, O, inv, loss, flag, lrm, b2, db2, lr);
@@ -356,6 +382,7 @@ __global__ __launch_bounds__(kBlock) void k_hidden_out(const float* __restrict__
 hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              const int32_t* mid, const int32_t* act, float* Z, float* H,
                              hipStream_t s) {
+  note_variant("k_hidden_out", kArithNone);
   k_hidden_out<<<grid_for((int64_t)B * N), kBlock, 0, s>>>(Zt, Bp, B, N, mid, act, Z, H);
   return hipGetLastError();
 }

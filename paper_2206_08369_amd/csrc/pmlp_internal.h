@@ -30,8 +30,23 @@ enum KernelId {
   KID_GEMM_BWD = 6,
   KID_AUX = 7,
   KID_BWD_FUSED = 8,  // fused backward (M3 backward + dW1 GEMM + updates)
-  KID_COUNT = 9
+  KID_DEEP = 9,       // the hidden-to-hidden layer of two-layer packs
+  KID_COUNT = 10
 };
+
+// The kernel a launcher chose and the arithmetic of its matrix products
+// (PMLP_ARITH_* of include/pmlp.h): every launcher notes it for the host
+// library, which keeps the last one per kernel role for pmlp_kernel_variant.
+struct KernelVariant {
+  const char* name;
+  int32_t arith;
+};
+inline KernelVariant& last_variant() {
+  static thread_local KernelVariant v{"", 0};
+  return v;
+}
+inline void note_variant(const char* name, int32_t arith) { last_variant() = KernelVariant{name, arith}; }
+constexpr int32_t kArithNone = 0, kArithFp32 = 1, kArithX3 = 2, kArithBf16 = 3;
 
 // GEMM epilogues: C[p][q] = sum_k P[p][k] Q[q][k]
 enum GemmEpi {
@@ -56,6 +71,8 @@ struct GemmArgs {
   const int32_t* mid;  // model of each row p (with lrm)
   float* db1;          // EPI_GRAD: column bcol (the hidden bias) goes to db1[p]
   int32_t bcol;
+  const uint32_t* fmask;  // EPI_SGD / EPI_GRAD: per-model feature masks (null: none)
+  int32_t fmw;            // words per model of fmask
 };
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
@@ -82,6 +99,8 @@ struct GemmBfArgs {
   int32_t bcol;
   unsigned short* outb;     // EPI_SGD: also store bf16 of the updated values (or null)
   int64_t ldob;
+  const uint32_t* fmask;    // EPI_SGD / EPI_GRAD: per-model feature masks (null: none)
+  int32_t fmw;              // words per model of fmask
 };
 bool gemm_bf16_args_ok(const GemmBfArgs& a);
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s);
@@ -121,6 +140,8 @@ struct BwdArgs {
   const float* lrm;  // per-model rates (null: lr for every row)
   float* db1;        // gradient mode: column bcol (the hidden bias) goes to db1[p]
   int32_t bcol;
+  const uint32_t* fmask;  // per-model feature masks of the dW1 product (null: none)
+  int32_t fmw;            // words per model of fmask
 };
 bool bwd_lds_supported(int32_t Bp, int32_t F4, int32_t O);
 hipError_t launch_bwd_lds(const BwdArgs& a, hipStream_t s);
@@ -158,7 +179,8 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
                          int64_t sm, int64_t sb, hipStream_t s);
 
 // flag[0] is raised by a label outside [0, O), flag[1] by a non-finite
-// per-model rate in lrm (may be null).
+// per-model rate in lrm (may be null); flag[2] counts models whose loss is
+// not finite (the regression head as well).
 // With b2 set, db2[m][o] = sum_b G[m][b][o] is stored into db2 (gradient
 // mode) or applied as b2 -= lr_m db2 (the rate lrm[m], or lr).
 hipError_t launch_ce(float* LG, const int32_t* y, int32_t M, int32_t Bp, int32_t B, int32_t O,
@@ -185,5 +207,46 @@ hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              hipStream_t s);
 
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
+
+// Two hidden layers per model (Section 7, Figure 3).  Model m has h1[m]
+// first-layer units (rows off1[m].. of Zt1), h2[m] second-layer units (rows
+// off2[m].. of Zt2) and the hidden-to-hidden block W12[koff[m] ..] of
+// [h2[m]][h1[m]] (row-major).
+struct DeepArgs {
+  const int64_t* off1;  // [M+1]
+  const int64_t* off2;  // [M+1]
+  const int64_t* koff;  // [M+1]
+  const int32_t* h1;    // [M]
+  const int32_t* h2;    // [M]
+  const int32_t* act;   // [M]
+  const float* W12;     // [K]
+};
+struct SegUnit {   // rows r0 .. r0+7 (those that exist) of one layer of model m
+  int32_t m, r0;
+};
+struct SegTile {   // rows i0 .. i0+15, columns j0 .. j0+63 of model m's W12 block
+  int32_t m, i0, j0, pad;
+};
+
+hipError_t launch_init_w2(float* W2, int64_t N, int64_t ldw, int32_t O, const int32_t* mid,
+                          const float* bound2, uint64_t key, hipStream_t s);
+hipError_t launch_init_w12(float* W12, int64_t K, const int64_t* koff, int32_t M,
+                           const float* bound12, uint64_t key, hipStream_t s);
+// Zt2 = W12 act(Zt1) per model; units over second-layer rows.
+hipError_t launch_seg_fwd(const float* Zt1, float* Zt2, int32_t Bp, const DeepArgs& a,
+                          const SegUnit* units, int32_t nunits, hipStream_t s);
+// G12 = dZ2 act(Zt1)^T per model; tiles of the W12 blocks.
+hipError_t launch_seg_grad(const float* Zt1, const float* dZ2, int32_t Bp, const DeepArgs& a,
+                           const SegTile* tiles, int32_t ntiles, float* G12, hipStream_t s);
+// Zt1 <- (W12^T dZ2) * act'(Zt1) per model; units over first-layer rows.
+hipError_t launch_seg_back(float* Zt1, const float* dZ2, int32_t Bp, const DeepArgs& a,
+                           const SegUnit* units, int32_t nunits, hipStream_t s);
+// W -= lr G
+hipError_t launch_sgd(float* W, const float* G, int64_t n, float lr, hipStream_t s);
+
+// W1[n][q] = 0 wherever model mid[n] does not see column q (fmask as in
+// the argument structs above), for n < Npad and q < F4.
+hipError_t launch_apply_fmask(float* W1, int64_t Npad, int32_t F4, const int32_t* mid,
+                              const uint32_t* fmask, int32_t fmw, hipStream_t s);
 
 }  // namespace pmlpk
