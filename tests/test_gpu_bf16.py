@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 import pmlp_workloads as wl
-from parity import cross_entropy, err_cols, err_logits, err_losses, err_rows, submodel
+from parity import offsets, cross_entropy, err_cols, err_logits, err_losses, err_rows, submodel
 
 pytestmark = pytest.mark.gpu
 
@@ -189,12 +189,13 @@ def test_bf16_full_size_w10k_f1000_on_sampled_models(pm, orc, torch):
     hs, acts = w.model_grid()
     X, y = wl.make_dataset(w.F, w.O, w.B, w.data_seed)
     net = bf16_net(pm, w.F, w.O, hs, acts, seed=w.init_seed)
-    W1, W2 = net.get_params()
+    models = np.unique(np.concatenate([np.arange(7, w.M, w.M // 12), [0, 999, w.M - 1]]))
+    sW1, sW2 = net.get_models(models)
+    shs, sacts = hs[models], acts[models]
+    rows = np.concatenate([np.arange(o, o + h) for o, h in zip(offsets(hs)[models], shs)])
     Xd, yd = dev(torch, X), dev(torch, y)
     dW1, dW2 = net.gradients(Xd, yd)
     loss = net.losses()
-    models = np.unique(np.concatenate([np.arange(7, w.M, w.M // 12), [0, 999, w.M - 1]]))
-    shs, sacts, sW1, sW2, rows = submodel(hs, acts, W1, W2, models)
     rows_t = torch.from_numpy(rows).cuda()
     g1 = dW1.index_select(0, rows_t).cpu().numpy()
     g2 = dW2.index_select(1, rows_t).cpu().numpy()
@@ -204,10 +205,10 @@ def test_bf16_full_size_w10k_f1000_on_sampled_models(pm, orc, torch):
     assert err_cols(g2, r2, shs).max() <= TOL_STEP
     assert err_losses(loss[models], rl).max() <= TOL_STEP
     net.train_step(Xd, yd, w.lr)
-    T1, T2 = net.get_params()
+    T1, T2 = net.get_models(models)
     O1, O2, _ = orc.train(shs, sacts, sW1, sW2, X, y, [(0, w.B)], w.lr, rounding="bf16")
-    assert err_rows(T1[rows], O1, shs, w.lr * allow).max() <= TOL_STEP
-    assert err_cols(T2[:, rows], O2, shs).max() <= TOL_STEP
+    assert err_rows(T1, O1, shs, w.lr * allow).max() <= TOL_STEP
+    assert err_cols(T2, O2, shs).max() <= TOL_STEP
     net.close()
 
 

@@ -52,6 +52,11 @@ CASES = {
     "f32_b29_o10": dict(M=25, hmax=200, F=32, O=10, B=29),
     "split": dict(hs=[1300, 513, 512, 1, 700, 3, 1024], F=10, O=2, B=33),   # two-halves segments
     "f1000_b300": dict(M=6, hmax=80, F=1000, O=2, B=300),
+    # the three-piece fused backward with the bias in its four-column tail:
+    # F = 96 (rows of 100 with the bias column) at 256 samples and F = 48
+    # (rows of 52) at 128 samples
+    "x3_f96_b256": dict(M=20, hmax=150, F=96, O=2, B=256),
+    "x3_f48_b128": dict(M=20, hmax=150, F=48, O=2, B=128),
 }
 
 
@@ -122,7 +127,8 @@ def test_hidden_forward_gradients_with_biases(pm, orc, torch, name, precision, p
     net.close()
 
 
-@pytest.mark.parametrize("name", ["f100_b250", "f128_b100_o4", "split"])
+@pytest.mark.parametrize("name", ["f100_b250", "f128_b100_o4", "split", "x3_f96_b256",
+                                  "x3_f48_b128"])
 def test_train_step_updates_biases(pm, orc, torch, name, path):
     hs, acts, F, O, B, X, y = case_inputs(name)
     rates = np.random.default_rng(3).uniform(0.0, 0.2, len(hs)).astype(np.float32)

@@ -1,0 +1,215 @@
+"""GPU parity of packs with two hidden layers per model (Section 7, Figure 3)
+with the oracle's per-model two-layer training.
+
+Bars as for one hidden layer: per-model normwise 1e-5 for one step (dW1 and
+dW12 after the oracle's allowances for kink ties of either layer and for
+the cancellation of G W2), 1e-3 for losses and weights after an epoch.
+Cases span the first layer's kernels (batches of 1 to 300 samples, F from
+3 to 100), second layers whose M3 tiles split a model in two, W12 blocks of
+several 16 x 64 gradient tiles, and every activation.  The oracle counts
+Hardshrink value ties (several correct results); the one-step cases assert
+that they meet none.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import pmlp_workloads as wl
+from conftest import load_golden
+from parity import err_cols, err_logits, err_losses, err_rows
+
+pytestmark = pytest.mark.gpu
+
+TOL_STEP = 1e-5
+TOL_EPOCH = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    torch.cuda.set_device(0)
+    return torch
+
+
+@pytest.fixture(scope="module")
+def pm(torch):
+    import paper_2206_08369_amd as pm
+    pm.load_library()
+    return pm
+
+
+def dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def err_blocks(g, r, h1, h2, allow=None):
+    """Per-model normwise error over the W12 blocks."""
+    g = np.asarray(g, np.float64)
+    r = np.asarray(r, np.float64)
+    d = np.abs(g - r)
+    if allow is not None:
+        d = np.maximum(d - allow, 0.0)
+    ko = np.concatenate([[0], np.cumsum(np.asarray(h1, np.int64) * h2)])
+    return np.array([d[ko[m]:ko[m + 1]].max() / max(np.abs(r[ko[m]:ko[m + 1]]).max(), 1e-300)
+                     for m in range(len(h1))])
+
+
+CASES = {
+    "b1_f3": dict(M=13, hmax=9, F=3, O=2, B=1),
+    "b7_f13_o3": dict(M=26, hmax=40, F=13, O=3, B=7),
+    "b64_f32_o10": dict(M=20, hmax=70, F=32, O=10, B=64),
+    "b200_f100": dict(M=13, hmax=100, F=100, O=2, B=200),
+    "b128_f50": dict(M=26, hmax=130, F=50, O=2, B=128),
+    "b300_f20": dict(M=13, hmax=60, F=20, O=4, B=300),
+}
+
+
+def case_inputs(name):
+    c = CASES[name]
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    h1 = rng.integers(1, c["hmax"] + 1, c["M"]).astype(np.int32)
+    h2 = rng.integers(1, c["hmax"] + 1, c["M"]).astype(np.int32)
+    acts = np.resize(np.arange(13, dtype=np.int32), c["M"])
+    rng.shuffle(acts)
+    X, y = wl.make_dataset(c["F"], c["O"], c["B"], seed=int(rng.integers(1 << 30)))
+    return h1, h2, acts, c["F"], c["O"], c["B"], X, y
+
+
+def test_init_is_bit_exact(pm, orc):
+    h1 = np.array([3, 1, 40, 7], np.int32)
+    h2 = np.array([2, 5, 1, 33], np.int32)
+    net = pm.DeepPackedMLP(9, 3, h1, h2, [0, 1, 2, 3], seed=4040)
+    W1, W12, W2 = net.get_params()
+    R1, R12, R2 = orc.deep_init(9, 3, h1, h2, 4040)
+    assert np.array_equal(W1, R1) and np.array_equal(W12, R12) and np.array_equal(W2, R2)
+    net.close()
+
+
+def test_figure3_example_every_activation(pm, orc, torch):
+    """The 4-1-2-2 and 4-2-3-2 MLPs of Figure 3 packed as one network."""
+    g = load_golden("deep_packing_example.json")
+    h1, h2 = np.asarray(g["h1"], np.int32), np.asarray(g["h2"], np.int32)
+    X, y = wl.make_dataset(g["F"], g["O"], 9, seed=3)
+    Xd, yd = dev(torch, X), dev(torch, y)
+    for act in range(13):
+        acts = np.full(2, act, np.int32)
+        net = pm.DeepPackedMLP(g["F"], g["O"], h1, h2, acts, seed=70 + act)
+        W1, W12, W2 = net.get_params()
+        got = net.forward(Xd).cpu().numpy()
+        assert got.shape == (9, 2, g["O"])
+        assert err_logits(got, orc.deep_forward(h1, h2, acts, W1, W12, W2, X)).max() <= TOL_STEP
+        d1, d12, d2 = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+        r1, r12, r2, rl, a1, a12, ties = orc.deep_gradients(h1, h2, acts, W1, W12, W2, X, y)
+        assert ties.sum() == 0
+        assert err_rows(d1, r1, h1, a1).max() <= TOL_STEP
+        assert err_blocks(d12, r12, h1, h2, a12).max() <= TOL_STEP
+        assert err_cols(d2, r2, h2).max() <= TOL_STEP
+        assert err_losses(net.losses(), rl).max() <= TOL_STEP
+        net.close()
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_forward_and_gradients(pm, orc, torch, name):
+    h1, h2, acts, F, O, B, X, y = case_inputs(name)
+    net = pm.DeepPackedMLP(F, O, h1, h2, acts, seed=81)
+    W1, W12, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    got = net.forward(Xd).cpu().numpy()
+    assert err_logits(got, orc.deep_forward(h1, h2, acts, W1, W12, W2, X)).max() <= TOL_STEP
+    d1, d12, d2 = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+    r1, r12, r2, rl, a1, a12, ties = orc.deep_gradients(h1, h2, acts, W1, W12, W2, X, y)
+    assert ties.sum() == 0
+    assert err_rows(d1, r1, h1, a1).max() <= TOL_STEP
+    assert err_blocks(d12, r12, h1, h2, a12).max() <= TOL_STEP
+    assert err_cols(d2, r2, h2).max() <= TOL_STEP
+    assert err_losses(net.losses(), rl).max() <= TOL_STEP
+    net.close()
+
+
+@pytest.mark.parametrize("name", ["b7_f13_o3", "b200_f100", "b64_f32_o10"])
+def test_train_step(pm, orc, torch, name):
+    h1, h2, acts, F, O, B, X, y = case_inputs(name)
+    lr = 0.05
+    net = pm.DeepPackedMLP(F, O, h1, h2, acts, seed=82)
+    W1, W12, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    g1, g12, g2 = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+    net.train_step(Xd, yd, lr)
+    T1, T12, T2 = net.get_params()
+    # the update is W - lr dW on the same gradients, to fp32 rounding
+    for W, T, G in ((W1, T1, g1), (W12, T12, g12), (W2, T2, g2)):
+        assert np.all(np.abs(T - (W - lr * G)) <= 2 * np.spacing(np.maximum(np.abs(W), np.abs(T))))
+    O1, O12, O2, ol, _ = orc.deep_train(h1, h2, acts, W1, W12, W2, X, y, [(0, B)], lr)
+    r = orc.deep_gradients(h1, h2, acts, W1, W12, W2, X, y)
+    assert err_losses(net.losses(), ol).max() <= TOL_STEP
+    assert err_rows(T1, O1, h1, lr * r[4]).max() <= TOL_STEP
+    assert err_blocks(T12, O12, h1, h2, lr * r[5]).max() <= TOL_STEP
+    assert err_cols(T2, O2, h2).max() <= TOL_STEP
+    net.close()
+
+
+def test_each_model_equals_itself_alone(pm, torch):
+    h1, h2, acts, F, O, B, X, y = case_inputs("b64_f32_o10")
+    net = pm.DeepPackedMLP(F, O, h1, h2, acts, seed=83)
+    W1, W12, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    logits = net.forward(Xd).cpu().numpy()
+    g1, g12, g2 = [t.cpu().numpy() for t in net.gradients(Xd, yd)]
+    o1 = np.concatenate([[0], np.cumsum(h1)])
+    o2 = np.concatenate([[0], np.cumsum(h2)])
+    ko = np.concatenate([[0], np.cumsum(h1.astype(np.int64) * h2)])
+    for m in (0, 9, 19):
+        one = pm.DeepPackedMLP(F, O, h1[m:m + 1], h2[m:m + 1], acts[m:m + 1])
+        one.set_params(W1[o1[m]:o1[m + 1]], W12[ko[m]:ko[m + 1]], W2[:, o2[m]:o2[m + 1]])
+        assert err_logits(one.forward(Xd).cpu().numpy(), logits[:, m:m + 1]).max() <= 1e-6
+        a1, a12, a2 = [t.cpu().numpy() for t in one.gradients(Xd, yd)]
+        assert err_rows(a1, g1[o1[m]:o1[m + 1]], h1[m:m + 1]).max() <= 1e-6
+        assert err_blocks(a12, g12[ko[m]:ko[m + 1]], h1[m:m + 1], h2[m:m + 1]).max() <= 1e-6
+        assert err_cols(a2, g2[:, o2[m]:o2[m + 1]], h2[m:m + 1]).max() <= 1e-6
+        one.close()
+    net.close()
+
+
+def test_one_epoch(pm, orc, torch):
+    """130 models (10 activations x 13 width pairs, widths up to 60), F = 20,
+    B = 64, 2,000 samples (31 batches + 16 samples)."""
+    rng = np.random.default_rng(90)
+    acts = np.repeat(np.arange(10, dtype=np.int32), 13)
+    h1 = rng.integers(1, 61, 130).astype(np.int32)
+    h2 = rng.integers(1, 61, 130).astype(np.int32)
+    X, y = wl.make_dataset(20, 2, 2000, seed=91)
+    net = pm.DeepPackedMLP(20, 2, h1, h2, acts, seed=92)
+    W1, W12, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    batches = wl.batch_bounds(2000, 64)
+    for s, n in batches:
+        net.train_step(Xd[s:s + n], yd[s:s + n], 0.05)
+    R1, R12, R2, rl, _ = orc.deep_train(h1, h2, acts, W1, W12, W2, X, y, batches, 0.05)
+    assert err_losses(net.losses(), rl).max() <= TOL_EPOCH
+    T1, T12, T2 = net.get_params()
+    assert err_rows(T1, R1, h1).max() <= TOL_EPOCH
+    assert err_blocks(T12, R12, h1, h2).max() <= TOL_EPOCH
+    assert err_cols(T2, R2, h2).max() <= TOL_EPOCH
+    net.close()
+
+
+def test_calls_a_deep_pack_does_not_take(pm, torch):
+    net = pm.DeepPackedMLP(4, 2, [1, 2], [2, 3], [0, 1])
+    X = dev(torch, np.ones((4, 4), np.float32))
+    y = dev(torch, np.zeros(4, np.int32))
+    t = torch.empty(64, device="cuda")
+    for call in (lambda: pm.pmlp_gradients(net.handle, X, y, 4, t, t),
+                 lambda: pm.pmlp_hidden(net.handle, X, 4, t, t),
+                 lambda: pm.pmlp_get_params(net.handle),
+                 lambda: pm.pmlp_set_precision(net.handle, pm.PMLP_BF16_GEMM)):
+        with pytest.raises(pm.PmlpError) as e:
+            call()
+        assert e.value.code == pm.PMLP_ESTATE
+    one = pm.PackedMLP(4, 2, [1, 2], [0, 1])
+    with pytest.raises(pm.PmlpError) as e:
+        pm.pmlp_info_deep(one.handle)
+    assert e.value.code == pm.PMLP_ESTATE
+    one.close()
+    net.close()

@@ -3,10 +3,12 @@ rest of the activation list of Section 4.2), mixed with the other ten, on
 both kernel paths and in both precision modes.
 
 Same bars as the other parity tests (per-model normwise 1e-5 for one step,
-1e-3 for losses after one epoch).  Hardshrink jumps by 0.5 at |z| = 0.5: a
-model with a sample whose Z lies within rounding of the jump has several
-correct fp32 results (the oracle counts such ties), so it is left out of the
-comparison; the test checks that this leaves almost every model in.
+1e-3 for losses after one epoch).  Hardshrink jumps by 0.5 at |z| = 0.5: where
+a Z lies within rounding of the jump, either side is a correct fp32 result.
+Every model is compared: the side the GPU took at each (sample, unit) is read
+from its hidden layer and handed to the oracle, which follows it only inside
+the tie band and counts any disagreement outside it (asserted zero), so the
+check covers which side was taken as well as everything downstream of it.
 """
 import zlib
 
@@ -71,12 +73,13 @@ def case_inputs(name):
     return hs, acts, c["F"], c["O"], c["B"], X, y
 
 
-def kept(orc, hs, acts, W1, X, rounding="exact"):
-    ties = orc.value_ties(hs, acts, W1, X, rounding=rounding)
-    keep = ties == 0
-    assert np.all(np.asarray(acts)[~keep] == 11)      # only Hardshrink has a jump
-    assert keep.sum() >= 0.85 * len(hs), ties
-    return keep
+def sides(H):
+    """The side of each (sample, unit) the GPU took: nonzero hidden value."""
+    return H.cpu().numpy() != 0
+
+
+def no_conflicts(orc):
+    assert orc.branch_conflicts() == 0
 
 
 def _net(pm, F, O, hs, acts, seed, precision):
@@ -91,20 +94,24 @@ def test_hidden_forward_gradients(pm, orc, torch, name, precision, path):
     hs, acts, F, O, B, X, y = case_inputs(name)
     net = _net(pm, F, O, hs, acts, 31, precision)
     W1, W2 = net.get_params()
-    keep = kept(orc, hs, acts, W1, X, rnd)
     Xd, yd = dev(torch, X), dev(torch, y)
     Z, H = net.hidden(Xd)
-    RZ, RH = orc.hidden(hs, acts, W1, X, rounding=rnd)
+    br = sides(H)
+    RZ, RH = orc.hidden(hs, acts, W1, X, rounding=rnd, branch=br)
+    no_conflicts(orc)
     assert err_cols(Z.cpu().numpy(), RZ, hs).max() <= TOL_STEP
-    assert err_cols(H.cpu().numpy(), RH, hs)[keep].max() <= TOL_STEP
+    assert err_cols(H.cpu().numpy(), RH, hs).max() <= TOL_STEP
     got = net.forward(Xd).cpu().numpy()
-    assert err_logits(got, orc.forward(hs, acts, W1, W2, X, rounding=rnd))[keep].max() <= TOL_STEP
+    want = orc.forward(hs, acts, W1, W2, X, rounding=rnd, branch=br)
+    no_conflicts(orc)
+    assert err_logits(got, want).max() <= TOL_STEP
     dW1, dW2 = net.gradients(Xd, yd)
     loss = net.losses()
-    r1, r2, rl, allow = orc.gradients(hs, acts, W1, W2, X, y, rounding=rnd)
-    assert err_rows(dW1.cpu().numpy(), r1, hs, allow)[keep].max() <= TOL_STEP
-    assert err_cols(dW2.cpu().numpy(), r2, hs)[keep].max() <= TOL_STEP
-    assert err_losses(loss, rl)[keep].max() <= TOL_STEP
+    r1, r2, rl, allow = orc.gradients(hs, acts, W1, W2, X, y, rounding=rnd, branch=br)
+    no_conflicts(orc)
+    assert err_rows(dW1.cpu().numpy(), r1, hs, allow).max() <= TOL_STEP
+    assert err_cols(dW2.cpu().numpy(), r2, hs).max() <= TOL_STEP
+    assert err_losses(loss, rl).max() <= TOL_STEP
     net.close()
 
 
@@ -113,19 +120,24 @@ def test_train_step_matches_oracle(pm, orc, torch, name, path):
     hs, acts, F, O, B, X, y = case_inputs(name)
     net = _net(pm, F, O, hs, acts, 32, "fp32")
     W1, W2 = net.get_params()
-    keep = kept(orc, hs, acts, W1, X)
-    net.train_step(dev(torch, X), dev(torch, y), 0.05)
+    Xd, yd = dev(torch, X), dev(torch, y)
+    br = sides(net.hidden(Xd)[1])
+    net.train_step(Xd, yd, 0.05)
     T1, T2 = net.get_params()
-    O1, O2, ol = orc.train(hs, acts, W1, W2, X, y, [(0, B)], 0.05)
-    allow = orc.gradients(hs, acts, W1, W2, X, y)[3]   # kink ties move dW1, hence W1'
-    assert err_losses(net.losses(), ol)[keep].max() <= TOL_STEP
-    assert err_rows(T1, O1, hs, 0.05 * allow)[keep].max() <= TOL_STEP
-    assert err_cols(T2, O2, hs)[keep].max() <= TOL_STEP
+    O1, O2, ol = orc.train(hs, acts, W1, W2, X, y, [(0, B)], 0.05, branch=br)
+    no_conflicts(orc)
+    allow = orc.gradients(hs, acts, W1, W2, X, y, branch=br)[3]   # kink ties move dW1, hence W1'
+    assert err_losses(net.losses(), ol).max() <= TOL_STEP
+    assert err_rows(T1, O1, hs, 0.05 * allow).max() <= TOL_STEP
+    assert err_cols(T2, O2, hs).max() <= TOL_STEP
     net.close()
 
 
 def test_one_epoch_all_thirteen_activations(pm, orc, torch, path):
-    """13 activations x widths 1..40, F = 50, B = 128, 5,000 samples."""
+    """13 activations x widths 1..40, F = 50, B = 128, 5,000 samples.  The
+    side of every Hardshrink tie is read from the GPU's hidden layer before
+    each step; the band is wider than in the one-step tests because the
+    weights of the two sides drift apart by rounding over the epoch."""
     hs = np.tile(np.arange(1, 41, dtype=np.int32), 13)
     acts = np.repeat(np.arange(13, dtype=np.int32), 40)
     X, y = wl.make_dataset(50, 2, 5000, 4242)
@@ -133,12 +145,16 @@ def test_one_epoch_all_thirteen_activations(pm, orc, torch, path):
     W1, W2 = net.get_params()
     Xd, yd = dev(torch, X), dev(torch, y)
     batches = wl.batch_bounds(5000, 128)
+    br = np.zeros((5000, int(hs.sum())), bool)
     for s, n in batches:
+        br[s:s + n] = sides(net.hidden(Xd[s:s + n])[1])
         net.train_step(Xd[s:s + n], yd[s:s + n], 0.05)
-    R1, R2, rl, ties = orc.train(hs, acts, W1, W2, X, y, batches, 0.05, return_ties=True)
-    keep = ties == 0           # a tie at any step: the model has several correct paths
-    assert np.all(acts[~keep] == 11) and keep.sum() >= 0.85 * len(hs)
-    assert err_losses(net.losses(), rl)[keep].max() <= TOL_EPOCH
-    T1, _ = net.get_params()
-    assert err_rows(T1, R1, hs)[keep].max() <= TOL_EPOCH
+    R1, R2, rl, ties = orc.train(hs, acts, W1, W2, X, y, batches, 0.05, return_ties=True,
+                                 branch=br, band=1e-4)
+    no_conflicts(orc)
+    assert ties[acts == 11].sum() > 0          # the epoch does meet ties
+    assert err_losses(net.losses(), rl).max() <= TOL_EPOCH
+    T1, T2 = net.get_params()
+    assert err_rows(T1, R1, hs).max() <= TOL_EPOCH
+    assert err_cols(T2, R2, hs).max() <= TOL_EPOCH
     net.close()

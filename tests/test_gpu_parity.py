@@ -353,13 +353,14 @@ def test_full_size_step_on_sampled_models(pm, orc, torch, wname):
     hs, acts = w.model_grid()
     X, y = wl.make_dataset(w.F, w.O, w.B, w.data_seed)
     net = make_net(pm, w.F, w.O, hs, acts, seed=w.init_seed)
-    W1, W2 = net.get_params()
+    models = np.arange(7, w.M, w.M // 12)
+    models = np.unique(np.concatenate([models, [0, 999, w.M - 1]]))
+    sW1, sW2 = net.get_models(models)
+    shs, sacts = hs[models], acts[models]
+    rows = np.concatenate([np.arange(o, o + h) for o, h in zip(offsets(hs)[models], shs)])
     Xd, yd = dev(torch, X), dev(torch, y)
     dW1, dW2 = net.gradients(Xd, yd)
     loss = net.losses()
-    models = np.arange(7, w.M, w.M // 12)
-    models = np.unique(np.concatenate([models, [0, 999, w.M - 1]]))
-    shs, sacts, sW1, sW2, rows = submodel(hs, acts, W1, W2, models)
     rows_t = torch.from_numpy(rows).cuda()
     g1 = dW1.index_select(0, rows_t).cpu().numpy()
     g2 = dW2.index_select(1, rows_t).cpu().numpy()
@@ -371,10 +372,10 @@ def test_full_size_step_on_sampled_models(pm, orc, torch, wname):
     # the fused update path on the same batch
     net.train_step(Xd, yd, w.lr)
     assert err_losses(net.losses()[models], rl).max() <= TOL_STEP
-    T1, T2 = net.get_params()
+    T1, T2 = net.get_models(models)
     O1, O2, _ = orc.train(shs, sacts, sW1, sW2, X, y, [(0, w.B)], w.lr)
-    assert err_rows(T1[rows], O1, shs, w.lr * allow).max() <= TOL_STEP
-    assert err_cols(T2[:, rows], O2, shs).max() <= TOL_STEP
+    assert err_rows(T1, O1, shs, w.lr * allow).max() <= TOL_STEP
+    assert err_cols(T2, O2, shs).max() <= TOL_STEP
     net.close()
 
 
@@ -399,6 +400,42 @@ def test_label_out_of_range_is_reported(pm, torch):
     assert e.value.code == pm.PMLP_EINVAL
     net.train_step(X, dev(torch, np.array([0, 1, 1, 0], np.int32)), 0.1)
     assert np.all(np.isfinite(net.losses()))
+    net.close()
+
+
+def test_get_models_equals_slices_of_get_params(pm):
+    rng = np.random.default_rng(12)
+    hs, acts = wl.random_models(rng, 30, 70)
+    net = make_net(pm, 11, 3, hs, acts, seed=17)
+    W1, W2 = net.get_params()
+    off = offsets(hs)
+    models = np.array([29, 0, 7, 7, 15], np.int32)     # any order, repeats allowed
+    rows = np.concatenate([np.arange(off[m], off[m + 1]) for m in models])
+    a1, a2 = net.get_models(models)
+    assert np.array_equal(a1, W1[rows]) and np.array_equal(a2, W2[:, rows])
+    with pytest.raises(pm.PmlpError) as e:
+        net.get_models([0, 30])
+    assert e.value.code == pm.PMLP_EINVAL
+    net.close()
+
+
+def test_nonfinite_losses_are_counted(pm, torch):
+    """A diverged model (NaN output weights) gives a NaN loss; the library
+    counts it per step while the other models train on unaffected."""
+    hs = np.array([2, 3, 4], np.int32)
+    net = make_net(pm, 3, 2, hs, [0, 1, 2])
+    W1, W2 = net.get_params()
+    W2[:, 2:5] = np.nan                                   # model 1
+    net.set_params(W1, W2)
+    X = dev(torch, np.linspace(-1, 1, 12, dtype=np.float32).reshape(4, 3))
+    y = dev(torch, np.array([0, 1, 1, 0], np.int32))
+    assert net.nonfinite_count() == 0
+    net.train_step(X, y, 0.1)
+    net.train_step(X, y, 0.1)
+    loss = net.losses()
+    assert np.isnan(loss[1]) and np.all(np.isfinite(loss[[0, 2]]))
+    assert net.nonfinite_count() == 2
+    assert net.nonfinite_count() == 0
     net.close()
 
 
