@@ -1,16 +1,21 @@
-"""Benchmark: packed ParallelMLPs SGD training steps on one MI355X.
+"""Benchmark: packed ParallelMLPs SGD training on one MI355X.
 
 One step = one batch through the whole hot path (batch packing, the
-input-layer GEMM, fused activation + M3 forward, per-model softmax
-cross-entropy, M3 backward with the W2 update, and the dW1 GEMM with the
-W1 update).  Inputs are seeded synthetic data shaped like the paper's
+input-layer product, activation + M3 forward, per-model softmax
+cross-entropy, the fused backward with both SGD updates).  Steps run in
+epoch order: contiguous batches of the workload's samples, the last partial
+batch included (Section 4.3 trains whole epochs), starting at an epoch
+boundary.  Inputs are seeded synthetic data shaped like the paper's
 simulated workloads, resident in GPU memory before timing; weights start
 from the library's seeded initialisation.
 
-Prints ONE JSON line with the throughput in model-samples trained per
-second, the roofline position of the dominant kernel (per-kernel times
-from HIP events recorded on the library's stream inside the timed region)
-and the CPU oracle's rate on a bounded sample of the same workload.
+Prints ONE JSON line: whole-window throughput in model-samples trained per
+second, the median over the whole epochs inside the timed window, the
+roofline position of the dominant kernel (per-kernel times from HIP events
+on the library's stream, taken in a separate profiled epoch so the timed
+window runs without them) and the CPU oracle's rate on a bounded sample of
+the same workload.  With --graph each epoch is captured once as a HIP graph
+and replayed (for packs small enough that launch overhead matters).
 """
 from __future__ import annotations
 
@@ -66,37 +71,18 @@ def kernel_work(name, B, F, N, M, O, precision="fp32"):
     return "hbm", 0.0, 0.0
 
 
-LDS_BYTES = 160 * 1024        # per workgroup
+# Matrix-core ceiling of a kernel, by the arithmetic the library reports it
+# ran (PMLP_ARITH_*), in TFLOP/s of the kernel's own (fp32-equivalent) work.
+ARITH_CEILING = {
+    1: PEAK_FP32_MFMA,            # fp32 matrix cores
+    2: PEAK_BF16_MFMA / 6.0,      # six bf16 products of three-piece splits per fp32 product
+    3: PEAK_BF16_MFMA,            # bf16 operands, fp32 accumulation
+}
 
 
-def padded_batch(B):
-    """Batch width of the LDS-resident kernels: 16, 32, 64, 128 or 256."""
-    return next((b for b in (16, 32, 64, 128, 256) if B <= b), None)
-
-
-def three_piece(name, B, F, O):
-    """True where the fp32 path runs the kernel's matrix products as six
-    bf16 products of three-piece operand splits (batches of 128 and 256
-    samples): the input-layer forward when its three LDS planes fit, the
-    fused backward for F4 = 52 or 100 and O = 2."""
-    bp, f4 = padded_batch(B), (F + 3) // 4 * 4
-    if bp not in (128, 256):
-        return False
-    if name == "gemm_fwd":
-        lds = 3 * bp * (f4 // 32) * 64 + bp * ((f4 % 32) // 4) * 16
-        return 32 <= f4 <= 140 and bp * f4 * 4 <= LDS_BYTES and lds <= LDS_BYTES
-    if name == "bwd_fused":
-        return O == 2 and f4 in (52, 100)
-    return False
-
-
-def mfma_peak(name, B, F, O, precision="fp32"):
-    """Matrix-core ceiling of one kernel in TFLOP/s of its own arithmetic:
-    the bf16 peak in the bf16 mode; in the fp32 path the fp32 peak, or a
-    sixth of the bf16 peak where each fp32 multiply-add is six bf16 ones."""
-    if precision == "bf16":
-        return PEAK_BF16_MFMA
-    return PEAK_BF16_MFMA / 6.0 if three_piece(name, B, F, O) else PEAK_FP32_MFMA
+def mfma_peak(arith: int):
+    """Matrix-core ceiling for a PMLP_ARITH_* code, or None (no matrix work)."""
+    return ARITH_CEILING.get(arith)
 
 
 def roofline_bound(bound, nbytes, flops, peak_tflops):
@@ -104,8 +90,8 @@ def roofline_bound(bound, nbytes, flops, peak_tflops):
     intensity (algorithmic flops per algorithmic byte) is above the ridge
     point of its matrix-core ceiling (peak flops / peak HBM bandwidth);
     below it the HBM roofline bounds it."""
-    if bound != "mfma" or not nbytes:
-        return bound
+    if bound != "mfma" or not nbytes or not peak_tflops:
+        return "hbm" if bound == "mfma" else bound
     ridge = peak_tflops * 1e12 / (PEAK_HBM_GBS * 1e9)
     return "mfma" if flops / nbytes >= ridge else "hbm"
 
@@ -196,13 +182,24 @@ def cpu_baseline(w, hs, acts, X, y, seconds_hint: float):
     }
 
 
+def epoch_batches(w):
+    """(offset, length) of every batch of one epoch, the partial one last."""
+    return w.batches()
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=40)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps, in epoch order from an epoch boundary "
+                         "(default: three whole epochs)")
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before (default: one whole epoch)")
     ap.add_argument("--workload", default="w10k_f100", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one epoch as a HIP graph and replay it (timed steps are "
+                         "rounded up to whole epochs)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time of the oracle baseline sample (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -226,13 +223,18 @@ def main(argv=None):
     N, M = int(hs.sum()), w.M
     Xd = torch.from_numpy(X).cuda()
     yd = torch.from_numpy(y).cuda()
-    nfull = w.S // w.B
+    batches = epoch_batches(w)
+    spe = len(batches)
+    steps = args.steps if args.steps is not None else 3 * spe
+    warmup = args.warmup if args.warmup is not None else spe
+    if args.graph:
+        steps = spe * max(1, -(-steps // spe))
     net = pm.PackedMLP(w.F, w.O, hs, acts, seed=w.init_seed,
                        precision=pm.PMLP_BF16_GEMM if args.precision == "bf16" else pm.PMLP_FP32)
 
     def step(k):
-        s = (k % nfull) * w.B
-        net.train_step(Xd[s:s + w.B], yd[s:s + w.B], w.lr)
+        s, n = batches[k % spe]
+        net.train_step(Xd[s:s + n], yd[s:s + n], w.lr)
 
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib * (1 << 20) // 4
@@ -242,38 +244,81 @@ def main(argv=None):
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for k in range(args.warmup):
+    # warm-up ends on an epoch boundary so the timed window starts one
+    warm = -(-warmup // spe) * spe if warmup else 0
+    for k in range(warm):
         step(k)
-    torch.cuda.synchronize()
-    net.profile_reset()
-    net.set_profiling(True)
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(0)                   # one eager step on the capture stream
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, capture_error_mode="thread_local"):
+            for k in range(spe):
+                step(k)
+        torch.cuda.synchronize()
+    samples = [batches[k % spe][1] for k in range(steps)]
+    marks = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(args.warmup + k)
+    start = torch.cuda.Event(enable_timing=True)
+    start.record()
+    if graph is not None:
+        for _ in range(steps // spe):
+            graph.replay()
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record()
+            marks.append(ev)
+    else:
+        for k in range(steps):
+            step(k)
+            if (k + 1) % spe == 0:
+                ev = torch.cuda.Event(enable_timing=True)
+                ev.record()
+                marks.append(ev)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    times = net.kernel_times()
-    net.set_profiling(False)
     losses = net.losses()
     if not np.all(np.isfinite(losses)):
         print("non-finite losses after the timed steps", file=sys.stderr)
         return 1
+    epoch_s = []
+    prev = start
+    for ev in marks:
+        epoch_s.append(prev.elapsed_time(ev) * 1e-3)
+        prev = ev
 
-    ms_per_step = 1e3 * elapsed / args.steps
-    value = M * w.B * args.steps / elapsed
+    # per-kernel times: the full batches of one more epoch, with HIP events
+    # around every launch (the roofline figures are per full-batch launch)
+    net.profile_reset()
+    net.set_profiling(True)
+    for k in range(spe):
+        if batches[k][1] == w.B:
+            step(k)
+    torch.cuda.synchronize()
+    times = net.kernel_times()
+    variants = net.kernel_variants()
+    net.set_profiling(False)
+
+    value = M * float(sum(samples)) / elapsed
+    ms_per_step = 1e3 * elapsed / steps
     kernels = {}
     for name, (ms, n) in times.items():
         if n == 0:
             continue
         bound, nbytes, flops = kernel_work(name, w.B, w.F, N, M, w.O, args.precision)
         avg = ms / n
-        kernels[name] = {"avg_ms": avg, "launches": n,
+        kernels[name] = {"avg_ms": avg, "launches": n, "kernel": variants[name][0],
                          "gbs": nbytes / (avg * 1e-3) / 1e9 if nbytes else None,
                          "tflops": flops / (avg * 1e-3) / 1e12 if flops else None}
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
     bound, nbytes, flops = kernel_work(dom, w.B, w.F, N, M, w.O, args.precision)
-    mpeak = mfma_peak(dom, w.B, w.F, w.O, args.precision)
+    arith = variants[dom][1]
+    mpeak = mfma_peak(arith)
     bound = roofline_bound(bound, nbytes, flops, mpeak)
     avg_s = kernels[dom]["avg_ms"] * 1e-3
     if bound == "mfma":
@@ -283,26 +328,29 @@ def main(argv=None):
         peak, achieved, unit = PEAK_HBM_GBS, nbytes / avg_s / 1e9, "GB/s"
     roofline = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                 "frac": achieved / peak, "traffic": load_traffic(dom, w.name, args.precision),
-                "kernel": dom,
-                # the kernel's matrix-core ceiling in TFLOP/s of fp32 work, which sets
-                # the ridge that chose `bound` (a sixth of the bf16 peak where the
-                # products run as six bf16 products of three-piece splits)
-                "mfma_ceiling": mpeak,
-                "three_piece": args.precision == "fp32" and three_piece(dom, w.B, w.F, w.O)}
+                "kernel": dom, "kernel_name": variants[dom][0],
+                # the matrix-core ceiling (TFLOP/s of the kernel's fp32-equivalent work)
+                # of the arithmetic the library reports the kernel ran; it sets the
+                # ridge that chose `bound`
+                "mfma_ceiling": mpeak, "arith": arith}
 
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(w, hs, acts, X, y, args.cpu_seconds)
 
+    med = float(np.median(epoch_s)) if epoch_s else None
     line = {
         "metric": METRIC, "value": value, "unit": "model-samples/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "steps": steps, "warmup": warm, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32" if args.precision == "fp32" else "bf16-gemm/f32",
         "data": "synthetic (seeded X ~ N(0,1), linear-teacher labels; seeded weight init)",
         "config": {"workload": w.name, "models": M, "hidden_units": N, "F": w.F, "O": w.O,
                    "batch": w.B, "samples": w.S, "hidden_sizes": "%d..%d" % w.sizes,
-                   "activations": len(w.acts)},
+                   "activations": len(w.acts), "steps_per_epoch": spe, "graph": bool(graph)},
+        "epochs": {"count": len(epoch_s), "median_s": med,
+                   "value_median": M * w.S / med if med else None,
+                   "all_s": epoch_s},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
