@@ -205,6 +205,29 @@ int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev,
 int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev,
                        int32_t B, const float* lr_dev);
 
+/* pmlp_train_step for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, but the step's workspaces (the
+ * batch copies, the hidden pre-activations Z [Npad, Bp] and the logits
+ * [M, Bp, O], Bp the padded batch) live in one static 256 MiB device array
+ * per GPU instead of the handle's growable workspace, and the call makes
+ * no hipMalloc, hipFree or event.  The first call on a device looks the
+ * array's device address up (hipGetSymbolAddress) and keeps it.
+ *   - Returns PMLP_EINVAL, before any device work, when those workspaces
+ *     exceed 256 MiB (about Npad * Bp * 4 bytes, e.g. 50,560 units at
+ *     1,024 samples fit, 5,005,056 units at 256 do not), and for the
+ *     arguments pmlp_train_step rejects.
+ *   - PMLP_ESTATE in the PMLP_BF16_GEMM mode (whose bf16 copies the handle
+ *     allocates) and for a PMLP_MSE handle.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents; every part a step reads is written earlier in the
+ *     same step, so nothing needs clearing between calls.  Calls that
+ *     overlap on one GPU (other handles, other streams, other threads)
+ *     race on the array: serialise them.
+ *   - Per-kernel profiling records nothing for this call. */
+int pmlp_train_step_noalloc(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
+                            float lr);
+
 /* Copy the per-model loss (mean cross-entropy, or mean squared error for a
  * PMLP_MSE handle) of the last training or gradient batch into out_host [M]
  * (fp32).  Synchronises the

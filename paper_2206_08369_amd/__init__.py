@@ -25,7 +25,7 @@ __all__ = [
     "pmlp_gradients", "pmlp_hidden", "pmlp_get_params", "pmlp_set_params", "pmlp_info",
     "pmlp_set_profiling", "pmlp_kernel_time", "pmlp_profile_reset", "pmlp_kernel_name",
     "pmlp_last_error", "pmlp_gradients_ex", "pmlp_get_biases", "pmlp_set_biases",
-    "PMLP_MSE", "pmlp_train_step_mse", "pmlp_gradients_mse", "pmlp_nonfinite",
+    "PMLP_MSE", "pmlp_train_step_mse", "pmlp_gradients_mse", "pmlp_nonfinite", "pmlp_train_step_noalloc",
     "pmlp_set_feature_mask", "pmlp_get_models", "pmlp_create_deep", "pmlp_gradients_deep",
     "pmlp_get_params_deep", "pmlp_set_params_deep", "pmlp_info_deep", "pmlp_kernel_variant",
     "PMLP_ARITH_NONE", "PMLP_ARITH_FP32", "PMLP_ARITH_X3", "PMLP_ARITH_BF16", "PackedMLP",
@@ -97,6 +97,7 @@ def load_library():
         "pmlp_kernel_time": [P, i32, C.POINTER(C.c_double), C.POINTER(i64)],
         "pmlp_profile_reset": [P],
         "pmlp_nonfinite": [P, C.POINTER(i32)],
+        "pmlp_train_step_noalloc": [P, P, P, i32, f32],
         "pmlp_set_feature_mask": [P, P],
         "pmlp_get_models": [P, P, i32, P, P],
         "pmlp_create_deep": [C.POINTER(P), i32, i32, i32, P, P, P, u64],
@@ -200,6 +201,11 @@ def pmlp_forward(h: int, X, B: int, logits) -> None:
 def pmlp_train_step(h: int, X, y, B: int, lr: float) -> None:
     _check(load_library().pmlp_train_step(h, _ptr(X), _ptr(y), int(B), float(lr)),
            "pmlp_train_step")
+
+
+def pmlp_train_step_noalloc(h: int, X, y, B: int, lr: float) -> None:
+    _check(load_library().pmlp_train_step_noalloc(h, _ptr(X), _ptr(y), int(B), float(lr)),
+           "pmlp_train_step_noalloc")
 
 
 def pmlp_train_step_lr(h: int, X, y, B: int, lr) -> None:

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -49,6 +50,15 @@ uint64_t splitmix64_host(uint64_t x) {
   return z ^ (z >> 31);
 }
 
+// Workspace of pmlp_train_step_noalloc: one static device array per GPU
+// (every GPU the library runs on holds it until the process ends).  Host
+// code never uses the array's name as an address: the device address comes
+// from hipGetSymbolAddress, once per device, with that device current.
+constexpr size_t kScratchBytes = (size_t)256 << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
 template <class T>
 void dfree(T*& p) {
   if (p) (void)hipFree(p);
@@ -56,6 +66,8 @@ void dfree(T*& p) {
 }
 
 }  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 // The second hidden layer of a pack made by pmlp_create_deep (the first
 // layer is the handle's own plan, W1 and workspaces).
@@ -270,6 +282,47 @@ struct Work {
 };
 
 Work handle_work(const pmlp* h) { return Work{h->Xp, h->Xt, h->Zt, h->LG}; }
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Bytes of the four workspaces of a Bp-sample batch, each 256-byte aligned.
+size_t work_bytes(const pmlp* h, int32_t Bp) {
+  return 2 * align256((size_t)Bp * h->F4 * sizeof(float)) +
+         align256((size_t)h->Npad * Bp * sizeof(float)) +
+         align256((size_t)h->M * Bp * h->O * sizeof(float));
+}
+
+// Device address of the static workspace on the current device `dev`.
+int scratch_base(int dev, unsigned char** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(PMLP_EDEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(PMLP_EDEVICE, std::string("hipGetSymbolAddress of the static workspace failed: ") +
+                                    hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = (unsigned char*)g_scratch_ptr[dev];
+  return PMLP_OK;
+}
+
+// The workspaces of a Bp-sample batch laid out in the static workspace.
+Work carve_work(const pmlp* h, int32_t Bp, unsigned char* base) {
+  Work w{};
+  size_t at = 0;
+  auto take = [&](size_t n) {
+    float* p = (float*)(base + at);
+    at += align256(n);
+    return p;
+  };
+  w.Xp = take((size_t)Bp * h->F4 * sizeof(float));
+  w.Xt = take((size_t)Bp * h->F4 * sizeof(float));
+  w.Zt = take((size_t)h->Npad * Bp * sizeof(float));
+  w.LG = take((size_t)h->M * Bp * h->O * sizeof(float));
+  return w;
+}
 
 // bf16 copies of the batch, allocated on the first bf16-mode call.
 int ensure_workspace_bf16(pmlp* h, int32_t Bp) {
@@ -880,6 +933,33 @@ int pmlp_train_step(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t 
   if (!std::isfinite(lr)) return fail(PMLP_EINVAL, "learning rate is not finite");
   if (h->deep) return step_deep(h, X_dev, y_dev, B, lr, nullptr, nullptr, nullptr);
   return step(h, X_dev, y_dev, B, lr, nullptr, nullptr, nullptr);
+}
+
+int pmlp_train_step_noalloc(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,
+                            float lr) {
+  if (int rc = check_batch(h, X_dev, B)) return rc;
+  if (int rc = one_layer_only(h, "pmlp_train_step_noalloc")) return rc;
+  if (h->mse) return fail(PMLP_ESTATE, "a regression handle trains with pmlp_train_step_mse");
+  if (!y_dev) return fail(PMLP_EINVAL, "null labels");
+  if (!std::isfinite(lr)) return fail(PMLP_EINVAL, "learning rate is not finite");
+  if (bf16_mode(h))
+    return fail(PMLP_ESTATE, "the allocation-free step runs in the PMLP_FP32 mode only");
+  const int32_t Bp = pad_batch(B);
+  const size_t need = work_bytes(h, Bp);
+  if (need > kScratchBytes)
+    return fail(PMLP_EINVAL, "the allocation-free step needs " + std::to_string(need >> 20) +
+                                 " MiB of workspace for this pack and batch; its limit is " +
+                                 std::to_string(kScratchBytes >> 20) + " MiB");
+  if (int rc = use_device(h)) return rc;
+  unsigned char* base = nullptr;
+  if (int rc = scratch_base(h->dev, &base)) return rc;
+  const Work w = carve_work(h, Bp, base);
+  // per-kernel timing would create events; this call records none
+  const bool prof = h->prof;
+  h->prof = false;
+  const int rc = step(h, X_dev, y_dev, B, lr, nullptr, nullptr, nullptr, nullptr, nullptr, &w);
+  h->prof = prof;
+  return rc;
 }
 
 int pmlp_train_step_lr(pmlp_t h, const float* X_dev, const int32_t* y_dev, int32_t B,

@@ -203,7 +203,8 @@ def test_calls_a_deep_pack_does_not_take(pm, torch):
     for call in (lambda: pm.pmlp_gradients(net.handle, X, y, 4, t, t),
                  lambda: pm.pmlp_hidden(net.handle, X, 4, t, t),
                  lambda: pm.pmlp_get_params(net.handle),
-                 lambda: pm.pmlp_set_precision(net.handle, pm.PMLP_BF16_GEMM)):
+                 lambda: pm.pmlp_set_precision(net.handle, pm.PMLP_BF16_GEMM),
+                 lambda: pm.pmlp_train_step_noalloc(net.handle, X, y, 4, 0.1)):
         with pytest.raises(pm.PmlpError) as e:
             call()
         assert e.value.code == pm.PMLP_ESTATE
