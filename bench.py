@@ -200,6 +200,9 @@ def main(argv=None):
     ap.add_argument("--graph", action="store_true",
                     help="capture one epoch as a HIP graph and replay it (timed steps are "
                          "rounded up to whole epochs)")
+    ap.add_argument("--no-partial", action="store_true",
+                    help="leave each epoch's partial last batch out (profiling runs, so that "
+                         "per-kernel averages are those of full-batch launches)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time of the oracle baseline sample (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -224,6 +227,8 @@ def main(argv=None):
     Xd = torch.from_numpy(X).cuda()
     yd = torch.from_numpy(y).cuda()
     batches = epoch_batches(w)
+    if args.no_partial:
+        batches = [b for b in batches if b[1] == w.B]
     spe = len(batches)
     steps = args.steps if args.steps is not None else 3 * spe
     warmup = args.warmup if args.warmup is not None else spe
@@ -257,7 +262,7 @@ def main(argv=None):
             step(0)                   # one eager step on the capture stream
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
-        with torch.cuda.graph(graph, capture_error_mode="thread_local"):
+        with torch.cuda.graph(graph, capture_error_mode="relaxed"):
             for k in range(spe):
                 step(k)
         torch.cuda.synchronize()
@@ -347,9 +352,10 @@ def main(argv=None):
         "data": "synthetic (seeded X ~ N(0,1), linear-teacher labels; seeded weight init)",
         "config": {"workload": w.name, "models": M, "hidden_units": N, "F": w.F, "O": w.O,
                    "batch": w.B, "samples": w.S, "hidden_sizes": "%d..%d" % w.sizes,
-                   "activations": len(w.acts), "steps_per_epoch": spe, "graph": bool(graph)},
+                   "activations": len(w.acts), "steps_per_epoch": spe, "graph": bool(graph),
+                   "partial_batches": not args.no_partial},
         "epochs": {"count": len(epoch_s), "median_s": med,
-                   "value_median": M * w.S / med if med else None,
+                   "value_median": M * sum(n for _, n in batches) / med if med else None,
                    "all_s": epoch_s},
         "roofline": roofline,
         "cpu_baseline": cpu,

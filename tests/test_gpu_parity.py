@@ -419,6 +419,42 @@ def test_get_models_equals_slices_of_get_params(pm):
     net.close()
 
 
+# (F, O, B, generic, precision) -> the kernels the library reports for the
+# forward product and the fused backward, and their arithmetic
+VARIANTS = [
+    ((100, 2, 256, False, "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
+    ((50, 2, 128, False, "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
+    ((32, 10, 32, False, "fp32"), ("k_fwd_lds_ring", 1), ("k_bwd_mf", 1)),
+    ((20, 2, 100, False, "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
+    ((100, 2, 256, True, "fp32"), ("k_gemm_nt", 1), None),
+    ((100, 2, 256, False, "bf16"), ("k_gemm_bf", 3), None),
+]
+
+
+@pytest.mark.parametrize("shape,fwd,bwd", VARIANTS)
+def test_kernel_variants_are_reported(pm, torch, monkeypatch, shape, fwd, bwd):
+    F, O, B, generic, precision = shape
+    if generic:
+        monkeypatch.setenv("PMLP_GENERIC_KERNELS", "1")
+    else:
+        monkeypatch.delenv("PMLP_GENERIC_KERNELS", raising=False)
+    rng = np.random.default_rng(1)
+    hs, acts = wl.random_models(rng, 20, 60)
+    net = make_net(pm, F, O, hs, acts, seed=3)
+    if precision == "bf16":
+        net.set_precision(pm.PMLP_BF16_GEMM)
+    X, y = wl.make_dataset(F, O, B, seed=2)
+    net.train_step(dev(torch, X), dev(torch, y), 0.01)
+    v = net.kernel_variants()
+    assert v["gemm_fwd"] == fwd
+    if bwd is not None:
+        assert v["bwd_fused"] == bwd
+    else:
+        assert v["gemm_bwd"] == fwd and v["m3_bwd"] == ("k_m3_bwd", 0)
+    assert v["ce"] == ("k_ce", 0)
+    net.close()
+
+
 def test_nonfinite_losses_are_counted(pm, torch):
     """A diverged model (NaN output weights) gives a NaN loss; the library
     counts it per step while the other models train on unaffected."""
