@@ -56,6 +56,9 @@ def kernel_work(name, B, F, N, M, O, precision="fp32"):
     if name == "gemm_bwd":       # W1 -= lr dZ^T X: read dZ, X; read+write W1 (+ its bf16 copy)
         return ("mfma", (2.0 if bf else f4) * N * B + fx * B * F + 2 * f4 * N * F
                 + (2.0 * N * F if bf else 0.0), 2.0 * B * F * N)
+    if name == "fwd_m3":         # one kernel: read W1, X, W2; write Z and the logits
+        return ("mfma", f4 * (N * F + B * F + N * B + O * N + B * M * O),
+                2.0 * B * F * N + 2.0 * B * O * N)
     if name == "m3_fwd":         # read Z, W2; write logits
         return "hbm", f4 * (N * B + O * N + B * M * O), 2.0 * B * O * N
     if name == "m3_bwd":         # read Z, G, W2; write dZ (bf16 in bf16 mode), W2
@@ -119,7 +122,8 @@ def load_traffic(kernel: str, workload: str, precision: str = "fp32"):
 # Source file that defines each timed kernel, per precision mode (the shared
 # headers are hashed with it).
 KERNEL_SOURCE = {
-    "fp32": {"gemm_fwd": "k_lds.hip", "bwd_fused": "k_lds.hip", "gemm_bwd": "k_gemm.hip",
+    "fp32": {"gemm_fwd": "k_lds.hip", "fwd_m3": "k_lds.hip", "bwd_fused": "k_lds.hip",
+             "gemm_bwd": "k_gemm.hip",
              "m3_fwd": "k_m3.hip", "m3_bwd": "k_m3.hip", "ce": "k_misc.hip",
              "pack_x": "k_misc.hip", "aux": "k_misc.hip"},
     "bf16": {"gemm_fwd": "k_gemm_bf16.hip", "gemm_bwd": "k_gemm_bf16.hip",

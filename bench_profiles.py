@@ -49,7 +49,8 @@ def agent(outdir: str):
 # kernel (template base name) -> bench.py role
 ROLE = {
     "k_pack_x": "pack_x", "k_pack_x_bf16": "pack_x", "k_fwd_lds": "gemm_fwd",
-    "k_fwd_lds_ring": "gemm_fwd", "k_fwd_x3": "gemm_fwd", "k_m3_fwd": "m3_fwd",
+    "k_fwd_lds_ring": "gemm_fwd", "k_fwd_x3": "gemm_fwd", "k_fwd_x3m": "fwd_m3",
+    "k_m3_fwd": "m3_fwd",
     "k_m3_fwd_mf": "m3_fwd", "k_ce": "ce", "k_mse": "ce", "k_fill": "aux",
     "k_bwd_lds": "bwd_fused", "k_bwd_x3": "bwd_fused", "k_bwd_mf": "bwd_fused",
     "k_m3_bwd": "m3_bwd", "k_w1_to_bf16": "aux",

@@ -323,7 +323,7 @@ int pmlp_info(pmlp_t h, int64_t* N, int32_t* M, int32_t* F, int32_t* O);
  * PMLP_NUM_KERNELS-1, names from pmlp_kernel_name), the summed duration
  * in milliseconds and the number of launches since the last reset;
  * pmlp_profile_reset clears the totals. */
-#define PMLP_NUM_KERNELS 10
+#define PMLP_NUM_KERNELS 11
 int pmlp_set_profiling(pmlp_t h, int32_t enable);
 int pmlp_kernel_time(pmlp_t h, int32_t k, double* total_ms, int64_t* launches);
 int pmlp_profile_reset(pmlp_t h);

@@ -41,7 +41,7 @@ PMLP_FP32 = 0
 PMLP_BF16_GEMM = 1
 PMLP_BIAS = 1
 PMLP_MSE = 2
-PMLP_NUM_KERNELS = 10
+PMLP_NUM_KERNELS = 11
 
 ACT_IDS = {
     "identity": 0, "relu": 1, "tanh": 2, "sigmoid": 3, "elu": 4, "leaky_relu": 5,

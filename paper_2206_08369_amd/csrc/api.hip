@@ -41,7 +41,7 @@ static_assert(KID_COUNT == PMLP_NUM_KERNELS, "kernel id table");
 
 const char* const kKernelNames[KID_COUNT] = {
     "pack_x", "gemm_fwd", "act", "m3_fwd", "ce", "m3_bwd", "gemm_bwd", "aux", "bwd_fused",
-    "hidden2"};
+    "hidden2", "fwd_m3"};
 
 uint64_t splitmix64_host(uint64_t x) {
   uint64_t z = x + 0x9E3779B97F4A7C15ull;
@@ -139,6 +139,9 @@ struct pmlp {
   bool have_loss = false;
   bool mse = false;         // regression head (PMLP_MSE)
   bool lds_kernels = true;  // persistent LDS-resident GEMMs where they apply
+  // the forward product with activation and M3 in one kernel (opt-in: on
+  // the 10,000-model shapes the two-kernel forward measures faster)
+  bool fused_forward = false;
 
   bool prof = false;
   struct Pending {
@@ -458,6 +461,48 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp, const Work& w
   return run(h, KID_GEMM_FWD, [&] { return launch_gemm(g, EPI_STORE, h->stream); });
 }
 
+// Whether the forward runs as one kernel: the input-to-hidden product with
+// the activation and the M3 forward in its epilogue.
+bool forward_fused(const pmlp* h, int32_t Bp) {
+  return h->lds_kernels && h->fused_forward && !bf16_mode(h) && !h->deep &&
+         fwd_m3_supported(Bp, h->F4, h->O);
+}
+
+// Batch copy and the whole forward of Section 3 (steps 1-4) in one kernel:
+// Zt and the logits out[m*sm + b*sb + o] (cleared first where the halves
+// of a wide segment add atomically).
+int forward_m3(pmlp* h, const float* X, int32_t B, int32_t Bp, const Work& w, float* out,
+               int64_t sm, int64_t sb, int64_t nout) {
+  if (int rc = run(h, KID_PACK_X, [&] {
+        return launch_pack_x(X, B, h->F, Bp, h->F4, h->bcol, w.Xp, w.Xt, h->stream);
+      }))
+    return rc;
+  if (h->has_split) {
+    if (int rc = run(h, KID_AUX, [&] { return launch_fill(out, nout, 0.f, h->stream); })) return rc;
+  }
+  FwdM3Args f{};
+  f.W1 = h->W1;
+  f.Xp = w.Xp;
+  f.Zt = w.Zt;
+  f.N = h->N;
+  f.Bp = Bp;
+  f.K = h->F4;
+  f.B = B;
+  f.O = h->O;
+  f.W2 = h->W2;
+  f.ldw = h->Npad;
+  f.seg_off = h->d_seg_off;
+  f.act = h->d_act;
+  f.tiles = h->d_tiles;
+  f.order = h->d_order;
+  f.ntiles = h->ntiles;
+  f.b2 = h->b2;
+  f.out = out;
+  f.sm = sm;
+  f.sb = sb;
+  return run(h, KID_FWD_M3, [&] { return launch_fwd_m3(f, h->stream); });
+}
+
 // Full step: forward, loss, backward and either the SGD update (dW1 and
 // dW2 null) or gradient stores.
 // With `work` set, the step runs in those workspaces (sized for the batch by
@@ -471,21 +516,27 @@ int step(pmlp* h, const float* X, const void* y, int32_t B, float lr, const floa
   if (!work)
     if (int rc = ensure_workspace(h, Bp)) return rc;
   const Work w = work ? *work : handle_work(h);
-  if (int rc = forward_hidden(h, X, B, Bp, w)) return rc;
-  // an fp32-mode update leaves the bf16 copy of W1 behind
-  if (!bf16_mode(h) && !dW1) h->w1b_valid = false;
-  if (h->has_split) {
-    if (int rc = run(h, KID_AUX, [&] {
-          return launch_fill(w.LG, (int64_t)h->M * Bp * h->O, 0.f, h->stream);
+  if (forward_fused(h, Bp)) {
+    if (int rc = forward_m3(h, X, B, Bp, w, w.LG, (int64_t)Bp * h->O, h->O,
+                            (int64_t)h->M * Bp * h->O))
+      return rc;
+  } else {
+    if (int rc = forward_hidden(h, X, B, Bp, w)) return rc;
+    if (h->has_split) {
+      if (int rc = run(h, KID_AUX, [&] {
+            return launch_fill(w.LG, (int64_t)h->M * Bp * h->O, 0.f, h->stream);
+          }))
+        return rc;
+    }
+    if (int rc = run(h, KID_M3_FWD, [&] {
+          return launch_m3_fwd(w.Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act,
+                               h->d_tiles, h->d_order, h->ntiles, h->b2, w.LG, (int64_t)Bp * h->O,
+                               h->O, h->stream);
         }))
       return rc;
   }
-  if (int rc = run(h, KID_M3_FWD, [&] {
-        return launch_m3_fwd(w.Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act,
-                             h->d_tiles, h->d_order, h->ntiles, h->b2, w.LG, (int64_t)Bp * h->O, h->O,
-                             h->stream);
-      }))
-    return rc;
+  // an fp32-mode update leaves the bf16 copy of W1 behind
+  if (!bf16_mode(h) && !dW1) h->w1b_valid = false;
   if (int rc = run(h, KID_CE, [&] {
         // output biases: updated here (db2 = sum_b G), or their gradient stored
         float* b2 = dW1 ? (db2 ? h->b2 : nullptr) : h->b2;
@@ -775,6 +826,7 @@ int pmlp_create_ex(pmlp_t* out, int32_t F, int32_t O, int32_t M, const int32_t* 
   h->N = N;
   h->Npad = (N + 63) / 64 * 64;
   if (const char* env = getenv("PMLP_GENERIC_KERNELS")) h->lds_kernels = env[0] == '0';
+  if (const char* env = getenv("PMLP_FUSED_FORWARD")) h->fused_forward = env[0] == '1';
   h->hs.assign(hidden_sizes, hidden_sizes + M);
   h->acts.assign(act_ids, act_ids + M);
   h->seg_off.resize((size_t)M + 1);
@@ -913,6 +965,9 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
                            (int64_t)h->M * h->O, h->stream);
     });
   }
+  if (forward_fused(h, Bp))
+    return forward_m3(h, X_dev, B, Bp, handle_work(h), logits_dev, h->O, (int64_t)h->M * h->O,
+                      (int64_t)B * h->M * h->O);
   if (int rc = forward_hidden(h, X_dev, B, Bp, handle_work(h))) return rc;
   if (h->has_split) {
     if (int rc = run(h, KID_AUX, [&] {

@@ -1,5 +1,7 @@
 // Persistent LDS-resident GEMMs: forward and fused backward.
 
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace pmlpk {
@@ -310,6 +312,20 @@ __device__ __forceinline__ f32x4 mfma_x3(const bf16x8& a0, const bf16x8& a1, con
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc, 0, 0, 0);
 }
 
+// Product k (0..5) of mfma_x3, in the same order.
+__device__ __forceinline__ f32x4 mfma_x3_step(int k, const bf16x8& a0, const bf16x8& a1,
+                                              const bf16x8& a2, const bf16x8& b0,
+                                              const bf16x8& b1, const bf16x8& b2, f32x4 acc) {
+  switch (k) {
+    case 0: return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b0, acc, 0, 0, 0);
+    case 1: return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc, 0, 0, 0);
+    case 2: return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b2, acc, 0, 0, 0);
+    case 3: return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b0, acc, 0, 0, 0);
+    case 4: return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b1, acc, 0, 0, 0);
+    default: return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc, 0, 0, 0);
+  }
+}
+
 template <int NC, int U, int RM>
 struct X3Strip {
   f32x4 c[U][2 * NC];
@@ -450,6 +466,291 @@ __global__ __launch_bounds__(kLdsBlock) void k_fwd_x3(FwdLdsArgs a) {
 #pragma unroll
       for (int s = 0; s < RM; ++s) wt[u][s] = nxt.t[u][s];
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The forward product with the activation and the M3 forward in its
+// epilogue (Section 3, steps 1-4 in one pass; the closing suggestion of
+// Section 5, a kernel specialised for the packed forward).  The products are
+// those of k_fwd_x3 with the operand roles swapped, so that lane (li, lk)
+// ends a 16-sample block i holding Z of the four consecutive units
+// base + 4lk .. +3 for the one sample 16i + li: the sum over a model's units
+// is then mostly a sum over the lane's own registers.  Z is still stored
+// (the fused backward reads it).
+//
+// Work units are the runs of the M3 plan (whole segments up to the tile
+// cap, or one half of a wider segment), taken widest first.  A wave walks
+// each model's piece of its run in 16-unit blocks that start at the
+// piece's first unit, so every block holds units of one model only (the
+// last block of a piece computes, but neither stores nor sums, the units
+// past it; at most 15 wasted rows per piece).  Per lane and 16-sample block
+// a running sum per output carries the piece across blocks; at the piece's
+// last block it is combined over the four lk lanes and written once: plain
+// stores for whole segments, two atomic additions onto zeroed logits for
+// the halves of a wider one, so the result does not depend on the
+// schedule.
+//
+// A block runs in parts of two 16-sample blocks, and the epilogue of each
+// part (Z store, activation, products with W2) is spread one unit at a time
+// between the matrix products of the next part, so the wave's vector work
+// issues while its products run.  The activation is resolved once per
+// block.  One 16-unit block per step keeps the strip, the running sums and
+// the M3 weights within 256 VGPRs (two waves per SIMD).
+// ---------------------------------------------------------------------------
+
+struct X3MStrip {
+  f32x4 c[2 * kKCMax / 2];
+  float t[kX3RemMax];
+};
+
+// W1 row base + li, k = 32c + 8lk .. +7 per chunk and the remainder values
+// k = 32NC + 4s + lk (rows past N clamp to the last unit; steps past rem
+// repeat step 0).
+template <int NC, int RM>
+__device__ __forceinline__ void x3m_load(X3MStrip& st, const float* __restrict__ W1,
+                                         int64_t base, int64_t N, int K, int rem, int li,
+                                         int lk) {
+  int64_t p = base + li;
+  if (p > N - 1) p = N - 1;
+  const float* row = W1 + p * K;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    st.c[2 * c] = *(const f32x4*)(row + 32 * c + 8 * lk);
+    st.c[2 * c + 1] = *(const f32x4*)(row + 32 * c + 8 * lk + 4);
+  }
+#pragma unroll
+  for (int s = 0; s < RM; ++s) {
+    int off = 32 * NC + 4 * (s < rem ? s : 0) + lk;
+    if (off > K - 1) off = K - 1;
+    st.t[s] = row[off];
+  }
+}
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), in order.
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (N > 0) {
+    static_for<N - 1>(f);
+    f(std::integral_constant<int, N - 1>{});
+  }
+}
+
+template <int TQ, int NC, int RM, int OM>
+__global__ __launch_bounds__(kLdsBlock) void k_fwd_x3m(FwdM3Args a) {
+  extern __shared__ float lds[];
+  const int K = a.K;
+  const int rem = RM < kX3RemMax ? RM : (K - 32 * NC) >> 2;
+  constexpr int PS = TQ * NC * 64;  // 16-byte slots per plane
+  constexpr int BP = 16 * TQ;       // the padded batch (the launcher checks)
+  bf16x8* planes = (bf16x8*)lds;
+  for (int slot = threadIdx.x; slot < PS; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / NC, c = rest - (rest / NC) * NC;
+    const float* src = a.Xp + (int64_t)(16 * i + (l & 15)) * K + 32 * c + 8 * (l >> 4);
+    bf16x8 p0, p1, p2;
+    split3(*(const f32x4*)src, *(const f32x4*)(src + 4), p0, p1, p2);
+    planes[slot] = p0;
+    planes[PS + slot] = p1;
+    planes[2 * PS + slot] = p2;
+  }
+  constexpr int T0 = 3 * PS * 4;
+  const int rdiv = rem > 0 ? rem : 1;
+  for (int slot = threadIdx.x; slot < TQ * rem * 64; slot += kLdsBlock) {
+    const int l = slot & 63, rest = slot >> 6;
+    const int i = rest / rdiv, s = rest - (rest / rdiv) * rdiv;
+    lds[T0 + slot] = a.Xp[(int64_t)(16 * i + (l & 15)) * K + 32 * NC + 4 * s + (l >> 4)];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int li = lane & 15, lk = lane >> 4;
+  const int rstride = gridDim.x * kLdsWaves;
+  int r = blockIdx.x * kLdsWaves + wave;
+  if (r >= a.ntiles) return;
+  const bf16x8* xq = planes + lane;
+  const float* qtail = lds + T0 + lane;
+
+  // run r: units [n0, n0 + len) of tile order[r]
+  Tile3 run = a.tiles[__builtin_amdgcn_readfirstlane(a.order[r])];
+  int64_t base = run.n0;
+  int m = run.m0;  // model of the block's units
+  X3MStrip nxt;
+  x3m_load<NC, RM>(nxt, a.W1, base, a.N, K, rem, li, lk);
+  bf16x8 w0[NC], w1[NC], w2p[NC];
+  float wt[RM > 0 ? RM : 1];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) split3(nxt.c[2 * c], nxt.c[2 * c + 1], w0[c], w1[c], w2p[c]);
+#pragma unroll
+  for (int s = 0; s < RM; ++s) wt[s] = nxt.t[s];
+  float macc[TQ][OM];  // running sums of the open piece, sample 16i + li
+#pragma unroll
+  for (int i = 0; i < TQ; ++i)
+#pragma unroll
+    for (int o = 0; o < OM; ++o) macc[i][o] = 0.f;
+  while (true) {
+    const int64_t rend = run.n0 + run.len;
+    int64_t pend = a.seg_off[m + 1];  // end of model m's piece of the run
+    if (pend > rend) pend = rend;
+    const int64_t bend = base + 16 < pend ? base + 16 : pend;
+    const bool last = bend == pend;
+    // the next block: in this piece, the next model's piece of this run,
+    // or the first block of the wave's next run
+    int rn = r, mn = m;
+    int64_t bn;
+    Tile3 nrun = run;
+    if (!last) {
+      bn = base + 16;
+    } else if (pend < rend) {
+      bn = pend;
+      mn = m + 1;
+    } else {
+      rn = r + rstride;
+      bn = -1;
+      if (rn < a.ntiles) {
+        nrun = a.tiles[__builtin_amdgcn_readfirstlane(a.order[rn])];
+        bn = nrun.n0;
+        mn = nrun.m0;
+      }
+    }
+    x3m_load<NC, RM>(nxt, a.W1, bn >= 0 ? bn : base, a.N, K, rem, li, lk);
+    // the lane's four units and their output weights; units past the
+    // piece get zero weights and are neither stored nor activated
+    const int64_t u0 = base + 4 * lk;
+    bool in[4];
+    float w2v[OM][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      in[q] = u0 + q < bend;
+      int64_t u = u0 + q;
+      if (u > a.N - 1) u = a.N - 1;
+#pragma unroll
+      for (int o = 0; o < OM; ++o) {
+        const float w = o < a.O ? a.W2[(int64_t)o * a.ldw + u] : 0.f;
+        w2v[o][q] = in[q] ? w : 0.f;
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    float* zp = a.Zt + u0 * (int64_t)BP + li;
+    bf16x8 xn0 = xq[0], xn1 = xq[PS], xn2 = xq[2 * PS];
+    // The block in parts of TP sample blocks; the epilogue of part P - 1
+    // goes between the products of part P, that of the last part after them.
+    auto blk = [&](auto ac) __attribute__((always_inline)) {
+      constexpr int A = decltype(ac)::value;
+      constexpr int TP = 2;           // sample blocks per part
+      constexpr int S = TP * 6 * NC;  // bf16 product slots per part
+      constexpr int E = 4 * TP;       // epilogue units per part
+      f32x4 acc[2][TP];
+      // unit e of the epilogue of part P (sample block P TP + e/4, unit e%4)
+      auto epi = [&](auto pc, int e) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
+        const int j = e >> 2, q = e & 3, i = P * TP + j;
+        const float z = acc[P & 1][j][q];
+        if (in[q]) zp[q * BP + 16 * i] = z;
+        const float h = in[q] ? act_fwd(A, z) : 0.f;
+#pragma unroll
+        for (int o = 0; o < OM; ++o) macc[i][o] = fmaf(h, w2v[o][q], macc[i][o]);
+      };
+      auto step = [&](auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
+#pragma unroll
+        for (int j = 0; j < TP; ++j) {
+          const int i = P * TP + j;
+          f32x4 c4 = f32x4{0.f, 0.f, 0.f, 0.f};
+          float qt[RM > 0 ? RM : 1];
+          if (rem > 0) {
+#pragma unroll
+            for (int s = 0; s < RM; ++s) qt[s] = qtail[(i * rem + (s < rem ? s : rem - 1)) * 64];
+          }
+#pragma unroll
+          for (int c = 0; c < NC; ++c) {
+            const bf16x8 x0 = xn0, x1 = xn1, x2 = xn2;
+            if (i * NC + c + 1 < TQ * NC) {
+              const int o = (i * NC + c + 1) * 64;
+              xn0 = xq[o];
+              xn1 = xq[PS + o];
+              xn2 = xq[2 * PS + o];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int k = 0; k < 6; ++k) {
+              c4 = mfma_x3_step(k, w0[c], w1[c], w2p[c], x0, x1, x2, c4);
+              if constexpr (P > 0) {
+                const int slot = (j * NC + c) * 6 + k;
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                  if (e * S / E == slot) epi(std::integral_constant<int, P - 1>{}, e);
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+#pragma unroll
+          for (int s = 0; s < RM; ++s)
+            if (s < rem) c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(wt[s], qt[s], c4, 0, 0, 0);
+          acc[P & 1][j] = c4;
+        }
+      };
+      static_for<TQ / TP>(step);
+#pragma unroll
+      for (int e = 0; e < E; ++e) epi(std::integral_constant<int, TQ / TP - 1>{}, e);
+    };
+    switch (a.act[m]) {
+      case 0: blk(std::integral_constant<int, 0>{}); break;
+      case 1: blk(std::integral_constant<int, 1>{}); break;
+      case 2: blk(std::integral_constant<int, 2>{}); break;
+      case 3: blk(std::integral_constant<int, 3>{}); break;
+      case 4: blk(std::integral_constant<int, 4>{}); break;
+      case 5: blk(std::integral_constant<int, 5>{}); break;
+      case 6: blk(std::integral_constant<int, 6>{}); break;
+      case 7: blk(std::integral_constant<int, 7>{}); break;
+      case 8: blk(std::integral_constant<int, 8>{}); break;
+      case 9: blk(std::integral_constant<int, 9>{}); break;
+      case 10: blk(std::integral_constant<int, 10>{}); break;
+      case 11: blk(std::integral_constant<int, 11>{}); break;
+      default: blk(std::integral_constant<int, 12>{}); break;
+    }
+    if (last) {
+      // model m's piece ends here: combine the four lk lanes and write each
+      // sample's logits once
+      const bool with_b2 = a.b2 && a.seg_off[m] >= run.n0;
+      // one lane address; the sample blocks step by a wave-uniform stride
+      float* const dst0 = a.out + (int64_t)m * a.sm + (int64_t)li * a.sb;
+#pragma unroll
+      for (int i = 0; i < TQ; ++i) {
+        float v[OM];
+#pragma unroll
+        for (int o = 0; o < OM; ++o) {
+          v[o] = macc[i][o];
+          v[o] += __shfl_xor(v[o], 16);
+          v[o] += __shfl_xor(v[o], 32);
+          macc[i][o] = 0.f;
+        }
+        const int b = 16 * i + li;
+        if (lk == 0 && b < a.B) {
+          float* dst = dst0 + (int64_t)(16 * i) * a.sb;
+#pragma unroll
+          for (int o = 0; o < OM; ++o)
+            if (o < a.O) {
+              const float val = v[o] + (with_b2 ? a.b2[(int64_t)m * a.O + o] : 0.f);
+              if (run.atomic) atomicAdd(dst + o, val);
+              else dst[o] = val;
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (bn < 0) break;
+    if (rn != r) {
+      r = rn;
+      run = nrun;
+    }
+    m = mn;
+    base = bn;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) split3(nxt.c[2 * c], nxt.c[2 * c + 1], w0[c], w1[c], w2p[c]);
+#pragma unroll
+    for (int s = 0; s < RM; ++s) wt[s] = nxt.t[s];
   }
 }
 
@@ -1270,6 +1571,49 @@ hipError_t launch_fwd_lds(const FwdLdsArgs& a0, hipStream_t s) {
     case 64: return fwd_lds_go<4>(a, lds, T, s);
     case 128: return fwd_lds_go<8>(a, lds, T, s);
     default: return fwd_lds_go<16>(a, lds, T, s);
+  }
+}
+
+// The forward with the M3 epilogue: batches of 128 and 256 samples, the
+// three planes of k_fwd_x3 in LDS, O <= 2.
+bool fwd_m3_supported(int32_t Bp, int32_t F4, int32_t O) {
+  if ((Bp != 128 && Bp != 256) || O > 2 || F4 < 32) return false;
+  const int nc = F4 / 32;
+  if (nc < 1 || nc > (Bp == 128 ? 4 : 3)) return false;
+  // with more than one fp32 remainder step the wider instances would spill
+  // registers (two or more chunks at 256 samples, four at 128); those
+  // shapes take the two-kernel forward
+  if ((F4 % 32) / 4 > 1 && (Bp == 256 ? nc >= 2 : nc >= 4)) return false;
+  return fwd_x3_bytes(Bp, F4) <= (size_t)dev_info().lds_max;
+}
+
+template <int TQ, int NC>
+static hipError_t fwd_m3_go(const FwdM3Args& a, hipStream_t s) {
+  const size_t lds = fwd_x3_bytes(a.Bp, a.K);
+  note_variant("k_fwd_x3m", kArithX3);
+  switch ((a.K % 32) / 4) {
+    case 0: return launch_persistent(k_fwd_x3m<TQ, NC, 0, 2>, kLdsBlock, lds, a.ntiles, s, a);
+    case 1: return launch_persistent(k_fwd_x3m<TQ, NC, 1, 2>, kLdsBlock, lds, a.ntiles, s, a);
+    default:
+      return launch_persistent(k_fwd_x3m<TQ, NC, kX3RemMax, 2>, kLdsBlock, lds, a.ntiles, s, a);
+  }
+}
+
+hipError_t launch_fwd_m3(const FwdM3Args& a, hipStream_t s) {
+  if (a.N <= 0 || a.ntiles <= 0) return hipSuccess;
+  if (!fwd_m3_supported(a.Bp, a.K, a.O)) return hipErrorInvalidValue;
+  if (a.Bp == 128) {
+    switch (a.K / 32) {
+      case 1: return fwd_m3_go<8, 1>(a, s);
+      case 2: return fwd_m3_go<8, 2>(a, s);
+      case 3: return fwd_m3_go<8, 3>(a, s);
+      default: return fwd_m3_go<8, 4>(a, s);
+    }
+  }
+  switch (a.K / 32) {
+    case 1: return fwd_m3_go<16, 1>(a, s);
+    case 2: return fwd_m3_go<16, 2>(a, s);
+    default: return fwd_m3_go<16, 3>(a, s);
   }
 }
 

@@ -31,7 +31,8 @@ enum KernelId {
   KID_AUX = 7,
   KID_BWD_FUSED = 8,  // fused backward (M3 backward + dW1 GEMM + updates)
   KID_DEEP = 9,       // the hidden-to-hidden layer of two-layer packs
-  KID_COUNT = 10
+  KID_FWD_M3 = 10,    // forward product with the activation and M3 in its epilogue
+  KID_COUNT = 11
 };
 
 // The kernel a launcher chose and the arithmetic of its matrix products
@@ -120,6 +121,31 @@ struct FwdLdsArgs {
 };
 bool fwd_lds_supported(int32_t Bp, int32_t F4);
 hipError_t launch_fwd_lds(const FwdLdsArgs& a, hipStream_t s);
+
+// The forward product with the activation and the M3 forward in its
+// epilogue: Zt as launch_fwd_lds, and the logits of every model,
+//   out[m*sm + b*sb + o] = sum_{n in model m} act_m(Zt[n][b]) W2[o][n] (+ b2[m][o]),
+// written per run of the M3 plan (plain stores; the halves of a split
+// segment add atomically onto zeroed logits).  Bp in {128, 256}, O <= 2.
+struct FwdM3Args {
+  const float* W1;  // [Npad][K]
+  const float* Xp;  // [Bp][K]
+  float* Zt;        // [Npad][Bp]
+  int64_t N;
+  int32_t Bp, K, B, O;
+  const float* W2;  // [O][ldw]
+  int64_t ldw;
+  const int64_t* seg_off;
+  const int32_t* act;
+  const Tile3* tiles;
+  const int32_t* order;
+  int32_t ntiles;
+  const float* b2;  // [M][O] or null
+  float* out;
+  int64_t sm, sb;
+};
+bool fwd_m3_supported(int32_t Bp, int32_t F4, int32_t O);
+hipError_t launch_fwd_m3(const FwdM3Args& a, hipStream_t s);
 
 // Fused backward (dZ formed in registers, dW1 GEMM, dW2, both updates),
 // persistent, with Xt resident in LDS.

@@ -67,3 +67,28 @@ def submodel(hs, acts, W1, W2, models):
     off = offsets(hs)
     rows = np.concatenate([np.arange(off[m], off[m + 1]) for m in models])
     return (np.asarray(hs)[models], np.asarray(acts)[models], W1[rows], W2[:, rows], rows)
+
+
+def dw2_terms(orc, hs, acts, W1, W2, X, y, **kw):
+    """[O, N]: sum_b |G[b,o]| |H[b,n]|, the size of the terms dW2 = G^T H
+    sums (oracle values).  dW2 can cancel across samples (a width-1 model
+    with two outputs has dW2[1] = -dW2[0], often small), so, as for db2,
+    its per-model error is taken relative to this size rather than to
+    |dW2|; where nothing cancels the two agree."""
+    _, H = orc.hidden(hs, acts, W1, X, **{k: v for k, v in kw.items() if k in ("rounding", "b1", "mask")})
+    L = orc.forward(hs, acts, W1, W2, X, **kw)
+    P = np.exp(L - L.max(axis=2, keepdims=True))
+    P /= P.sum(axis=2, keepdims=True)
+    G = P.copy()
+    G[np.arange(L.shape[0]), :, np.asarray(y)] -= 1.0
+    G /= L.shape[0]
+    off = offsets(hs)
+    mid = np.repeat(np.arange(len(hs)), np.asarray(hs, np.int64))
+    Gn = np.abs(G[:, mid, :])               # [B, N, O]: G of each unit's model
+    return np.einsum("bno,bn->on", Gn, np.abs(H))
+
+
+def err_dw2(g, r, hs, terms):
+    """Per-model error of dW2 [O, N] relative to the size of its terms."""
+    d = np.abs(np.asarray(g, np.float64) - np.asarray(r, np.float64)).max(axis=0)
+    return _seg_max(d, hs) / np.maximum(_seg_max(np.asarray(terms).max(axis=0), hs), 1e-300)

@@ -13,8 +13,8 @@ import pytest
 
 import pmlp_workloads as wl
 from conftest import load_golden
-from parity import (cross_entropy, err_cols, err_logits, err_losses, err_rows, offsets,
-                    submodel)
+from parity import (cross_entropy, dw2_terms, err_cols, err_dw2, err_logits, err_losses,
+                    err_rows, offsets, submodel)
 
 pytestmark = pytest.mark.gpu
 
@@ -89,19 +89,31 @@ CASES = {
     # widest forward shape of the three-piece kernel: four chunks, one unit
     # tile per wave, three run-time remainder steps
     "x3_f140_b128": dict(M=12, hmax=64, F=140, O=2, B=128),
+    # the forward with the activation and M3 in its epilogue: several
+    # segments in one 16-unit block, segments ending on and off block edges,
+    # halves of wide segments, ragged batches of 256- and 128-sample tiles
+    "fm3_mixed_b256": dict(hs=[3, 1, 1, 17, 16, 15, 600, 2, 1, 33, 1000, 5, 48, 1, 16, 513],
+                           F=64, O=2, B=250),
+    "fm3_mixed_b128": dict(hs=[1] * 40 + [7, 9, 16, 32, 17, 1300, 2, 3, 64, 513],
+                           F=100, O=2, B=100),
+    "fm3_f128_b128": dict(M=40, hmax=90, F=128, O=2, B=128),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
-# allows them) and the generic kernels, selected when the handle is made.
-PATHS = ["default", "generic"]
+# allows them), the same with the forward in one kernel (product with the
+# activation and M3 in its epilogue, opt-in) where that kernel applies, and
+# the generic kernels; selected when the handle is made.
+PATHS = ["default", "fused_forward", "generic"]
 
 
 @pytest.fixture(params=PATHS)
 def path(request, monkeypatch):
+    monkeypatch.delenv("PMLP_GENERIC_KERNELS", raising=False)
+    monkeypatch.delenv("PMLP_FUSED_FORWARD", raising=False)
     if request.param == "generic":
         monkeypatch.setenv("PMLP_GENERIC_KERNELS", "1")
-    else:
-        monkeypatch.delenv("PMLP_GENERIC_KERNELS", raising=False)
+    elif request.param == "fused_forward":
+        monkeypatch.setenv("PMLP_FUSED_FORWARD", "1")
     return request.param
 
 
@@ -209,13 +221,14 @@ def test_gradients_and_losses(pm, orc, torch, name, path):
     loss = net.losses()
     r1, r2, rl, allow = orc.gradients(hs, acts, W1, W2, X, y)
     assert err_rows(dW1.cpu().numpy(), r1, hs, allow).max() <= TOL_STEP
-    assert err_cols(dW2.cpu().numpy(), r2, hs).max() <= TOL_STEP
+    terms = dw2_terms(orc, hs, acts, W1, W2, X, y)
+    assert err_dw2(dW2.cpu().numpy(), r2, hs, terms).max() <= TOL_STEP
     assert err_losses(loss, rl).max() <= TOL_STEP
     net.close()
 
 
 @pytest.mark.parametrize("name", ["ragged", "tile_spanning", "o10_b32", "b300_f100",
-                                  "f100_b250", "f128_b100_o4", "f32_b32_o10"])
+                                  "f100_b250", "f128_b100_o4", "f32_b32_o10", "fm3_mixed_b256"])
 def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name, path):
     """The fused update equals W - lr * dW with dW from the gradient mode
     (to fp32 rounding of W), and the step's losses match the oracle."""
@@ -367,7 +380,7 @@ def test_full_size_step_on_sampled_models(pm, orc, torch, wname):
     del dW1, dW2
     r1, r2, rl, allow = orc.gradients(shs, sacts, sW1, sW2, X, y)
     assert err_rows(g1, r1, shs, allow).max() <= TOL_STEP
-    assert err_cols(g2, r2, shs).max() <= TOL_STEP
+    assert err_dw2(g2, r2, shs, dw2_terms(orc, shs, sacts, sW1, sW2, X, y)).max() <= TOL_STEP
     assert err_losses(loss[models], rl).max() <= TOL_STEP
     # the fused update path on the same batch
     net.train_step(Xd, yd, w.lr)
@@ -419,25 +432,29 @@ def test_get_models_equals_slices_of_get_params(pm):
     net.close()
 
 
-# (F, O, B, generic, precision) -> the kernels the library reports for the
+# (F, O, B, path, precision) -> the kernels the library reports for the
 # forward product and the fused backward, and their arithmetic
 VARIANTS = [
-    ((100, 2, 256, False, "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
-    ((50, 2, 128, False, "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
-    ((32, 10, 32, False, "fp32"), ("k_fwd_lds_ring", 1), ("k_bwd_mf", 1)),
-    ((20, 2, 100, False, "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
-    ((100, 2, 256, True, "fp32"), ("k_gemm_nt", 1), None),
-    ((100, 2, 256, False, "bf16"), ("k_gemm_bf", 3), None),
+    ((100, 2, 256, "default", "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
+    ((100, 2, 256, "fused_forward", "fp32"), ("k_fwd_x3m", 2), ("k_bwd_x3", 2)),
+    ((50, 2, 128, "fused_forward", "fp32"), ("k_fwd_x3m", 2), ("k_bwd_x3", 2)),
+    ((100, 4, 256, "fused_forward", "fp32"), ("k_fwd_x3", 2), ("k_bwd_lds", 1)),
+    ((32, 10, 32, "default", "fp32"), ("k_fwd_lds_ring", 1), ("k_bwd_mf", 1)),
+    ((20, 2, 100, "default", "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
+    ((100, 2, 256, "generic", "fp32"), ("k_gemm_nt", 1), None),
+    ((100, 2, 256, "default", "bf16"), ("k_gemm_bf", 3), None),
 ]
 
 
 @pytest.mark.parametrize("shape,fwd,bwd", VARIANTS)
 def test_kernel_variants_are_reported(pm, torch, monkeypatch, shape, fwd, bwd):
-    F, O, B, generic, precision = shape
-    if generic:
+    F, O, B, path, precision = shape
+    monkeypatch.delenv("PMLP_GENERIC_KERNELS", raising=False)
+    monkeypatch.delenv("PMLP_FUSED_FORWARD", raising=False)
+    if path == "generic":
         monkeypatch.setenv("PMLP_GENERIC_KERNELS", "1")
-    else:
-        monkeypatch.delenv("PMLP_GENERIC_KERNELS", raising=False)
+    elif path == "fused_forward":
+        monkeypatch.setenv("PMLP_FUSED_FORWARD", "1")
     rng = np.random.default_rng(1)
     hs, acts = wl.random_models(rng, 20, 60)
     net = make_net(pm, F, O, hs, acts, seed=3)
@@ -446,7 +463,7 @@ def test_kernel_variants_are_reported(pm, torch, monkeypatch, shape, fwd, bwd):
     X, y = wl.make_dataset(F, O, B, seed=2)
     net.train_step(dev(torch, X), dev(torch, y), 0.01)
     v = net.kernel_variants()
-    assert v["gemm_fwd"] == fwd
+    assert v["fwd_m3" if fwd[0] == "k_fwd_x3m" else "gemm_fwd"] == fwd
     if bwd is not None:
         assert v["bwd_fused"] == bwd
     else:
