@@ -186,6 +186,32 @@ def cpu_baseline(w, hs, acts, X, y, seconds_hint: float):
     }
 
 
+def measured_hbm(torch, gib: int = 2):
+    """GB/s of plain device streams: a sum (read), a fill (write) and a copy
+    (read + write, counted both ways) over `gib` GiB, best of three each."""
+    n = gib * (1 << 30) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    out = {}
+    for name, fn, nbytes in (("read", lambda: a.sum(), 4 * n), ("write", lambda: b.fill_(2.0), 4 * n),
+                             ("copy", lambda: b.copy_(a), 8 * n)):
+        best = None
+        for _ in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        out[name] = nbytes / (best * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    out["unit"] = "GB/s"
+    out["how"] = "torch sum / fill_ / copy_ over %d GiB fp32, best of 3 after one warm-up" % gib
+    return out
+
+
 def epoch_batches(w):
     """(offset, length) of every batch of one epoch, the partial one last."""
     return w.batches()
@@ -343,6 +369,17 @@ def main(argv=None):
                 # ridge that chose `bound`
                 "mfma_ceiling": mpeak, "arith": arith}
 
+    # what this GPU's HBM sustains for plain streams (torch reductions, fills
+    # and copies over 2 GiB, best of three): the practical ceiling the
+    # memory-bound kernels are read against, beside the published peak
+    hbm = measured_hbm(torch)
+    roofline["frac_of_measured_copy"] = (achieved / hbm["copy"] if unit == "GB/s" else None)
+    nfull = sum(1 for _, n in batches if n == w.B)
+    step_bytes = 0.0
+    for name, (ms, n) in times.items():
+        if n:
+            step_bytes += kernel_work(name, w.B, w.F, N, M, w.O, args.precision)[1] * n / nfull
+
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(w, hs, acts, X, y, args.cpu_seconds)
@@ -362,6 +399,10 @@ def main(argv=None):
                    "value_median": M * sum(n for _, n in batches) / med if med else None,
                    "all_s": epoch_s},
         "roofline": roofline,
+        "hbm_measured": hbm,
+        # algorithmic HBM bytes of one full-batch step (all kernels) and the
+        # rate they move at over the timed steps
+        "step_traffic": {"bytes": step_bytes, "gbs": step_bytes / (ms_per_step * 1e-3) / 1e9},
         "cpu_baseline": cpu,
         "kernels": kernels,
     }

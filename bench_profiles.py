@@ -19,9 +19,16 @@ $W = workload, $P = precision, $O = an output directory):
               python3 $R/bench.py ... --copy-probe-mib 1024
   write:  the same with WRITE_SIZE
 
-and the benchmark's own line, `python3 $R/bench.py ... > $O/bench.json`.
+  set C:  rocprofv3 --pmc SQ_VALU_MFMA_COEXEC_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_MFMA \\
+              SQ_INSTS_VALU_TRANS_F32 GRBM_GUI_ACTIVE --kernel-trace -f csv -d $O/C -o run -- \\
+              python3 $R/bench.py ...   (optional)
 
-usage: python bench_profiles.py OUTDIR WORKLOAD [PRECISION]
+and the benchmark's own line, `python3 $R/bench.py ... > $O/bench.json`.  With
+--label L and --env NAME=VALUE the runs were made with that environment
+setting (for instance PMLP_FUSED_FORWARD=1) and the files are named for
+WORKLOAD_L.
+
+usage: python bench_profiles.py OUTDIR WORKLOAD [PRECISION] [--label L --env NAME=VALUE]
 """
 from __future__ import annotations
 
@@ -60,6 +67,8 @@ SET_A = ("SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_ACTIVE_INST
          "SQ_ACTIVE_INST_LDS SQ_VALU_MFMA_BUSY_CYCLES SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE")
 SET_B = ("SQ_INSTS_VALU SQ_INSTS_LDS SQ_INSTS_SALU SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR "
          "SQ_ACTIVE_INST_VMEM SQ_ACTIVE_INST_ANY SQ_WAIT_ANY GRBM_GUI_ACTIVE")
+SET_C = ("SQ_VALU_MFMA_COEXEC_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_MFMA SQ_INSTS_VALU_TRANS_F32 "
+         "GRBM_GUI_ACTIVE")
 
 
 def short(name: str) -> str:
@@ -114,23 +123,36 @@ def main(argv):
     if len(argv) < 2:
         print(__doc__)
         return 2
-    outdir, wk = argv[0], argv[1]
-    prec = argv[2] if len(argv) > 2 else "fp32"
+    label, env = None, None
+    pos = []
+    it = iter(argv)
+    for a in it:
+        if a == "--label":
+            label = next(it)
+        elif a == "--env":
+            env = next(it)
+        else:
+            pos.append(a)
+    outdir, wk = pos[0], pos[1]
+    prec = pos[2] if len(pos) > 2 else "fp32"
     tag = wk if prec == "fp32" else "%s_%s" % (wk, prec)
+    if label:
+        tag += "_" + label
+    envp = (env + " ") if env else ""
     b = json.load(open(os.path.join(outdir, "bench.json")))
     cfg = b["config"]
     N, M, F, O, B = cfg["hidden_units"], cfg["models"], cfg["F"], cfg["O"], cfg["batch"]
     args = "--workload %s%s --steps 3 --warmup 1 --cpu-seconds 0 --no-partial" % (
         wk, "" if prec == "fp32" else " --precision " + prec)
-    head = "# %%s: `%s` (%d models, N = %s, F = %d, O = %d, B = %d), %s\n" % (
-        wk, M, format(N, ","), F, O, B, prec)
+    head = "# %%s: `%s` (%d models, N = %s, F = %d, O = %d, B = %d), %s%s\n" % (
+        wk, M, format(N, ","), F, O, B, prec, (", with " + env) if env else "")
 
     # kernel trace
     tr = kernel_trace(outdir)
     lines = [head % "Kernel trace", "Command (one MI355X, from /tmp with TMPDIR=/tmp; $R = repository root):", "",
-             "```", "rocprofv3 --kernel-trace --stats -f csv -d $R/gpurun_out/prof/%s/trace -o run -- \\" % tag,
-             "    python3 $R/bench.py %s" % args, "python3 $R/bench_profiles.py $R/gpurun_out/prof/%s %s %s"
-             % (tag, wk, prec), "```", "",
+             "```", envp + "rocprofv3 --kernel-trace --stats -f csv -d $R/gpurun_out/prof/%s/trace -o run -- \\" % tag,
+             "    python3 $R/bench.py %s" % args, "python3 $R/bench_profiles.py $R/gpurun_out/prof/%s %s %s%s"
+             % (tag, wk, prec, (" --label %s --env %s" % (label, env)) if label else ""), "```", "",
              "Every launch of the run (warm-up epoch, timed steps and the profiled epoch, full batches only):", "",
              "| kernel (role) | calls | avg (us) | min (us) | max (us) | % of GPU time |",
              "|---|---:|---:|---:|---:|---:|"]
@@ -156,58 +178,87 @@ def main(argv):
         b["ms_per_step"], b["value"])]
     open(os.path.join(ROOT, "profiles", "kernel_trace_%s.md" % tag), "w").write("\n".join(lines) + "\n")
 
-    # counters
+    # counters (only where the counter passes were taken)
     ca, cb = counters(outdir, "A"), counters(outdir, "B")
+    if not ca:
+        return 0
     simds, nxcc = agent(outdir)
     lines = [head % "Counters", "Two counter passes, each in its own run (arguments of bench.py as in "
              "`kernel_trace_%s.md`):" % tag, "", "```",
-             "rocprofv3 --pmc %s --kernel-trace -f csv -d $R/gpurun_out/prof/%s/A -o run -- python3 $R/bench.py %s"
+             envp + "rocprofv3 --pmc %s --kernel-trace -f csv -d $R/gpurun_out/prof/%s/A -o run -- python3 $R/bench.py %s"
              % (SET_A, tag, args),
-             "rocprofv3 --pmc %s --kernel-trace -f csv -d $R/gpurun_out/prof/%s/B -o run -- python3 $R/bench.py %s"
-             % (SET_B, tag, args), "```", "",
+             envp + "rocprofv3 --pmc %s --kernel-trace -f csv -d $R/gpurun_out/prof/%s/B -o run -- python3 $R/bench.py %s"
+             % (SET_B, tag, args),
+             envp + "rocprofv3 --pmc %s --kernel-trace -f csv -d $R/gpurun_out/prof/%s/C -o run -- python3 $R/bench.py %s"
+             % (SET_C, tag, args), "```", "",
              "Per kernel, means over its dispatches.  GRBM_GUI_ACTIVE is summed over the %d XCDs, "
              "so T = GRBM_GUI_ACTIVE / %d is the kernel's active cycles.  Derived columns:" % (nxcc, nxcc), "",
              "- MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (T x %d SIMDs)" % simds,
              "- VALU busy = 4 x SQ_ACTIVE_INST_VALU / (T x %d SIMDs) (rocprof's VALUBusy)" % simds,
-             "- wait = SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES (share of wave time stalled on s_waitcnt)",
+             "- issue wait = SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES (share of wave time with an instruction "
+             "ready but not issued)",
+             "- s_waitcnt = SQ_WAIT_ANY / SQ_WAVE_CYCLES (share of wave time in s_waitcnt, pass B)",
              "- LDS conflicts = SQ_LDS_BANK_CONFLICT / SQ_ACTIVE_INST_LDS",
-             "- clock = T / kernel duration (duration from the trace of the same run)", "",
-             "| kernel | MFMA busy | VALU busy | wait | LDS conflicts | clock (GHz) | VALU instr / wave | "
-             "LDS instr / wave | waves |", "|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+             "- clock = T / kernel duration (duration from the trace of the same run)",
+             "- co-exec = SQ_VALU_MFMA_COEXEC_CYCLES / (T x %d SIMDs): cycles in which a vector "
+             "instruction issued while the matrix pipe was busy (pass C, where taken)" % simds, "",
+             "| kernel | MFMA busy | VALU busy | co-exec | issue wait | s_waitcnt | LDS conflicts | "
+             "clock (GHz) | VALU instr / wave | LDS instr / wave | waves |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    cc = counters(outdir, "C")
+    nan = float("nan")
     for name in sorted(ca, key=lambda n: -mean(ca[n].get("GRBM_GUI_ACTIVE", [0]))):
         if name.startswith("__amd"):
             continue
-        a, bb = ca[name], cb.get(name, {})
+        a, bb, c3 = ca[name], cb.get(name, {}), cc.get(name, {})
         g = mean(a["GRBM_GUI_ACTIVE"]) / nxcc
-        d = mean(tr.get(name, [])) if tr.get(name) else float("nan")
+        d = mean(tr.get(name, [])) if tr.get(name) else nan
         waves = mean(a["SQ_WAVES"])
-        lines.append("| `%s` | %.2f | %.2f | %.2f | %.3f | %.2f | %.0f | %.0f | %.0f |" % (
+        co = (mean(c3["SQ_VALU_MFMA_COEXEC_CYCLES"]) / ((mean(c3["GRBM_GUI_ACTIVE"]) / nxcc) * simds)
+              if c3 else nan)
+        lines.append("| `%s` | %.2f | %.2f | %.2f | %.2f | %.2f | %.3f | %.2f | %.0f | %.0f | %.0f |" % (
             name, mean(a["SQ_VALU_MFMA_BUSY_CYCLES"]) / (g * simds),
-            4 * mean(a["SQ_ACTIVE_INST_VALU"]) / (g * simds),
+            4 * mean(a["SQ_ACTIVE_INST_VALU"]) / (g * simds), co,
             mean(a["SQ_WAIT_INST_ANY"]) / max(mean(a["SQ_WAVE_CYCLES"]), 1.0),
+            mean(bb.get("SQ_WAIT_ANY", [nan])) / max(mean(a["SQ_WAVE_CYCLES"]), 1.0),
             mean(a["SQ_LDS_BANK_CONFLICT"]) / max(mean(a["SQ_ACTIVE_INST_LDS"]), 1.0),
-            g / (d * 1e3) if d == d else float("nan"),
-            mean(bb.get("SQ_INSTS_VALU", [float("nan")])) / max(waves, 1.0),
-            mean(bb.get("SQ_INSTS_LDS", [float("nan")])) / max(waves, 1.0), waves))
+            g / (d * 1e3) if d == d else nan,
+            mean(bb.get("SQ_INSTS_VALU", [nan])) / max(waves, 1.0),
+            mean(bb.get("SQ_INSTS_LDS", [nan])) / max(waves, 1.0), waves))
     open(os.path.join(ROOT, "profiles", "counters_%s.md" % tag), "w").write("\n".join(lines) + "\n")
 
-    # traffic, calibrated on the 1 GiB device copy of the same runs
+    # traffic, calibrated on plain kernels of known size in the same runs:
+    # bench.py's HBM probe sums 2 GiB (a read-only reduction) and fills
+    # 2 GiB (a write-only elementwise kernel); HIP's device copy is listed too
     fs = counters(outdir, "FETCH_SIZE")
     ws = counters(outdir, "WRITE_SIZE")
-    copy = [n for n in fs if n.startswith("__amd_rocclr_copyBuffer")]
+    if not fs or not ws:
+        return 0
     kib = 1024.0 * 1024.0
-    cf = kib / max(fs[copy[0]]["FETCH_SIZE"])
-    cw = kib / max(ws[copy[0]]["WRITE_SIZE"])
+    ref = 2.0 * kib   # KiB each probe kernel moves
+    red = [n for n in fs if "reduce_kernel" in n and "sum_functor" in n]
+    fil = [n for n in ws if "FillFunctor" in n]
+    cf = ref / max(fs[red[0]]["FETCH_SIZE"])
+    cw = ref / max(ws[fil[0]]["WRITE_SIZE"])
+    copy = [n for n in fs if n.startswith("__amd_rocclr_copyBuffer")]
+    copy_note = ""
+    if copy and copy[0] in ws:
+        copy_note = (" For comparison, HIP's device-to-device copy of 1 GiB (`--copy-probe-mib 1024`) "
+                     "reads FETCH_SIZE = %.0f KiB and WRITE_SIZE = %.0f KiB for 1,048,576 KiB each "
+                     "way; its counts differ from one box to another and from how the counters read "
+                     "the kernels here, so it is not the reference." % (
+                         max(fs[copy[0]]["FETCH_SIZE"]), max(ws[copy[0]]["WRITE_SIZE"])))
     tpath = os.path.join(ROOT, "profiles", "traffic.json")
     table = json.load(open(tpath)) if os.path.exists(tpath) else {}
     lines = [head % "HBM traffic per launch", "Two counter passes (KiB per dispatch), each in its own run:", "",
-             "```", "rocprofv3 --pmc FETCH_SIZE --kernel-trace -f csv -d $R/gpurun_out/prof/%s/FETCH_SIZE -o run -- "
+             "```", envp + "rocprofv3 --pmc FETCH_SIZE --kernel-trace -f csv -d $R/gpurun_out/prof/%s/FETCH_SIZE -o run -- "
              "python3 $R/bench.py %s --copy-probe-mib 1024" % (tag, args),
-             "rocprofv3 --pmc WRITE_SIZE --kernel-trace -f csv -d $R/gpurun_out/prof/%s/WRITE_SIZE -o run -- "
+             envp + "rocprofv3 --pmc WRITE_SIZE --kernel-trace -f csv -d $R/gpurun_out/prof/%s/WRITE_SIZE -o run -- "
              "python3 $R/bench.py %s --copy-probe-mib 1024" % (tag, args), "```", "",
-             "Calibration: the same runs copy 1 GiB device to device (`--copy-probe-mib 1024`, HIP's copy "
-             "kernel), which reads FETCH_SIZE = %.0f KiB and WRITE_SIZE = %.0f KiB for 1,048,576 KiB moved "
-             "each way: scale factors %.3f (fetch) and %.3f (write)." % (kib / cf, kib / cw, cf, cw), "",
+             "Calibration: in the same runs bench.py sums 2 GiB (torch's reduction, a read-only "
+             "stream) and fills 2 GiB (torch's fill, a write-only stream); they read FETCH_SIZE = "
+             "%.0f KiB and WRITE_SIZE = %.0f KiB for 2,097,152 KiB moved: scale factors %.3f "
+             "(fetch) and %.3f (write).%s" % (ref / cf, ref / cw, cf, cw, copy_note), "",
              "| kernel (role) | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | HBM bytes (scaled) | algorithmic bytes | ratio |",
              "|---|---:|---:|---:|---:|---:|"]
     for name in fs:
