@@ -20,7 +20,14 @@ the other columns.
 `rounding="bf16"` (forward, gradients, train, hidden, dataset_loss) emulates
 the bf16-in / fp32-accumulate variant of the two input-layer products: X,
 W1 and dZ go to fp32 and then to the nearest bfloat16 before they are
-multiplied; all other arithmetic stays fp64.
+multiplied; all other arithmetic stays fp64.  `rounding="bf16_store"` is
+that variant with Z also kept in bfloat16: the pre-activation is stored as
+the bfloat16 nearest to its fp32 value and the activation, its slope and
+everything after them use the stored value; `stored_z` (forward, gradients,
+train, hidden) gives the checked result's stored Z [rows, N] so that, where
+two stored values are correct (a rounding midpoint within `zband` times
+the size of the terms of Z), the oracle takes the checked one (see
+orc_set_stored_z in pmlp_oracle.c; stored_z_conflicts counts the rest).
 """
 from __future__ import annotations
 
@@ -92,6 +99,10 @@ def _load():
         lib.orc_set_branch.argtypes = [P, i64, dbl]
         lib.orc_branch_conflicts.restype = i64
         lib.orc_branch_conflicts.argtypes = []
+        lib.orc_set_stored_z.restype = C.c_int
+        lib.orc_set_stored_z.argtypes = [P, i64, dbl]
+        lib.orc_stored_z_conflicts.restype = i64
+        lib.orc_stored_z_conflicts.argtypes = []
         lib.orc_set_feature_mask.restype = C.c_int
         lib.orc_set_feature_mask.argtypes = [P]
         lib.orc_dataset_loss.restype = C.c_int
@@ -123,7 +134,7 @@ def _check(rc: int, what: str):
         raise RuntimeError("oracle %s failed with code %d" % (what, rc))
 
 
-_ROUNDING = {"exact": 0, "bf16": 1}
+_ROUNDING = {"exact": 0, "bf16": 1, "bf16_store": 2}
 
 
 @contextlib.contextmanager
@@ -174,6 +185,36 @@ def _branch(br, band: float, N: int):
     finally:
         _last_conflicts = int(lib.orc_branch_conflicts())
         lib.orc_set_branch(None, 0, 0.0)
+
+
+_last_z_conflicts = 0
+
+
+@contextlib.contextmanager
+def _stored_z(zs, band: float, N: int):
+    """Stored-Z choices of the bf16 storage variant for the duration of one
+    call (see orc_set_stored_z in pmlp_oracle.c): zs is [rows, N] fp32, the
+    stored Z of the checked result; None gives none."""
+    global _last_z_conflicts
+    lib = _load()
+    a = None
+    if zs is not None:
+        a = np.ascontiguousarray(zs, dtype=np.float32)
+        if a.ndim != 2 or a.shape[1] != N:
+            raise ValueError("stored Z must be [rows, %d]" % N)
+    _check(lib.orc_set_stored_z(_p(a), 0 if a is None else N, float(band)), "set_stored_z")
+    try:
+        yield
+    finally:
+        _last_z_conflicts = int(lib.orc_stored_z_conflicts())
+        lib.orc_set_stored_z(None, 0, 0.0)
+
+
+def stored_z_conflicts() -> int:
+    """Number of (sample, unit) pairs in the last call given stored Z where
+    the given value is not among the correct stored values (it kept its
+    own there)."""
+    return _last_z_conflicts
 
 
 @contextlib.contextmanager
@@ -257,7 +298,7 @@ def init_biases(F: int, O: int, hidden_sizes, seed: int) -> Tuple[np.ndarray, np
 
 def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
             rounding: str = "exact", b1=None, b2=None, branch=None,
-            band: float = 1e-6, mask=None) -> np.ndarray:
+            band: float = 1e-6, mask=None, stored_z=None, zband: float = 1e-6) -> np.ndarray:
     """logits [B, M, O] in fp64; optional biases b1 [N] and b2 [M, O];
     optional branch choices [B, N] at Hardshrink's jumps (see _branch)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
@@ -266,7 +307,7 @@ def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
     O, N = W2d.shape
     c1, c2 = _bias(b1, N, "b1"), _bias(b2, len(hs) * O, "b2")
     out = np.empty((B, len(hs), O), np.float64)
-    with _rounding(rounding), _branch(branch, band, N), _fmask(mask, len(hs), F):
+    with _rounding(rounding), _branch(branch, band, N), _stored_z(stored_z, zband, N), _fmask(mask, len(hs), F):
         _check(_load().orc_forward(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                    _p(c2), _p(Xf), B, _p(out), nthreads), "forward")
     return out
@@ -275,7 +316,8 @@ def forward(hidden_sizes, act_ids, W1, W2, X, nthreads: int = 0,
 def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
               with_allowance: bool = True, nthreads: int = 0, rounding: str = "exact",
               tie_rel: float = 1e-5, cond_rel: float = 2.4e-7, b1=None, b2=None,
-              head: str = "ce", branch=None, band: float = 1e-6, mask=None):
+              head: str = "ce", branch=None, band: float = 1e-6, mask=None, stored_z=None,
+              zband: float = 1e-6):
     """(dW1 [N,F], dW2 [O,N], loss [M], allow_dW1 [N,F] or None) in fp64.
 
     allow_dW1 bounds what a correct fp32 evaluation may differ by where a
@@ -304,7 +346,7 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
     db1 = np.empty(N, np.float64) if c1 is not None else None
     db2 = np.empty((M, O), np.float64) if c2 is not None else None
     allow_b = np.empty(N, np.float64) if (with_allowance and c1 is not None) else None
-    with _rounding(rounding), _head(head), _branch(branch, band, N), _fmask(mask, M, F):
+    with _rounding(rounding), _head(head), _branch(branch, band, N), _stored_z(stored_z, zband, N), _fmask(mask, M, F):
         _check(_load().orc_gradients(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                      _p(c2), _p(Xf), _p(yi), B, _p(dW1), _p(dW2), _p(db1),
                                      _p(db2), _p(loss), _p(allow), _p(allow_b),
@@ -319,7 +361,8 @@ def gradients(hidden_sizes, act_ids, W1, W2, X, y, kink_rel: float = 1e-6,
 def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]],
           lr: float, models: Optional[Sequence[int]] = None, nthreads: int = 0,
           rounding: str = "exact", return_ties: bool = False, tie_rel: float = 1e-6,
-          b1=None, b2=None, head: str = "ce", branch=None, band: float = 1e-6, mask=None):
+          b1=None, b2=None, head: str = "ce", branch=None, band: float = 1e-6, mask=None,
+          stored_z=None, zband: float = 1e-6):
     """SGD over the given (offset, length) batches.
 
     Returns (W1' [N,F], W2' [O,N], loss_last [M]) in fp64.  With a model
@@ -353,7 +396,7 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
         if lr_m.size != len(hs):
             raise ValueError("per-model lr needs one rate per model")
         lr = 0.0
-    with _rounding(rounding), _head(head), _branch(branch, band, N), _fmask(mask, len(hs), F):
+    with _rounding(rounding), _head(head), _branch(branch, band, N), _stored_z(stored_z, zband, N), _fmask(mask, len(hs), F):
         _check(_load().orc_train(F, O, len(hs), _p(hs), _p(ac), _p(W1d), _p(W2d), _p(c1),
                                  _p(c2), _p(Xf), _p(yi), len(batches), _p(off), _p(ln),
                                  float(lr), _p(lr_m), _p(W1o), _p(W2o), _p(b1o), _p(b2o),
@@ -368,7 +411,8 @@ def train(hidden_sizes, act_ids, W1, W2, X, y, batches: Sequence[Tuple[int, int]
 
 
 def hidden(hidden_sizes, act_ids, W1, X, rounding: str = "exact", b1=None,
-           branch=None, band: float = 1e-6, mask=None) -> Tuple[np.ndarray, np.ndarray]:
+           branch=None, band: float = 1e-6, mask=None, stored_z=None,
+           zband: float = 1e-6) -> Tuple[np.ndarray, np.ndarray]:
     """Z = X W1^T and H = act(Z), both [B, N] fp64 (branch: see _branch)."""
     hs, ac = _c(hidden_sizes, np.int32), _c(act_ids, np.int32)
     W1d, Xf = _c(W1, np.float64), _c(X, np.float32)
@@ -376,7 +420,7 @@ def hidden(hidden_sizes, act_ids, W1, X, rounding: str = "exact", b1=None,
     N = int(hs.sum())
     Z = np.empty((B, N), np.float64)
     H = np.empty((B, N), np.float64)
-    with _rounding(rounding), _branch(branch, band, N), _fmask(mask, len(hs), F):
+    with _rounding(rounding), _branch(branch, band, N), _stored_z(stored_z, zband, N), _fmask(mask, len(hs), F):
         _check(_load().orc_hidden(F, len(hs), _p(hs), _p(ac), _p(W1d), _p(_bias(b1, N, "b1")),
                                   _p(Xf), B, _p(Z), _p(H)), "hidden")
     return Z, H

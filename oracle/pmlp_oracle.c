@@ -231,11 +231,15 @@ int orc_init_biases(int32_t F, int32_t O, int32_t M, const int32_t* hidden_sizes
 /* Operand rounding of the input-layer products.                            */
 /* ------------------------------------------------------------------------ */
 
-/* 0: exact (fp64 products of the given values); 1: bfloat16 operands. */
+/* 0: exact (fp64 products of the given values); 1: bfloat16 operands;
+ * 2: bfloat16 operands and Z kept in bfloat16 (the storage variant: the
+ * hidden pre-activation is stored as the bfloat16 nearest to its fp32
+ * value, and the activation, its slope and everything after them see that
+ * stored value). */
 static int orc_rounding = 0;
 
 int orc_set_input_rounding(int mode) {
-  if (mode != 0 && mode != 1) return ORC_EINVAL;
+  if (mode < 0 || mode > 2) return ORC_EINVAL;
   orc_rounding = mode;
   return ORC_OK;
 }
@@ -286,6 +290,10 @@ typedef struct {
    * (NULL: no choices given); pass [B,h] records the branch taken. */
   const uint8_t* br;
   uint8_t* pass;
+  /* Stored-Z choices of rounding mode 2 (see orc_set_stored_z): zc points
+   * at this model's first unit in the first sample row of the current
+   * batch (NULL: none given). */
+  const float* zc;
 } orc_scratch;
 
 /* Every caller declares its scratch zero-initialised, so that a failed
@@ -299,6 +307,7 @@ static int orc_scratch_alloc(orc_scratch* s, int B, int h, int F, int O, int act
   s->dH = (double*)malloc(sizeof(double) * (size_t)B * h);
   s->dZ = (double*)malloc(sizeof(double) * (size_t)B * h);
   s->br = NULL;
+  s->zc = NULL;
   s->pass = (uint8_t*)malloc((size_t)B * h);
   return (s->Z && s->H && s->L && s->G && s->dH && s->dZ && s->pass) ? ORC_OK : ORC_ENOMEM;
 }
@@ -349,6 +358,59 @@ static int orc_hardshrink_pass(double z, double mag, int g) {
   return own;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Stored Z of rounding mode 2.  Z is kept as the bfloat16 nearest to its   */
+/* fp32 value.  An fp32 evaluation of Z that is correct to within rounding  */
+/* may lie on the other side of a bfloat16 rounding midpoint than the fp32  */
+/* value of the exact Z, and is then stored as the neighbouring bfloat16:  */
+/* two stored values are correct there.  A caller that wants to check one  */
+/* particular such result gives the stored value it produced for every    */
+/* (sample, unit): zc[row * ld + n].  The oracle takes the given value only */
+/* where it is a bfloat16 neighbour of its own and the midpoint between    */
+/* the two lies within band * sum_f |x_f w_f| of the exact Z; anywhere     */
+/* else it keeps its own and counts a disagreement (orc_stored_z_conflicts).*/
+/* ------------------------------------------------------------------------ */
+
+static const float* orc_zc = NULL;
+static int64_t orc_zc_ld = 0;
+static double orc_zc_band = 0.0;
+static int64_t orc_zc_conflict_count = 0;
+
+int orc_set_stored_z(const float* zc, int64_t ld, double band) {
+  if (zc && (ld < 1 || !(band >= 0.0))) return ORC_EINVAL;
+  orc_zc = zc;
+  orc_zc_ld = zc ? ld : 0;
+  orc_zc_band = zc ? band : 0.0;
+  orc_zc_conflict_count = 0;
+  return ORC_OK;
+}
+
+int64_t orc_stored_z_conflicts(void) { return orc_zc_conflict_count; }
+
+/* The stored value of an exact Z z (mag = sum_f |x_f w_f|) under rounding
+ * mode 2, given the caller's stored value g (NULL: none). */
+static double orc_store_z(double z, double mag, const float* g) {
+  const float own = orc_bf16((float)z);
+  if (!g || *g == own || (isnan(*g) && isnan(own))) return (double)own;
+  uint32_t uo, ug;
+  memcpy(&uo, &own, sizeof uo);
+  memcpy(&ug, g, sizeof ug);
+  /* bfloat16 neighbours of one sign differ by one unit of the 16-bit
+   * pattern; across zero the neighbours of +0 / -0 are the smallest
+   * bfloat16 of either sign */
+  const uint32_t d = uo > ug ? uo - ug : ug - uo;
+  const int adjacent = ((uo ^ ug) & 0x80000000u) == 0
+                           ? d == 0x10000u
+                           : ((uo & 0x7FFFFFFFu) + (ug & 0x7FFFFFFFu)) == 0x10000u;
+  if (adjacent && (ug & 0xFFFFu) == 0) {
+    const double mid = 0.5 * ((double)own + (double)*g);
+    if (fabs(z - mid) <= orc_zc_band * mag) return (double)*g;
+  }
+#pragma omp atomic
+  orc_zc_conflict_count += 1;
+  return (double)own;
+}
+
 /* The slope used by back-propagation for element i of a model's scratch. */
 static double orc_slope(const orc_scratch* s, int64_t i) {
   if (s->br && s->act == 11) return s->pass[i] ? 1.0 : 0.0;
@@ -372,9 +434,16 @@ static void orc_model_forward(const orc_scratch* s, int B, const float* X,
       for (int f = 0; f < F; ++f)
         acc += orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]);
       if (b1) acc += orc_in(b1[j]);   /* the weight of a constant input 1 */
+      if (orc_rounding == 2) {
+        double mag = b1 ? fabs(orc_in(b1[j])) : 0.0;
+        if (s->zc)
+          for (int f = 0; f < F; ++f)
+            mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
+        acc = orc_store_z(acc, mag, s->zc ? s->zc + (int64_t)b * orc_zc_ld + j : NULL);
+      }
       s->Z[(int64_t)b * h + j] = acc;
       s->H[(int64_t)b * h + j] = orc_act(s->act, acc);
-      if (s->br && s->act == 11) {
+      if (s->br && s->act == 11 && orc_rounding != 2) {
         double mag = b1 ? fabs(orc_in(b1[j])) : 0.0;
         for (int f = 0; f < F; ++f)
           mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(w1[(int64_t)j * F + f]));
@@ -767,6 +836,7 @@ int orc_forward(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_
     } else {
       orc_take(N, O, off[m], h, &v, W1, W2, w1, w2);
       s.br = orc_branch ? orc_branch + off[m] : NULL;
+      s.zc = orc_zc ? orc_zc + off[m] : NULL;
       orc_model_forward(&s, B, orc_view_rows(&v, X, B), w1, w2, b1 ? b1 + off[m] : NULL,
                         b2 ? b2 + (int64_t)m * O : NULL);
       for (int b = 0; b < B; ++b)
@@ -819,6 +889,7 @@ int orc_gradients(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int3
       const float* Xm = orc_view_rows(&v, X, B);
       const double* bm1 = b1 ? b1 + off[m] : NULL;
       s.br = orc_branch ? orc_branch + off[m] : NULL;
+      s.zc = orc_zc ? orc_zc + off[m] : NULL;
       orc_model_forward(&s, B, Xm, w1, w2, bm1, b2 ? b2 + (int64_t)m * O : NULL);
       loss[m] = orc_model_loss(&s, B, y);
       orc_model_backward(&s, B, Xm, w2, g1, g2, db1 ? db1 + off[m] : NULL,
@@ -902,6 +973,7 @@ int orc_train(int32_t F, int32_t O, int32_t M, const int32_t* hs, const int32_t*
         const float* Xb = orc_view_rows(&v, X + batch_off[k] * F, B);
         const void* yb = orc_labels_at(y, batch_off[k], O);
         s.br = orc_branch ? orc_branch + batch_off[k] * orc_branch_ld + off[m] : NULL;
+        s.zc = orc_zc ? orc_zc + batch_off[k] * orc_zc_ld + off[m] : NULL;
         orc_model_forward(&s, B, Xb, w1, w2, c1, c2);
         last = orc_model_loss(&s, B, yb);
         if (ties) ties[m] += orc_model_value_ties(&s, B, Xb, w1, c1, tie_rel);
@@ -949,9 +1021,17 @@ int orc_hidden(int32_t F, int32_t M, const int32_t* hs, const int32_t* acts,
           if (!orc_fmask || orc_fmask[(int64_t)m * F + f])
             acc += orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]);
         if (b1) acc += orc_in(b1[n]);
+        if (orc_rounding == 2) {
+          double mag = b1 ? fabs(orc_in(b1[n])) : 0.0;
+          if (orc_zc)
+            for (int f = 0; f < F; ++f)
+              if (!orc_fmask || orc_fmask[(int64_t)m * F + f])
+                mag += fabs(orc_in(X[(int64_t)b * F + f]) * orc_in(W1[n * F + f]));
+          acc = orc_store_z(acc, mag, orc_zc ? orc_zc + (int64_t)b * orc_zc_ld + n : NULL);
+        }
         Z[(int64_t)b * N + n] = acc;
         H[(int64_t)b * N + n] = orc_act(acts[m], acc);
-        if (orc_branch && acts[m] == 11) {
+        if (orc_branch && acts[m] == 11 && orc_rounding != 2) {
           double mag = b1 ? fabs(orc_in(b1[n])) : 0.0;
           for (int f = 0; f < F; ++f)
             if (!orc_fmask || orc_fmask[(int64_t)m * F + f])
