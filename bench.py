@@ -47,12 +47,14 @@ def kernel_work(name, B, F, N, M, O, precision="fp32"):
     the path stores it: fp32, except in the bf16 mode the batch copies, the
     bf16 copy of W1 (read by the input-to-hidden product, rewritten by the
     update) and dZ (written by the M3 backward, read by the dW1 product);
-    flops count multiply-adds as two operations."""
+    flops count multiply-adds as two operations.  The bf16 storage mode also
+    keeps Z in bf16 (2 bytes per element wherever Z is written or read)."""
     f4 = 4.0
-    bf = precision == "bf16"
+    bf = precision in ("bf16", "bf16_store")
     fx = 2.0 if bf else 4.0      # bytes per element of the batch copy
+    fz = 2.0 if precision == "bf16_store" else 4.0   # bytes per element of Z
     if name == "gemm_fwd":       # Z = X W1^T: read W1 (bf16 copy in bf16 mode), X; write Z
-        return "mfma", (2.0 if bf else f4) * N * F + fx * B * F + f4 * N * B, 2.0 * B * F * N
+        return "mfma", (2.0 if bf else f4) * N * F + fx * B * F + fz * N * B, 2.0 * B * F * N
     if name == "gemm_bwd":       # W1 -= lr dZ^T X: read dZ, X; read+write W1 (+ its bf16 copy)
         return ("mfma", (2.0 if bf else f4) * N * B + fx * B * F + 2 * f4 * N * F
                 + (2.0 * N * F if bf else 0.0), 2.0 * B * F * N)
@@ -60,9 +62,9 @@ def kernel_work(name, B, F, N, M, O, precision="fp32"):
         return ("mfma", f4 * (N * F + B * F + N * B + O * N + B * M * O),
                 2.0 * B * F * N + 2.0 * B * O * N)
     if name == "m3_fwd":         # read Z, W2; write logits
-        return "hbm", f4 * (N * B + O * N + B * M * O), 2.0 * B * O * N
+        return "hbm", fz * N * B + f4 * (O * N + B * M * O), 2.0 * B * O * N
     if name == "m3_bwd":         # read Z, G, W2; write dZ (bf16 in bf16 mode), W2
-        return ("hbm", f4 * N * B + (2.0 if bf else f4) * N * B + f4 * (2 * O * N + B * M * O),
+        return ("hbm", fz * N * B + (2.0 if bf else f4) * N * B + f4 * (2 * O * N + B * M * O),
                 4.0 * B * O * N)
     if name == "bwd_fused":      # read Z, G, X; read+write W1 and W2 (dZ stays in registers)
         return ("mfma", f4 * (N * B + B * M * O + B * F + 2 * N * F + 2 * O * N),
@@ -130,6 +132,7 @@ KERNEL_SOURCE = {
              "m3_fwd": "k_m3.hip", "m3_bwd": "k_m3.hip", "ce": "k_misc.hip",
              "pack_x": "k_misc.hip", "aux": "k_misc.hip"},
 }
+KERNEL_SOURCE["bf16_store"] = KERNEL_SOURCE["bf16"]
 
 
 def kernel_source_digest(kernel: str = None, precision: str = "fp32") -> str:
@@ -226,7 +229,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps before (default: one whole epoch)")
     ap.add_argument("--workload", default="w10k_f100", choices=sorted(wl.WORKLOADS))
-    ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"])
+    ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16", "bf16_store"],
+                    help="bf16: the bf16 operand mode (PMLP_BF16_GEMM); bf16_store: with Z "
+                         "also stored in bf16 (PMLP_BF16_STORE)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one epoch as a HIP graph and replay it (timed steps are "
                          "rounded up to whole epochs)")
@@ -264,8 +269,9 @@ def main(argv=None):
     warmup = args.warmup if args.warmup is not None else spe
     if args.graph:
         steps = spe * max(1, -(-steps // spe))
-    net = pm.PackedMLP(w.F, w.O, hs, acts, seed=w.init_seed,
-                       precision=pm.PMLP_BF16_GEMM if args.precision == "bf16" else pm.PMLP_FP32)
+    mode = {"fp32": pm.PMLP_FP32, "bf16": pm.PMLP_BF16_GEMM,
+            "bf16_store": pm.PMLP_BF16_STORE}[args.precision]
+    net = pm.PackedMLP(w.F, w.O, hs, acts, seed=w.init_seed, precision=mode)
 
     def step(k):
         s, n = batches[k % spe]
@@ -389,7 +395,8 @@ def main(argv=None):
         "metric": METRIC, "value": value, "unit": "model-samples/s", "n_gpus": 1,
         "steps": steps, "warmup": warm, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if args.precision == "fp32" else "bf16-gemm/f32",
+        "dtype": {"fp32": "f32", "bf16": "bf16-gemm/f32",
+                  "bf16_store": "bf16-gemm/bf16-z/f32"}[args.precision],
         "data": "synthetic (seeded X ~ N(0,1), linear-teacher labels; seeded weight init)",
         "config": {"workload": w.name, "models": M, "hidden_units": N, "F": w.F, "O": w.O,
                    "batch": w.B, "samples": w.S, "hidden_sizes": "%d..%d" % w.sizes,

@@ -71,6 +71,8 @@ extern "C" {
 #define PMLP_FP32 0       /* fp32 operands, fp32 accumulation (default) */
 #define PMLP_BF16_GEMM 1  /* the two input-layer GEMMs take bf16-rounded
                              operands with fp32 accumulation */
+#define PMLP_BF16_STORE 2 /* PMLP_BF16_GEMM with the hidden pre-activation Z
+                             also stored in bf16 between the kernels */
 
 #define PMLP_NUM_ACTS 13
 
@@ -178,7 +180,16 @@ int pmlp_set_stream(pmlp_t h, void* stream);
  *     the products read them and the products accumulate in fp32; the
  *     weights, Z, the activations, logits, loss, gradients of W2 and the
  *     SGD updates stay fp32.  Every shape is supported.
- * Returns PMLP_EINVAL for any other mode; the handle keeps its mode. */
+ *   PMLP_BF16_STORE: PMLP_BF16_GEMM, and Z is kept between the kernels as
+ *     the bf16 nearest (ties to even) to the fp32 accumulator, in half the
+ *     bytes (the memory remark of Section 5: Z is the largest tensor a
+ *     step moves); the activation, its derivative and everything after
+ *     them use the stored value, and pmlp_hidden returns it (as fp32).
+ *     bf16 keeps fp32's exponent range, so nothing in this mode needs
+ *     loss scaling.
+ * Both bf16 modes are for packs with one hidden layer (PMLP_ESTATE for a
+ * pmlp_create_deep handle).  Returns PMLP_EINVAL for any other mode; the
+ * handle keeps its mode. */
 int pmlp_set_precision(pmlp_t h, int32_t mode);
 
 /* Forward pass only (Section 3: input-to-hidden product, per-model

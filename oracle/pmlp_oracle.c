@@ -362,13 +362,13 @@ static int orc_hardshrink_pass(double z, double mag, int g) {
 /* Stored Z of rounding mode 2.  Z is kept as the bfloat16 nearest to its   */
 /* fp32 value.  An fp32 evaluation of Z that is correct to within rounding  */
 /* may lie on the other side of a bfloat16 rounding midpoint than the fp32  */
-/* value of the exact Z, and is then stored as the neighbouring bfloat16:  */
-/* two stored values are correct there.  A caller that wants to check one  */
+/* value of the exact Z, and is then stored as another bfloat16: several    */
+/* stored values are correct there.  A caller that wants to check one       */
 /* particular such result gives the stored value it produced for every    */
 /* (sample, unit): zc[row * ld + n].  The oracle takes the given value only */
-/* where it is a bfloat16 neighbour of its own and the midpoint between    */
-/* the two lies within band * sum_f |x_f w_f| of the exact Z; anywhere     */
-/* else it keeps its own and counts a disagreement (orc_stored_z_conflicts).*/
+/* where some value within band * sum_f |x_f w_f| of the exact Z rounds to  */
+/* it (see orc_store_z); anywhere else it keeps its own and counts a        */
+/* disagreement (orc_stored_z_conflicts).                                   */
 /* ------------------------------------------------------------------------ */
 
 static const float* orc_zc = NULL;
@@ -387,24 +387,41 @@ int orc_set_stored_z(const float* zc, int64_t ld, double band) {
 
 int64_t orc_stored_z_conflicts(void) { return orc_zc_conflict_count; }
 
+static float orc_bf16_bits(uint32_t u) {
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return f;
+}
+
 /* The stored value of an exact Z z (mag = sum_f |x_f w_f|) under rounding
- * mode 2, given the caller's stored value g (NULL: none). */
+ * mode 2, given the caller's stored value g (NULL: none).  g is correct if
+ * it is the bfloat16 that some value within band * mag of z rounds to: its
+ * rounding interval (half-way to each bfloat16 neighbour) reaches within
+ * band * mag of z.  Under heavy cancellation (|z| far below mag) that holds
+ * for more than the two neighbours of z. */
 static double orc_store_z(double z, double mag, const float* g) {
   const float own = orc_bf16((float)z);
   if (!g || *g == own || (isnan(*g) && isnan(own))) return (double)own;
-  uint32_t uo, ug;
-  memcpy(&uo, &own, sizeof uo);
+  uint32_t ug;
   memcpy(&ug, g, sizeof ug);
-  /* bfloat16 neighbours of one sign differ by one unit of the 16-bit
-   * pattern; across zero the neighbours of +0 / -0 are the smallest
-   * bfloat16 of either sign */
-  const uint32_t d = uo > ug ? uo - ug : ug - uo;
-  const int adjacent = ((uo ^ ug) & 0x80000000u) == 0
-                           ? d == 0x10000u
-                           : ((uo & 0x7FFFFFFFu) + (ug & 0x7FFFFFFFu)) == 0x10000u;
-  if (adjacent && (ug & 0xFFFFu) == 0) {
-    const double mid = 0.5 * ((double)own + (double)*g);
-    if (fabs(z - mid) <= orc_zc_band * mag) return (double)*g;
+  if ((ug & 0xFFFFu) == 0 && isfinite(*g)) {
+    /* the bfloat16 neighbours of g by value (through zero as well) */
+    const uint32_t mag_bits = ug & 0x7FFFFFFFu, sign = ug & 0x80000000u;
+    double up, dn;
+    if (mag_bits == 0) {
+      up = (double)orc_bf16_bits(0x00010000u);
+      dn = (double)orc_bf16_bits(0x80010000u);
+    } else if (!sign) {
+      up = (double)orc_bf16_bits(ug + 0x10000u);
+      dn = (double)orc_bf16_bits(ug - 0x10000u);
+    } else {
+      up = (double)orc_bf16_bits(ug - 0x10000u);
+      dn = (double)orc_bf16_bits(ug + 0x10000u);
+    }
+    const double gv = (double)*g;
+    const double lo = 0.5 * (gv + dn), hi = 0.5 * (gv + up);
+    const double dist = z < lo ? lo - z : (z > hi ? z - hi : 0.0);
+    if (dist <= orc_zc_band * mag) return gv;
   }
 #pragma omp atomic
   orc_zc_conflict_count += 1;

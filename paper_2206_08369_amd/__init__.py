@@ -18,7 +18,7 @@ import numpy as np
 
 __all__ = [
     "PMLP_OK", "PMLP_EINVAL", "PMLP_ENOMEM", "PMLP_EDEVICE", "PMLP_ESTATE",
-    "PMLP_FP32", "PMLP_BF16_GEMM", "PMLP_BIAS", "PMLP_NUM_KERNELS", "ACT_IDS", "PmlpError",
+    "PMLP_FP32", "PMLP_BF16_GEMM", "PMLP_BF16_STORE", "PMLP_BIAS", "PMLP_NUM_KERNELS", "ACT_IDS", "PmlpError",
     "library_path", "load_library", "pmlp_create", "pmlp_destroy", "pmlp_set_stream",
     "pmlp_set_precision", "pmlp_forward", "pmlp_train_step", "pmlp_train_step_lr",
     "pmlp_losses",
@@ -39,6 +39,7 @@ PMLP_EDEVICE = -3
 PMLP_ESTATE = -4
 PMLP_FP32 = 0
 PMLP_BF16_GEMM = 1
+PMLP_BF16_STORE = 2
 PMLP_BIAS = 1
 PMLP_MSE = 2
 PMLP_NUM_KERNELS = 11

@@ -350,7 +350,10 @@ int ensure_workspace_bf16(pmlp* h, int32_t Bp) {
   return PMLP_OK;
 }
 
-bool bf16_mode(const pmlp* h) { return h->precision == PMLP_BF16_GEMM; }
+// Both bf16 modes round the operands of the input-layer products; the
+// storage mode also keeps Z as bfloat16 (in the first half of Zt).
+bool bf16_mode(const pmlp* h) { return h->precision != PMLP_FP32; }
+bool z_bf16(const pmlp* h) { return h->precision == PMLP_BF16_STORE; }
 
 // The bf16 copy of W1 read by the bf16 input-to-hidden product: allocated
 // on first use, rebuilt whenever W1 changed outside a bf16-mode SGD step
@@ -430,6 +433,10 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp, const Work& w
     g.out = w.Zt;
     g.ldo = Bp;
     g.ncols = Bp;
+    if (z_bf16(h)) {
+      g.outb = (unsigned short*)w.Zt;
+      g.ldob = Bp;
+    }
     return run(h, KID_GEMM_FWD, [&] { return launch_gemm_bf16(g, EPI_STORE, h->stream); });
   }
   if (int rc = run(h, KID_PACK_X, [&] {
@@ -531,7 +538,7 @@ int step(pmlp* h, const float* X, const void* y, int32_t B, float lr, const floa
     if (int rc = run(h, KID_M3_FWD, [&] {
           return launch_m3_fwd(w.Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act,
                                h->d_tiles, h->d_order, h->ntiles, h->b2, w.LG, (int64_t)Bp * h->O,
-                               h->O, h->stream);
+                               h->O, h->stream, z_bf16(h));
         }))
       return rc;
   }
@@ -579,7 +586,7 @@ int step(pmlp* h, const float* X, const void* y, int32_t B, float lr, const floa
   if (int rc = run(h, KID_M3_BWD, [&] {
         return launch_m3_bwd(w.Zt, bf16_mode(h) ? h->dZ16 : nullptr, Bp, h->W2, h->N, h->Npad,
                              h->O, h->d_mid, h->d_seg_off,
-                             h->d_act, w.LG, lr, lrm, dW2, h->stream);
+                             h->d_act, w.LG, lr, lrm, dW2, h->stream, z_bf16(h));
       }))
     return rc;
   if (bf16_mode(h)) {
@@ -937,9 +944,10 @@ int pmlp_set_stream(pmlp_t h, void* stream) {
 
 int pmlp_set_precision(pmlp_t h, int32_t mode) {
   if (int rc = check_handle(h)) return rc;
-  if (mode != PMLP_FP32 && mode != PMLP_BF16_GEMM) return fail(PMLP_EINVAL, "unknown precision mode");
-  if (mode == PMLP_BF16_GEMM)
-    if (int rc = one_layer_only(h, "the PMLP_BF16_GEMM mode")) return rc;
+  if (mode != PMLP_FP32 && mode != PMLP_BF16_GEMM && mode != PMLP_BF16_STORE)
+    return fail(PMLP_EINVAL, "unknown precision mode");
+  if (mode != PMLP_FP32)
+    if (int rc = one_layer_only(h, "the bf16 modes")) return rc;
   h->precision = mode;
   return PMLP_OK;
 }
@@ -977,7 +985,8 @@ int pmlp_forward(pmlp_t h, const float* X_dev, int32_t B, float* logits_dev) {
   }
   return run(h, KID_M3_FWD, [&] {
     return launch_m3_fwd(h->Zt, Bp, B, h->W2, h->Npad, h->O, h->d_seg_off, h->d_act, h->d_tiles,
-                         h->d_order, h->ntiles, h->b2, logits_dev, h->O, (int64_t)h->M * h->O, h->stream);
+                         h->d_order, h->ntiles, h->b2, logits_dev, h->O, (int64_t)h->M * h->O,
+                         h->stream, z_bf16(h));
   });
 }
 
@@ -1104,7 +1113,8 @@ int pmlp_hidden(pmlp_t h, const float* X_dev, int32_t B, float* Z_dev, float* H_
   if (int rc = forward_hidden(h, X_dev, B, Bp, handle_work(h))) return rc;
   if (!Z_dev && !H_dev) return PMLP_OK;
   return run(h, KID_ACT, [&] {
-    return launch_hidden_out(h->Zt, Bp, B, h->N, h->d_mid, h->d_act, Z_dev, H_dev, h->stream);
+    return launch_hidden_out(h->Zt, Bp, B, h->N, h->d_mid, h->d_act, Z_dev, H_dev, h->stream,
+                             z_bf16(h));
   });
 }
 

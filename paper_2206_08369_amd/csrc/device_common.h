@@ -135,6 +135,31 @@ __device__ __forceinline__ float mish_t(float z, float* u_out) {
   return n * frcp(n + 2.f);
 }
 
+// Z of the hidden layer as stored: fp32, or (zb, the bf16 storage mode)
+// the bfloat16 bit patterns in the first half of the same buffer, widened
+// exactly to fp32.  idx is an element index of the [Npad][Bp] layout.
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b16) {
+  return __uint_as_float(b16 << 16);
+}
+__device__ __forceinline__ f32x4 load_z4(const float* Zt, bool zb, int64_t idx) {
+  if (zb) {
+    const uint2 v = *(const uint2*)((const unsigned short*)Zt + idx);
+    return f32x4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u),
+                 __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u)};
+  }
+  return *(const f32x4*)(Zt + idx);
+}
+__device__ __forceinline__ f32x2 load_z2(const float* Zt, bool zb, int64_t idx) {
+  if (zb) {
+    const uint32_t v = *(const uint32_t*)((const unsigned short*)Zt + idx);
+    return f32x2{__uint_as_float(v << 16), __uint_as_float(v & 0xFFFF0000u)};
+  }
+  return *(const f32x2*)(Zt + idx);
+}
+__device__ __forceinline__ float load_z1(const float* Zt, bool zb, int64_t idx) {
+  return zb ? bf16_bits_to_f32(((const unsigned short*)Zt)[idx]) : Zt[idx];
+}
+
 __device__ __forceinline__ float act_fwd(int a, float z) {
   switch (a) {
     case 0: return z;

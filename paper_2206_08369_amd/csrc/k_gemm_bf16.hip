@@ -281,7 +281,12 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
         const f32x4 v =
             (EPI != EPI_STORE && a.fmask) ? fmask4(a.fmask, a.fmw, a.mid[p], q, v0) : v0;
         if (EPI == EPI_STORE) {
-          *(f32x4*)o = v0;
+          if (a.outb) {  // the bf16 storage mode keeps Z as bfloat16 (nearest even)
+            const bf16x4 zb = {(__bf16)v0[0], (__bf16)v0[1], (__bf16)v0[2], (__bf16)v0[3]};
+            *(bf16x4*)(a.outb + p * a.ldob + q) = zb;
+          } else {
+            *(f32x4*)o = v0;
+          }
         } else if (EPI == EPI_SGD) {
           f32x4 w = *(f32x4*)o;
           w -= lr * v;

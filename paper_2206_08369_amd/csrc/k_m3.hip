@@ -25,7 +25,7 @@ namespace pmlpk {
 
 static constexpr int kU = 4;  // hidden units per lane group per pass (loads in flight)
 
-template <int OM, int A>
+template <int OM, int A, bool ZB>
 __device__ __forceinline__ void fwd_segment(const float* __restrict__ Zt, int Bp, int bl,
                                             const float* __restrict__ W2, int64_t ldw, int O,
                                             int64_t nbeg, int64_t nend, int g, int NG,
@@ -40,7 +40,7 @@ __device__ __forceinline__ void fwd_segment(const float* __restrict__ Zt, int Bp
     for (int u = 0; u < kU; ++u) {
       int64_t n = n0 + u * NG;
       if (n >= nend) n = nend - 1;
-      z[u] = *(const f32x4*)(Zt + n * Bp + bl);
+      z[u] = load_z4(Zt, ZB, n * Bp + bl);
 #pragma unroll
       for (int o = 0; o < OM; ++o) {
         const float v = W2[(int64_t)(o < O ? o : O - 1) * ldw + n];
@@ -60,7 +60,7 @@ __device__ __forceinline__ void fwd_segment(const float* __restrict__ Zt, int Bp
   }
 }
 
-template <int OM>
+template <int OM, bool ZB>
 __global__ __launch_bounds__(kBlock) void k_m3_fwd(
     const float* __restrict__ Zt, int Bp, int B, const float* __restrict__ W2, int64_t ldw,
     int O, const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
@@ -92,19 +92,19 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
 #pragma unroll
       for (int o = 0; o < OM; ++o) acc[i][o] = 0.f;
     switch (a) {
-      case 0: fwd_segment<OM, 0>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 1: fwd_segment<OM, 1>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 2: fwd_segment<OM, 2>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 3: fwd_segment<OM, 3>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 4: fwd_segment<OM, 4>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 5: fwd_segment<OM, 5>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 6: fwd_segment<OM, 6>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 7: fwd_segment<OM, 7>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 8: fwd_segment<OM, 8>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 9: fwd_segment<OM, 9>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 10: fwd_segment<OM, 10>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      case 11: fwd_segment<OM, 11>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
-      default: fwd_segment<OM, 12>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 0: fwd_segment<OM, 0, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 1: fwd_segment<OM, 1, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 2: fwd_segment<OM, 2, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 3: fwd_segment<OM, 3, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 4: fwd_segment<OM, 4, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 5: fwd_segment<OM, 5, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 6: fwd_segment<OM, 6, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 7: fwd_segment<OM, 7, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 8: fwd_segment<OM, 8, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 9: fwd_segment<OM, 9, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 10: fwd_segment<OM, 10, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      case 11: fwd_segment<OM, 11, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
+      default: fwd_segment<OM, 12, ZB>(Zt, Bp, bl, W2, ldw, O, n, se, g, NG, acc); break;
     }
     for (int s = LG; s < 64; s <<= 1)
 #pragma unroll
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd(
 // model's values.  One wave per (tile of whole segments, 16 NBB samples).
 // ---------------------------------------------------------------------------
 
-template <int NBB, int A>
+template <int NBB, int A, bool ZB>
 __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* __restrict__ Zt,
                                                int Bp, int b0, const float* __restrict__ wrow,
                                                bool orow_ok, int64_t nbeg, int64_t nend, int li,
@@ -169,17 +169,17 @@ __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* _
     for (int u = 0; u < kUM; ++u) {
       int64_t n = n0 + 4 * u + lk;
       if (n > nend - 1) n = nend - 1;
-      const float* zp = Zt + n * Bp + bl;
+      const int64_t zi = n * Bp + bl;
       if constexpr (NBB == 4) {
-        const f32x4 v = *(const f32x4*)zp;
+        const f32x4 v = load_z4(Zt, ZB, zi);
 #pragma unroll
         for (int i = 0; i < 4; ++i) z[u][i] = v[i];
       } else if constexpr (NBB == 2) {
-        const f32x2 v = *(const f32x2*)zp;
+        const f32x2 v = load_z2(Zt, ZB, zi);
         z[u][0] = v[0];
         z[u][1] = v[1];
       } else {
-        z[u][0] = zp[0];
+        z[u][0] = load_z1(Zt, ZB, zi);
       }
       w[u] = wrow[n];
     }
@@ -197,7 +197,7 @@ __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* _
   }
 }
 
-template <int NBB>
+template <int NBB, bool ZB>
 __global__ __launch_bounds__(kBlock) void k_m3_fwd_mf(
     const float* __restrict__ Zt, int Bp, int B, const float* __restrict__ W2, int64_t ldw,
     int O, const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
@@ -225,19 +225,19 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd_mf(
 #pragma unroll
     for (int i = 0; i < NBB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     switch (a) {
-      case 0: fwd_segment_mf<NBB, 0>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 1: fwd_segment_mf<NBB, 1>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 2: fwd_segment_mf<NBB, 2>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 3: fwd_segment_mf<NBB, 3>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 4: fwd_segment_mf<NBB, 4>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 5: fwd_segment_mf<NBB, 5>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 6: fwd_segment_mf<NBB, 6>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 7: fwd_segment_mf<NBB, 7>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 8: fwd_segment_mf<NBB, 8>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 9: fwd_segment_mf<NBB, 9>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 10: fwd_segment_mf<NBB, 10>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      case 11: fwd_segment_mf<NBB, 11>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
-      default: fwd_segment_mf<NBB, 12>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 0: fwd_segment_mf<NBB, 0, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 1: fwd_segment_mf<NBB, 1, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 2: fwd_segment_mf<NBB, 2, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 3: fwd_segment_mf<NBB, 3, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 4: fwd_segment_mf<NBB, 4, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 5: fwd_segment_mf<NBB, 5, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 6: fwd_segment_mf<NBB, 6, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 7: fwd_segment_mf<NBB, 7, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 8: fwd_segment_mf<NBB, 8, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 9: fwd_segment_mf<NBB, 9, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 10: fwd_segment_mf<NBB, 10, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      case 11: fwd_segment_mf<NBB, 11, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
+      default: fwd_segment_mf<NBB, 12, ZB>(acc, Zt, Bp, b0, wrow, orow_ok, n, se, li, lk); break;
     }
     if (orow_ok) {
       // the output bias goes with the piece that starts the segment
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(kBlock) void k_m3_fwd_mf(
 }
 
 template <int NBB>
-static void m3_fwd_mf_dispatch(const float* Zt, int32_t Bp, int32_t B, const float* W2,
+static void m3_fwd_mf_dispatch(const float* Zt, bool zb, int32_t Bp, int32_t B, const float* W2,
                                int64_t ldw, int32_t O, const int64_t* seg_off,
                                const int32_t* act, const Tile3* tiles, const int32_t* order, int32_t ntiles,
                                const float* b2, float* out, int64_t sm, int64_t sb,
@@ -268,12 +268,16 @@ static void m3_fwd_mf_dispatch(const float* Zt, int32_t Bp, int32_t B, const flo
   const int nbblk = ceil_div_i(Bp, 16 * NBB);
   const int64_t waves = (int64_t)ntiles * nbblk;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
-  k_m3_fwd_mf<NBB><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order,
+  if (zb)
+    k_m3_fwd_mf<NBB, true><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles,
+                                                     order, ntiles, nbblk, b2, out, sm, sb);
+  else
+    k_m3_fwd_mf<NBB, false><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order,
                                              ntiles, nbblk, b2, out, sm, sb);
 }
 
 template <int OM>
-static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float* W2,
+static void m3_fwd_dispatch(const float* Zt, bool zb, int32_t Bp, int32_t B, const float* W2,
                             int64_t ldw, int32_t O, const int64_t* seg_off, const int32_t* act,
                             const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
                             int64_t sm, int64_t sb, hipStream_t s) {
@@ -283,22 +287,26 @@ static void m3_fwd_dispatch(const float* Zt, int32_t Bp, int32_t B, const float*
   const int nbblk = ceil_div_i(Bp, BW);
   const int64_t waves = (int64_t)ntiles * nbblk;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
-  k_m3_fwd<OM><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles,
+  if (zb)
+    k_m3_fwd<OM, true><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles,
+                                                 order, ntiles, BW, LG, nbblk, b2, out, sm, sb);
+  else
+    k_m3_fwd<OM, false><<<blocks, kBlock, 0, s>>>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles,
                                          BW, LG, nbblk, b2, out, sm, sb);
 }
 
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
                          const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
-                         int64_t sm, int64_t sb, hipStream_t s) {
+                         int64_t sm, int64_t sb, hipStream_t s, bool zb) {
   if (ntiles <= 0) return hipSuccess;
   note_variant(O <= 4 ? "k_m3_fwd" : "k_m3_fwd_mf", O <= 4 ? kArithNone : kArithFp32);
-  if (O <= 2) m3_fwd_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
-  else if (O <= 4) m3_fwd_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  if (O <= 2) m3_fwd_dispatch<2>(Zt, zb, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else if (O <= 4) m3_fwd_dispatch<4>(Zt, zb, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
   // wider output layers: one MFMA per four units and 16 samples
-  else if (Bp <= 16) m3_fwd_mf_dispatch<1>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
-  else if (Bp <= 32) m3_fwd_mf_dispatch<2>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
-  else m3_fwd_mf_dispatch<4>(Zt, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else if (Bp <= 16) m3_fwd_mf_dispatch<1>(Zt, zb, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else if (Bp <= 32) m3_fwd_mf_dispatch<2>(Zt, zb, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
+  else m3_fwd_mf_dispatch<4>(Zt, zb, Bp, B, W2, ldw, O, seg_off, act, tiles, order, ntiles, b2, out, sm, sb, s);
   return hipGetLastError();
 }
 
@@ -321,9 +329,9 @@ hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2
 
 static constexpr int kT5 = 256;
 
-template <int OM, int A>
-__device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, unsigned short* __restrict__ dZ16,
-                                            int Bp, int bl, bool bvalid,
+template <int OM, int A, bool ZB>
+__device__ __forceinline__ void bwd_segment(float* __restrict__ Zt,
+                                            unsigned short* __restrict__ dZ16, int Bp, int bl, bool bvalid,
                                             const float* __restrict__ W2, int64_t ldw, int O,
                                             int64_t nbeg, int64_t nend, int g, int NG, int LG,
                                             int pp, const float (&gr)[4][OM],
@@ -335,7 +343,7 @@ __device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, unsigned sho
     for (int u = 0; u < kU; ++u) {
       int64_t n = n0 + u * NG;
       if (n >= nend) n = nend - 1;
-      z[u] = *(const f32x4*)(Zt + n * Bp + bl);
+      z[u] = load_z4(Zt, ZB, n * Bp + bl);
 #pragma unroll
       for (int o = 0; o < OM; ++o) {
         const float v = W2[(int64_t)(o < O ? o : O - 1) * ldw + n];
@@ -382,9 +390,10 @@ __device__ __forceinline__ void bwd_segment(float* __restrict__ Zt, unsigned sho
   }
 }
 
-template <int OM, bool GRAD>
+template <int OM, bool GRAD, bool ZB>
 __global__ __launch_bounds__(kBlock) void k_m3_bwd(
-    float* __restrict__ Zt, unsigned short* __restrict__ dZ16, int Bp, float* __restrict__ W2,
+    float* __restrict__ Zt, unsigned short* __restrict__ dZ16, int Bp,
+    float* __restrict__ W2,
     int64_t N, int64_t ldw, int O, const int32_t* __restrict__ mid,
     const int64_t* __restrict__ seg_off, const int32_t* __restrict__ act,
     const float* __restrict__ G, int LG, int slots, float lr, const float* __restrict__ lrm,
@@ -421,19 +430,19 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
           }
         const bool first = slot == 0;
         switch (a) {
-          case 0: bwd_segment<OM, 0>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 1: bwd_segment<OM, 1>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 2: bwd_segment<OM, 2>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 3: bwd_segment<OM, 3>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 4: bwd_segment<OM, 4>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 5: bwd_segment<OM, 5>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 6: bwd_segment<OM, 6>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 7: bwd_segment<OM, 7>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 8: bwd_segment<OM, 8>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 9: bwd_segment<OM, 9>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 10: bwd_segment<OM, 10>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          case 11: bwd_segment<OM, 11>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
-          default: bwd_segment<OM, 12>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 0: bwd_segment<OM, 0, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 1: bwd_segment<OM, 1, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 2: bwd_segment<OM, 2, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 3: bwd_segment<OM, 3, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 4: bwd_segment<OM, 4, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 5: bwd_segment<OM, 5, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 6: bwd_segment<OM, 6, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 7: bwd_segment<OM, 7, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 8: bwd_segment<OM, 8, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 9: bwd_segment<OM, 9, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 10: bwd_segment<OM, 10, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          case 11: bwd_segment<OM, 11, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
+          default: bwd_segment<OM, 12, ZB>(Zt, dZ16, Bp, bl, bvalid, W2, ldw, O, n, se, g, NG, LG, pp, gr, dwl, r0, first); break;
         }
         n = se;
         ++m;
@@ -453,7 +462,7 @@ __global__ __launch_bounds__(kBlock) void k_m3_bwd(
 }
 
 template <int OM>
-static void m3_bwd_dispatch(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
+static void m3_bwd_dispatch(float* Zt, bool zb, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
                             int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
                             const int32_t* act, const float* G, float lr, const float* lrm,
                             float* dW2, hipStream_t s) {
@@ -466,24 +475,30 @@ static void m3_bwd_dispatch(float* Zt, unsigned short* dZ16, int32_t Bp, float* 
   const int slots = ceil_div_i(Bp, 4 * LG);
   const int64_t waves = (N + kT5 - 1) / kT5;
   const unsigned blocks = (unsigned)((waves + 3) / 4);
-  if (dW2)
-    k_m3_bwd<OM, true><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act,
-                                                 G, LG, slots, lr, lrm, dW2);
+  if (dW2 && zb)
+    k_m3_bwd<OM, true, true><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off,
+                                                       act, G, LG, slots, lr, lrm, dW2);
+  else if (dW2)
+    k_m3_bwd<OM, true, false><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off,
+                                                        act, G, LG, slots, lr, lrm, dW2);
+  else if (zb)
+    k_m3_bwd<OM, false, true><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off,
+                                                        act, G, LG, slots, lr, lrm, dW2);
   else
-    k_m3_bwd<OM, false><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act,
-                                                  G, LG, slots, lr, lrm, dW2);
+    k_m3_bwd<OM, false, false><<<blocks, kBlock, 0, s>>>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off,
+                                                         act, G, LG, slots, lr, lrm, dW2);
 }
 
 hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
                          int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
                          const int32_t* act, const float* G, float lr, const float* lrm,
-                         float* dW2, hipStream_t s) {
+                         float* dW2, hipStream_t s, bool zb) {
   note_variant("k_m3_bwd", kArithNone);
-  if (O <= 2) m3_bwd_dispatch<2>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
-  else if (O <= 4) m3_bwd_dispatch<4>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
-  else if (O <= 8) m3_bwd_dispatch<8>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
-  else if (O <= 10) m3_bwd_dispatch<10>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
-  else m3_bwd_dispatch<16>(Zt, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  if (O <= 2) m3_bwd_dispatch<2>(Zt, zb, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else if (O <= 4) m3_bwd_dispatch<4>(Zt, zb, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else if (O <= 8) m3_bwd_dispatch<8>(Zt, zb, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else if (O <= 10) m3_bwd_dispatch<10>(Zt, zb, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
+  else m3_bwd_dispatch<16>(Zt, zb, dZ16, Bp, W2, N, ldw, O, mid, seg_off, act, G, lr, lrm, dW2, s);
   return hipGetLastError();
 }
 

@@ -362,7 +362,7 @@ hipError_t launch_mse(float* LG, const float* Y, int32_t M, int32_t Bp, int32_t 
 // Hidden layer in the caller's [B][N] layout (inspection path).
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void k_hidden_out(const float* __restrict__ Zt, int Bp,
+__global__ __launch_bounds__(kBlock) void k_hidden_out(const float* __restrict__ Zt, bool zb, int Bp,
                                                        int B, int64_t N,
                                                        const int32_t* __restrict__ mid,
                                                        const int32_t* __restrict__ act,
@@ -373,7 +373,7 @@ __global__ __launch_bounds__(kBlock) void k_hidden_out(const float* __restrict__
        i += (int64_t)gridDim.x * kBlock) {
     const int64_t b = i / N;
     const int64_t n = i - b * N;
-    const float z = Zt[n * Bp + b];
+    const float z = load_z1(Zt, zb, n * Bp + b);
     if (Z) Z[i] = z;
     if (H) H[i] = act_fwd(act[mid[n]], z);
   }
@@ -381,9 +381,9 @@ __global__ __launch_bounds__(kBlock) void k_hidden_out(const float* __restrict__
 
 hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              const int32_t* mid, const int32_t* act, float* Z, float* H,
-                             hipStream_t s) {
+                             hipStream_t s, bool zb) {
   note_variant("k_hidden_out", kArithNone);
-  k_hidden_out<<<grid_for((int64_t)B * N), kBlock, 0, s>>>(Zt, Bp, B, N, mid, act, Z, H);
+  k_hidden_out<<<grid_for((int64_t)B * N), kBlock, 0, s>>>(Zt, zb, Bp, B, N, mid, act, Z, H);
   return hipGetLastError();
 }
 

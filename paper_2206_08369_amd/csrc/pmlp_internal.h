@@ -98,7 +98,8 @@ struct GemmBfArgs {
   const int32_t* mid;       // model of each row p (with lrm)
   float* db1;               // EPI_GRAD: column bcol (the hidden bias) goes to db1[p]
   int32_t bcol;
-  unsigned short* outb;     // EPI_SGD: also store bf16 of the updated values (or null)
+  unsigned short* outb;     // EPI_SGD: also store bf16 of the updated values (or null);
+                            // EPI_STORE: store bf16 of C here instead of fp32 to out
   int64_t ldob;
   const uint32_t* fmask;    // EPI_SGD / EPI_GRAD: per-model feature masks (null: none)
   int32_t fmw;              // words per model of fmask
@@ -202,7 +203,7 @@ hipError_t launch_pack_x_bf16(const float* X, int32_t B, int32_t F, int32_t Bp, 
 hipError_t launch_m3_fwd(const float* Zt, int32_t Bp, int32_t B, const float* W2, int64_t ldw,
                          int32_t O, const int64_t* seg_off, const int32_t* act,
                          const Tile3* tiles, const int32_t* order, int32_t ntiles, const float* b2, float* out,
-                         int64_t sm, int64_t sb, hipStream_t s);
+                         int64_t sm, int64_t sb, hipStream_t s, bool zb = false);
 
 // flag[0] is raised by a label outside [0, O), flag[1] by a non-finite
 // per-model rate in lrm (may be null); flag[2] counts models whose loss is
@@ -226,11 +227,11 @@ hipError_t launch_mse(float* LG, const float* Y, int32_t M, int32_t Bp, int32_t 
 hipError_t launch_m3_bwd(float* Zt, unsigned short* dZ16, int32_t Bp, float* W2, int64_t N,
                          int64_t ldw, int32_t O, const int32_t* mid, const int64_t* seg_off,
                          const int32_t* act, const float* G, float lr, const float* lrm,
-                         float* dW2, hipStream_t s);
+                         float* dW2, hipStream_t s, bool zb = false);
 
 hipError_t launch_hidden_out(const float* Zt, int32_t Bp, int32_t B, int64_t N,
                              const int32_t* mid, const int32_t* act, float* Z, float* H,
-                             hipStream_t s);
+                             hipStream_t s, bool zb = false);
 
 hipError_t launch_fill(float* p, int64_t n, float v, hipStream_t s);
 

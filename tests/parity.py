@@ -75,7 +75,8 @@ def dw2_terms(orc, hs, acts, W1, W2, X, y, **kw):
     with two outputs has dW2[1] = -dW2[0], often small), so, as for db2,
     its per-model error is taken relative to this size rather than to
     |dW2|; where nothing cancels the two agree."""
-    _, H = orc.hidden(hs, acts, W1, X, **{k: v for k, v in kw.items() if k in ("rounding", "b1", "mask")})
+    _, H = orc.hidden(hs, acts, W1, X, **{k: v for k, v in kw.items()
+                                          if k in ("rounding", "b1", "mask", "stored_z", "zband")})
     L = orc.forward(hs, acts, W1, W2, X, **kw)
     P = np.exp(L - L.max(axis=2, keepdims=True))
     P /= P.sum(axis=2, keepdims=True)

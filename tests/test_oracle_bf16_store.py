@@ -184,3 +184,25 @@ def test_stored_z_mode_does_not_leak(orc):
     assert np.array_equal(orc.forward(hs, acts, W1, W2, X), exact)
     with pytest.raises(ValueError):
         orc.hidden(hs, acts, W1, X, rounding="bf16_store", stored_z=np.zeros((9, 3), np.float32))
+
+
+def test_stored_z_choice_under_cancellation(orc):
+    """Z = 2 - 2 + 2^-20 (terms of size 4): every bfloat16 whose rounding
+    interval comes within band * 4 of Z is a correct stored value, here
+    also one two units of 2^-27 away, as long as the band reaches it."""
+    hs = np.asarray([1], np.int32)
+    acts = np.asarray([0], np.int32)
+    X = np.ones((1, 3), np.float32)
+    W1 = np.asarray([[2.0, -2.0, 2.0 ** -20]], np.float64)
+    Z, _ = orc.hidden(hs, acts, W1, X, rounding="bf16_store")
+    assert Z[0, 0] == 2.0 ** -20
+    two_away = np.asarray([[2.0 ** -20 + 2.0 ** -26]], np.float32)   # two bfloat16 units up
+    # its rounding interval starts 2^-26 - 2^-28 = 1.1e-8 above Z
+    Zc, _ = orc.hidden(hs, acts, W1, X, rounding="bf16_store", stored_z=two_away, zband=1e-6)
+    assert Zc[0, 0] == two_away[0, 0] and orc.stored_z_conflicts() == 0
+    Zn, _ = orc.hidden(hs, acts, W1, X, rounding="bf16_store", stored_z=two_away, zband=1e-9)
+    assert Zn[0, 0] == 2.0 ** -20 and orc.stored_z_conflicts() == 1
+    # a value that is not a bfloat16 is never taken
+    odd = np.asarray([[2.0 ** -20 * (1 + 2.0 ** -12)]], np.float32)
+    Zo, _ = orc.hidden(hs, acts, W1, X, rounding="bf16_store", stored_z=odd, zband=1e-6)
+    assert Zo[0, 0] == 2.0 ** -20 and orc.stored_z_conflicts() == 1
