@@ -1644,24 +1644,45 @@ static hipError_t bwd_mf_go(const BwdArgs& a, size_t lds, hipStream_t s) {
   return launch_persistent(k_bwd_mf<TQ, 2, NT>, NT, lds, T, s, a);
 }
 
-// Batches of 128 and 256 samples with F4 = 100 or 52 (six or three column
-// blocks and the four-column tail) and O = 2: the bf16 three-piece kernel.
+// Batches of 128 and 256 samples with F4 = 16 TQ or 16 TQ + 4 (TQ column
+// blocks and the four-column tail), 32 <= F4 <= 128, and O = 2 or 4: the
+// bf16 three-piece kernel.
 static size_t bwd_x3_bytes(int32_t Bp, int32_t F4) {
   const int tq = F4 / 16, nc = Bp / 32;
   return (size_t)3 * (tq * nc * 64 + (F4 % 16 ? nc * 16 : 0)) * 16 + (F4 % 16 ? 16 : 0);
 }
 
 static bool bwd_x3_shape(const BwdArgs& a) {
-  return (a.Bp == 128 || a.Bp == 256) && a.O == 2 && (a.F4 == 100 || a.F4 == 52) &&
+  return (a.Bp == 128 || a.Bp == 256) && (a.O == 2 || a.O == 4) && a.F4 >= 32 &&
+         a.F4 <= 128 && (a.F4 % 16 == 0 || a.F4 % 16 == 4) &&
          bwd_x3_bytes(a.Bp, a.F4) <= (size_t)dev_info().lds_max;
+}
+
+template <int TQ, int OM, bool TAIL>
+static hipError_t bwd_x3_go_t(const BwdArgs& a, size_t lds, int64_t T, hipStream_t s) {
+  return launch_persistent(k_bwd_x3<TQ, OM, 2, 512, TAIL>, 512, lds, T, s, a);
+}
+
+template <int OM>
+static hipError_t bwd_x3_go_o(const BwdArgs& a, size_t lds, int64_t T, hipStream_t s) {
+  const bool tail = a.F4 % 16 != 0;
+  switch (a.F4 / 16) {
+    case 2: return tail ? bwd_x3_go_t<2, OM, true>(a, lds, T, s) : bwd_x3_go_t<2, OM, false>(a, lds, T, s);
+    case 3: return tail ? bwd_x3_go_t<3, OM, true>(a, lds, T, s) : bwd_x3_go_t<3, OM, false>(a, lds, T, s);
+    case 4: return tail ? bwd_x3_go_t<4, OM, true>(a, lds, T, s) : bwd_x3_go_t<4, OM, false>(a, lds, T, s);
+    case 5: return tail ? bwd_x3_go_t<5, OM, true>(a, lds, T, s) : bwd_x3_go_t<5, OM, false>(a, lds, T, s);
+    case 6: return tail ? bwd_x3_go_t<6, OM, true>(a, lds, T, s) : bwd_x3_go_t<6, OM, false>(a, lds, T, s);
+    case 7: return tail ? bwd_x3_go_t<7, OM, true>(a, lds, T, s) : bwd_x3_go_t<7, OM, false>(a, lds, T, s);
+    default: return bwd_x3_go_t<8, OM, false>(a, lds, T, s);
+  }
 }
 
 static hipError_t bwd_x3_go(const BwdArgs& a, hipStream_t s) {
   const int64_t T = (a.N + 15) / 16;
   const size_t lds = bwd_x3_bytes(a.Bp, a.F4);
   note_variant("k_bwd_x3", kArithX3);
-  if (a.F4 == 100) return launch_persistent(k_bwd_x3<6, 2, 2, 512, true>, 512, lds, T, s, a);
-  return launch_persistent(k_bwd_x3<3, 2, 2, 512, true>, 512, lds, T, s, a);
+  if (a.O == 4) return bwd_x3_go_o<4>(a, lds, T, s);
+  return bwd_x3_go_o<2>(a, lds, T, s);
 }
 
 template <int TQ, int OM, bool TAIL = false>

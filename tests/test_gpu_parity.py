@@ -97,6 +97,15 @@ CASES = {
     "fm3_mixed_b128": dict(hs=[1] * 40 + [7, 9, 16, 32, 17, 1300, 2, 3, 64, 513],
                            F=100, O=2, B=100),
     "fm3_f128_b128": dict(M=40, hmax=90, F=128, O=2, B=128),
+    # the three-piece fused backward at other column counts and four
+    # outputs: five blocks, two and seven blocks with the four-column tail,
+    # four blocks at O = 4; 116 columns at 256 samples exceed LDS and take
+    # the fp32 kernels
+    "bx3_f80_b256": dict(M=20, hmax=150, F=80, O=2, B=256),
+    "bx3_f36_b128_o4": dict(M=25, hmax=100, F=36, O=4, B=128),
+    "bx3_f116_b120": dict(M=15, hmax=120, F=116, O=2, B=120),
+    "f116_b200": dict(M=15, hmax=120, F=116, O=2, B=200),
+    "bx3_f64_b256_o4": dict(M=20, hmax=100, F=64, O=4, B=256),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
@@ -228,7 +237,8 @@ def test_gradients_and_losses(pm, orc, torch, name, path):
 
 
 @pytest.mark.parametrize("name", ["ragged", "tile_spanning", "o10_b32", "b300_f100",
-                                  "f100_b250", "f128_b100_o4", "f32_b32_o10", "fm3_mixed_b256"])
+                                  "f100_b250", "f128_b100_o4", "f32_b32_o10", "fm3_mixed_b256",
+                                  "bx3_f36_b128_o4", "bx3_f116_b120"])
 def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name, path):
     """The fused update equals W - lr * dW with dW from the gradient mode
     (to fp32 rounding of W), and the step's losses match the oracle."""
@@ -438,7 +448,10 @@ VARIANTS = [
     ((100, 2, 256, "default", "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
     ((100, 2, 256, "fused_forward", "fp32"), ("k_fwd_x3m", 2), ("k_bwd_x3", 2)),
     ((50, 2, 128, "fused_forward", "fp32"), ("k_fwd_x3m", 2), ("k_bwd_x3", 2)),
-    ((100, 4, 256, "fused_forward", "fp32"), ("k_fwd_x3", 2), ("k_bwd_lds", 1)),
+    ((100, 4, 256, "fused_forward", "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
+    ((40, 2, 256, "default", "fp32"), ("k_fwd_x3", 2), ("k_bwd_lds", 1)),
+    ((116, 2, 120, "default", "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
+    ((116, 2, 200, "default", "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
     ((32, 10, 32, "default", "fp32"), ("k_fwd_lds_ring", 1), ("k_bwd_mf", 1)),
     ((20, 2, 100, "default", "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
     ((100, 2, 256, "generic", "fp32"), ("k_gemm_nt", 1), None),
