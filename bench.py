@@ -23,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -107,7 +108,8 @@ def traffic_key(kernel: str, workload: str, precision: str) -> str:
 
 def load_traffic(kernel: str, workload: str, precision: str = "fp32"):
     """HBM bytes per launch from committed rocprofv3 counter summaries, if
-    they were taken on the current kernel source; otherwise None."""
+    they were taken on the current source of the kernel they name; otherwise
+    None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -116,31 +118,36 @@ def load_traffic(kernel: str, workload: str, precision: str = "fp32"):
     except ValueError:
         return None
     ent = table.get(traffic_key(kernel, workload, precision))
-    if not ent or ent.get("kernels_sha") != kernel_source_digest(kernel, precision):
+    if not ent or ent.get("kernels_sha") != kernel_source_digest(ent.get("kernel", "")):
         return None
     return ent.get("bytes_per_launch")
 
 
-# Source file that defines each timed kernel, per precision mode (the shared
-# headers are hashed with it).
-KERNEL_SOURCE = {
-    "fp32": {"gemm_fwd": "k_lds.hip", "fwd_m3": "k_lds.hip", "bwd_fused": "k_lds.hip",
-             "gemm_bwd": "k_gemm.hip",
-             "m3_fwd": "k_m3.hip", "m3_bwd": "k_m3.hip", "ce": "k_misc.hip",
-             "pack_x": "k_misc.hip", "aux": "k_misc.hip"},
-    "bf16": {"gemm_fwd": "k_gemm_bf16.hip", "gemm_bwd": "k_gemm_bf16.hip",
-             "m3_fwd": "k_m3.hip", "m3_bwd": "k_m3.hip", "ce": "k_misc.hip",
-             "pack_x": "k_misc.hip", "aux": "k_misc.hip"},
-}
-KERNEL_SOURCE["bf16_store"] = KERNEL_SOURCE["bf16"]
+# variants the library reports under their own name that are instances of
+# another kernel
+VARIANT_KERNEL = {"k_gemm_x3": "k_gemm_bf"}
 
 
-def kernel_source_digest(kernel: str = None, precision: str = "fp32") -> str:
-    """sha256 (16 hex digits) over the source of one kernel and the shared
-    headers (all HIP sources when the kernel is not named)."""
+def kernel_source(kernel: str):
+    """Source file (under csrc/) that defines a kernel, given the name the
+    library reports or a trace shows (template arguments are ignored)."""
+    base = kernel.split("<")[0].strip()
+    base = VARIANT_KERNEL.get(base, base)
+    csrc = os.path.join(ROOT, "paper_2206_08369_amd", "csrc")
+    pat = re.compile(r"\bvoid\s+%s\s*\(" % re.escape(base))
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith(".hip") and pat.search(open(os.path.join(csrc, name)).read()):
+            return name
+    return None
+
+
+def kernel_source_digest(kernel: str = None) -> str:
+    """sha256 (16 hex digits) over the source file of one kernel and the
+    shared headers (all HIP sources when the kernel is not named or not
+    found)."""
     csrc = os.path.join(ROOT, "paper_2206_08369_amd", "csrc")
     names = sorted(n for n in os.listdir(csrc) if n.endswith((".hip", ".h")))
-    src = KERNEL_SOURCE.get(precision, {}).get(kernel) if kernel else None
+    src = kernel_source(kernel) if kernel else None
     if src:
         names = sorted(n for n in names if n.endswith(".h") or n == src)
     h = hashlib.sha256()

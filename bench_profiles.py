@@ -272,7 +272,7 @@ def main(argv):
             name, role, f_k, w_k, hbm, alg, "%.3f" % (hbm / alg) if alg else "-"))
         table[bench.traffic_key(role, wk, prec)] = {
             "kernel": name, "bytes_per_launch": hbm, "fetch_kib": f_k, "write_kib": w_k,
-            "kernels_sha": bench.kernel_source_digest(role, prec)}
+            "kernels_sha": bench.kernel_source_digest(name)}
     lines += ["", "Each entry of `profiles/traffic.json` carries the hash of its kernel's source file "
               "and the shared headers; `bench.py` reports `traffic` only while it matches."]
     open(os.path.join(ROOT, "profiles", "traffic_%s.md" % tag), "w").write("\n".join(lines) + "\n")

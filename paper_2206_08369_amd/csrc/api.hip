@@ -453,6 +453,21 @@ int forward_hidden(pmlp* h, const float* X, int32_t B, int32_t Bp, const Work& w
     f.K = h->F4;
     return run(h, KID_GEMM_FWD, [&] { return launch_fwd_lds(f, h->stream); });
   }
+  if (h->lds_kernels) {  // fp32 accuracy on the bf16 matrix cores
+    GemmBfArgs g{};
+    g.P = h->W1;
+    g.ldp = h->F4;
+    g.kp = h->F4;
+    g.NP = h->N;
+    g.Qf = w.Xp;
+    g.ldq = h->F4;
+    g.NQ = Bp;
+    g.K = h->F4;
+    g.out = w.Zt;
+    g.ldo = Bp;
+    g.ncols = Bp;
+    return run(h, KID_GEMM_FWD, [&] { return launch_gemm_bf16(g, EPI_STORE, h->stream); });
+  }
   GemmArgs g{};
   g.P = h->W1;
   g.ldp = h->F4;
@@ -609,6 +624,33 @@ int step(pmlp* h, const float* X, const void* y, int32_t B, float lr, const floa
     g.bcol = h->bcol;
     g.outb = dW1 ? nullptr : h->W1b;  // the update keeps the bf16 copy current
     g.ldob = bf16_ld(h->F4);
+    g.fmask = h->d_fmask;
+    g.fmw = h->fmw;
+    if (int rc = run(h, KID_GEMM_BWD, [&] {
+          return launch_gemm_bf16(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
+        }))
+      return rc;
+    h->have_loss = true;
+    return PMLP_OK;
+  }
+  if (h->lds_kernels) {  // fp32 accuracy on the bf16 matrix cores
+    GemmBfArgs g{};
+    g.P = w.Zt;
+    g.ldp = Bp;
+    g.kp = Bp;
+    g.NP = h->N;
+    g.Qf = w.Xt;
+    g.ldq = Bp;
+    g.NQ = h->F4;
+    g.K = Bp;
+    g.out = dW1 ? dW1 : h->W1;
+    g.ldo = dW1 ? h->F : h->F4;
+    g.ncols = h->F;
+    g.lr = lr;
+    g.lrm = lrm;
+    g.mid = h->d_mid;
+    g.db1 = dW1 ? db1 : nullptr;
+    g.bcol = h->bcol;
     g.fmask = h->d_fmask;
     g.fmw = h->fmw;
     if (int rc = run(h, KID_GEMM_BWD, [&] {

@@ -1,7 +1,15 @@
-// Input-layer GEMMs with bf16 operands and fp32 accumulation on the bf16
-// matrix cores (the bf16-in / fp32-accumulate precision mode).
+// Input-layer GEMMs on the bf16 matrix cores with fp32 accumulation, in
+// two arithmetics:
 //
-//   C[p][q] = sum_k bf16(P[p][k]) * Q[q][k]
+// * bf16 operands (the bf16-in / fp32-accumulate precision mode):
+//     C[p][q] = sum_k bf16(P[p][k]) * Q[q][k]
+// * fp32 accuracy from three-piece splits (the fp32 mode, for the shapes the
+//   LDS-resident kernels do not take): both operands fp32, each element split
+//   as it is staged into bf16 pieces a = a0 + a1 + a2 (every piece the
+//   round-to-nearest of what the previous ones leave, exact for normal a),
+//   and every k step taken as the six piece products q2 p0, q1 p1, q0 p2,
+//   q1 p0, q0 p1, q0 p0 in fp32 accumulation; the three left out are at most
+//   2^-23 of each product, so C carries the error of an fp32 dot product.
 //
 // P is the big fp32 operand (W1 for the forward product of Section 3 step 1,
 // dZ^T for dW1), rounded to bf16 (nearest even, v_cvt_pk_bf16_f32) as it is
@@ -25,6 +33,10 @@
 // every wave reads its fragments with conflict-free ds_read_b128.  Two LDS
 // stages: the global loads of stage k+1 are in flight during the MFMAs of
 // stage k, one barrier per stage.
+//
+// In the three-piece mode each operand has three LDS planes per stage (the
+// pieces), the stage is 16 k deep (one MFMA k step), and k past K reads as
+// zero on both operands.
 //
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8, and the nqt
 // q-tiles of one p-tile are consecutive workgroups of the same XCD, so the
@@ -56,7 +68,16 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const f32x4& a, const f32x4& b) {
   return __builtin_bit_cast(u32x4, r);
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, int EPI>
+// Three bf16 pieces of four fp32 values: v = p0 + p1 + p2, each piece the
+// round-to-nearest-even of the remainder (exact subtractions in fp32).
+__device__ __forceinline__ void split3x4(const f32x4& v, bf16x4& p0, bf16x4& p1, bf16x4& p2) {
+  p0 = __builtin_convertvector(v, bf16x4);
+  const f32x4 r1 = v - __builtin_convertvector(p0, f32x4);
+  p1 = __builtin_convertvector(r1, bf16x4);
+  p2 = __builtin_convertvector(r1 - __builtin_convertvector(p1, f32x4), bf16x4);
+}
+
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, int EPI, bool X3 = false>
 __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   constexpr int NT = 64 * WP * WQ;
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
@@ -66,17 +87,22 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   // one wave load covers whole cache lines of a few rows.  fp32 P chunks are
   // four fp32 (half of one lane's 8-k bf16 operand entry); bf16 P (PB) and
   // Q chunks are eight bf16.
-  constexpr int PE = PB ? 8 : 4;           // P elements per chunk
-  constexpr int CP = KS / PE, CQ = KS / 8;  // chunks per row and stage
+  // In the three-piece mode Q is fp32 too (four per chunk).
+  static_assert(!X3 || (!PB && KS == 16), "three-piece mode: fp32 P, one k step per stage");
+  constexpr int PE = PB ? 8 : 4;            // P elements per chunk
+  constexpr int QE = X3 ? 4 : 8;            // Q elements per chunk
+  constexpr int CP = KS / PE, CQ = KS / QE;  // chunks per row and stage
   constexpr int LP = (MP * CP + NT - 1) / NT, LQ = (MQ * CQ + NT - 1) / NT;
   static_assert((MP * CP) % NT == 0 || MP * CP < NT, "loader shape");
   static_assert((MQ * CQ) % NT == 0 || MQ * CQ < NT, "loader shape");
   static_assert((MP * CP) % 64 == 0 && (MQ * CQ) % 64 == 0, "loader shape");
-  constexpr int PS = MP * 2 * NS, QS = MQ * 2 * NS;  // 16-byte entries per stage
+  constexpr int PS = MP * 2 * NS, QS = MQ * 2 * NS;  // 16-byte entries per plane and stage
+  constexpr int PL = X3 ? 3 : 1;                     // planes (pieces) per operand
+  constexpr int SS = PL * (PS + QS);                 // entries per stage
   // epilogue scratch: QB adjacent 32 x 32 blocks per wave, rows padded by 4
   constexpr int QB = TQ % 2 == 0 ? 2 : 1, LDT = 32 * QB + 4;
   constexpr int SCR = NT / 64 * 32 * LDT / 4;  // 16-byte units
-  constexpr int LDSN = 2 * (PS + QS) > SCR ? 2 * (PS + QS) : SCR;
+  constexpr int LDSN = 2 * SS > SCR ? 2 * SS : SCR;
   __shared__ u32x4 lds[LDSN];
 
   const int blk = blockIdx.x;
@@ -112,30 +138,37 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
     pk[e] = k;
     poff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (PB ? 0 : 8 * (c & 1));
   }
-  const unsigned short* qptr[LQ];
-  int qoff[LQ];
+  typedef typename std::conditional<X3, float, unsigned short>::type QT;
+  const QT* qbase = X3 ? (const QT*)a.Qf : (const QT*)a.Q;
+  const QT* qptr[LQ];
+  int qk[LQ], qoff[LQ];
 #pragma unroll
   for (int e = 0; e < LQ; ++e) {
     const int idx = (t + e * NT) % (MQ * CQ), row = idx / CQ, c = idx % CQ;
     const int q = min(q0 + row, a.NQ - 1);
-    const int k = 8 * c, h = k / KH, st = (k % KH) / 8;
-    qptr[e] = a.Q + (int64_t)q * a.ldq + k;
-    qoff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16;
+    const int k = QE * c, h = k / KH, st = (k % KH) / 8;
+    qptr[e] = qbase + (int64_t)q * a.ldq + k;
+    qk[e] = k;
+    qoff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (X3 ? 8 * (c & 1) : 0);
   }
 
   // Global loads of one stage into registers, without branches so that the
   // compiler's wait counts stay exact: the stage index is clamped to the
   // last stage, and P reads at or past kp (the last stage when kp is not a
   // multiple of KS) are redirected to the start of the row, a finite value
-  // that meets the zero padding of Q.
+  // that meets the zero padding of Q.  In the three-piece mode Q reads at or
+  // past K are redirected the same way, and both operands' chunks past the
+  // end are stored as zero.
   struct Regs {
     u32x4 p[LP];
     u32x4 q[LQ];
+    int k0;
   };
   const int K = a.K, kp = a.kp;
   const int nk = (K + KS - 1) / KS;
   auto load = [&](Regs& r, int kt) {
     const int k0 = min(kt, nk - 1) * KS;
+    r.k0 = k0;
 #pragma unroll
     for (int e = 0; e < LP; ++e) {
       if (MP * CP < NT && t >= MP * CP) continue;
@@ -145,12 +178,36 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
 #pragma unroll
     for (int e = 0; e < LQ; ++e) {
       if (MQ * CQ < NT && t >= MQ * CQ) continue;
-      r.q[e] = *(const u32x4*)(qptr[e] + k0);
+      const int off = !X3 || k0 + qk[e] < K ? k0 : -qk[e];
+      r.q[e] = *(const u32x4*)(qptr[e] + off);
     }
   };
   auto store = [&](const Regs& r, int sb) {
-    char* ps = (char*)(lds + sb * (PS + QS));
-    char* qs = ps + PS * 16;
+    char* ps = (char*)(lds + sb * SS);
+    char* qs = ps + PL * PS * 16;
+    if constexpr (X3) {
+#pragma unroll
+      for (int e = 0; e < LP; ++e) {
+        if (MP * CP < NT && t >= MP * CP) continue;
+        const f32x4 f = r.k0 + pk[e] < kp ? __builtin_bit_cast(f32x4, r.p[e]) : f32x4{0, 0, 0, 0};
+        bf16x4 v0, v1, v2;
+        split3x4(f, v0, v1, v2);
+        *(bf16x4*)(ps + poff[e]) = v0;
+        *(bf16x4*)(ps + PS * 16 + poff[e]) = v1;
+        *(bf16x4*)(ps + 2 * PS * 16 + poff[e]) = v2;
+      }
+#pragma unroll
+      for (int e = 0; e < LQ; ++e) {
+        if (MQ * CQ < NT && t >= MQ * CQ) continue;
+        const f32x4 f = r.k0 + qk[e] < K ? __builtin_bit_cast(f32x4, r.q[e]) : f32x4{0, 0, 0, 0};
+        bf16x4 v0, v1, v2;
+        split3x4(f, v0, v1, v2);
+        *(bf16x4*)(qs + qoff[e]) = v0;
+        *(bf16x4*)(qs + QS * 16 + qoff[e]) = v1;
+        *(bf16x4*)(qs + 2 * QS * 16 + qoff[e]) = v2;
+      }
+      return;
+    }
 #pragma unroll
     for (int e = 0; e < LP; ++e) {
       if (MP * CP < NT && t >= MP * CP) continue;
@@ -182,8 +239,32 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   auto compute = [&](int sb) {
-    const u32x4* ps = lds + sb * (PS + QS);
-    const u32x4* qs = ps + PS;
+    const u32x4* ps = lds + sb * SS;
+    const u32x4* qs = ps + PL * PS;
+    if constexpr (X3) {
+      // the six piece products, smallest first; each pass over the TQ x TP
+      // blocks issues independent MFMAs back to back
+      constexpr int QI[6] = {2, 1, 0, 1, 0, 0}, PI[6] = {0, 1, 2, 0, 1, 0};
+      bf16x8 pf[3][TP], qf[3][TQ];
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+#pragma unroll
+        for (int j = 0; j < TP; ++j)
+          pf[c][j] = __builtin_bit_cast(bf16x8, ps[c * PS + entry(wp * TP + j, 0, lane)]);
+#pragma unroll
+        for (int i = 0; i < TQ; ++i)
+          qf[c][i] = __builtin_bit_cast(bf16x8, qs[c * QS + entry(wq * TQ + i, 0, lane)]);
+      }
+#pragma unroll
+      for (int x = 0; x < 6; ++x)
+#pragma unroll
+        for (int i = 0; i < TQ; ++i)
+#pragma unroll
+          for (int j = 0; j < TP; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[QI[x]][i], pf[PI[x]][j],
+                                                                acc[i][j], 0, 0, 0);
+      return;
+    }
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       bf16x8 pf[TP], qf[TQ];
@@ -306,7 +387,7 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
     }
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB>
+template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, bool X3 = false>
 hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
   const int64_t npt64 = (a.NP + MP - 1) / MP;
@@ -317,13 +398,13 @@ hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   const dim3 grid((unsigned)nblk), block(64 * WP * WQ);
   switch (epi) {
     case EPI_STORE:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_STORE><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_STORE, X3><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
     case EPI_SGD:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_SGD><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_SGD, X3><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
     default:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_GRAD><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_GRAD, X3><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
   }
   return hipGetLastError();
@@ -333,9 +414,13 @@ hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
 
 bool gemm_bf16_args_ok(const GemmBfArgs& a) {
   const int pe = a.Pb ? 8 : 4;
-  return a.NP > 0 && a.NQ > 0 && a.K > 0 && a.K % 4 == 0 && a.NQ % 4 == 0 &&
-         (a.P != nullptr) != (a.Pb != nullptr) && a.kp > 0 && a.kp % pe == 0 &&
-         a.ldp >= a.kp && a.ldq % 64 == 0 && a.ldq >= ((a.K + 63) / 64) * 64;
+  if (!(a.NP > 0 && a.NQ > 0 && a.K > 0 && a.K % 4 == 0 && a.NQ % 4 == 0 &&
+        (a.P != nullptr) != (a.Pb != nullptr) && a.kp > 0 && a.kp % pe == 0 && a.ldp >= a.kp &&
+        a.ldp % 4 == 0))
+    return false;
+  if (a.Qf)  // three-piece mode: fp32 P and Q, rows 16-byte aligned
+    return a.P != nullptr && a.Q == nullptr && a.ldq % 4 == 0 && a.ldq >= a.K;
+  return a.Q != nullptr && a.ldq % 64 == 0 && a.ldq >= ((a.K + 63) / 64) * 64;
 }
 
 template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH>
@@ -345,6 +430,15 @@ hipError_t gemm_bf_p(const GemmBfArgs& a, int epi, hipStream_t s) {
 }
 
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
+  if (a.Qf) {
+    note_variant("k_gemm_x3", kArithX3);
+    if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
+    if (!gemm_bf16_args_ok(a)) return hipErrorInvalidValue;
+    // one 16-k stage of three planes per operand, loaded a stage ahead
+    if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 16, 1, false, true>(a, epi, s);
+    if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 16, 1, false, true>(a, epi, s);
+    return gemm_bf_go<4, 2, 2, 4, 16, 1, false, true>(a, epi, s);
+  }
   note_variant("k_gemm_bf", kArithBf16);
   if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
   if (!gemm_bf16_args_ok(a)) return hipErrorInvalidValue;

@@ -78,16 +78,20 @@ struct GemmArgs {
 
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
 
-// bf16-in / fp32-accumulate input-layer GEMM:
-// C[p][q] = sum_k bf16(P[p][k]) Q[q][k], epilogues as above.
+// Input-layer GEMM on the bf16 matrix cores, epilogues as above:
+// C[p][q] = sum_k bf16(P[p][k]) Q[q][k] with bf16 Q, or, with fp32 Qf and
+// fp32 P, the fp32 product at fp32 accuracy (three-piece splits of both
+// operands, six bf16 products per k step).
 struct GemmBfArgs {
-  const float* P;           // [NP][ldp] fp32, rounded to bf16 on load, or null and
+  const float* P;           // [NP][ldp] fp32 (rounded to bf16 on load, or split), or null and
   const unsigned short* Pb; // [NP][ldp] bf16 bit patterns
   int64_t ldp;              // >= kp
   int32_t kp;               // P columns k < kp are read (finite); later k count as 0
   int64_t NP;
   const unsigned short* Q;  // [NQ][ldq] bf16 bit patterns, zero for K <= k < ldq
-  int64_t ldq;              // multiple of 64, >= K rounded up to 64
+  const float* Qf;          // or [NQ][ldq] fp32 (with fp32 P): the three-piece mode
+  int64_t ldq;              // bf16 Q: multiple of 64, >= K rounded up to 64;
+                            // fp32 Q: multiple of 4, >= K
   int32_t NQ;               // multiple of 4
   int32_t K;                // multiple of 4
   float* out;

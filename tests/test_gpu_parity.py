@@ -106,6 +106,11 @@ CASES = {
     "bx3_f116_b120": dict(M=15, hmax=120, F=116, O=2, B=120),
     "f116_b200": dict(M=15, hmax=120, F=116, O=2, B=200),
     "bx3_f64_b256_o4": dict(M=20, hmax=100, F=64, O=4, B=256),
+    # the three-piece GEMMs (shapes the LDS-resident kernels do not take):
+    # 64-, 128- and 256-wide q tiles, K tails of 8 and 0, a ragged last q tile
+    "gx3_f1000_b64": dict(M=8, hmax=60, F=1000, O=2, B=64),
+    "gx3_f1000_b120_o4": dict(M=8, hmax=60, F=1000, O=4, B=120),
+    "gx3_f300_b520": dict(M=10, hmax=90, F=300, O=2, B=520),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
@@ -238,7 +243,8 @@ def test_gradients_and_losses(pm, orc, torch, name, path):
 
 @pytest.mark.parametrize("name", ["ragged", "tile_spanning", "o10_b32", "b300_f100",
                                   "f100_b250", "f128_b100_o4", "f32_b32_o10", "fm3_mixed_b256",
-                                  "bx3_f36_b128_o4", "bx3_f116_b120"])
+                                  "bx3_f36_b128_o4", "bx3_f116_b120",
+                                  "gx3_f1000_b120_o4", "gx3_f300_b520"])
 def test_train_step_is_sgd_on_the_same_gradients(pm, orc, torch, name, path):
     """The fused update equals W - lr * dW with dW from the gradient mode
     (to fp32 rounding of W), and the step's losses match the oracle."""
@@ -452,6 +458,8 @@ VARIANTS = [
     ((40, 2, 256, "default", "fp32"), ("k_fwd_x3", 2), ("k_bwd_lds", 1)),
     ((116, 2, 120, "default", "fp32"), ("k_fwd_x3", 2), ("k_bwd_x3", 2)),
     ((116, 2, 200, "default", "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
+    ((20, 3, 300, "default", "fp32"), ("k_gemm_x3", 2), None),
+    ((1000, 2, 64, "default", "fp32"), ("k_gemm_x3", 2), None),
     ((32, 10, 32, "default", "fp32"), ("k_fwd_lds_ring", 1), ("k_bwd_mf", 1)),
     ((20, 2, 100, "default", "fp32"), ("k_fwd_lds", 1), ("k_bwd_lds", 1)),
     ((100, 2, 256, "generic", "fp32"), ("k_gemm_nt", 1), None),
