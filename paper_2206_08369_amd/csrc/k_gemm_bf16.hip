@@ -7,8 +7,8 @@
 //   LDS-resident kernels do not take): both operands fp32, each element split
 //   as it is staged into bf16 pieces a = a0 + a1 + a2 (every piece the
 //   round-to-nearest of what the previous ones leave, exact for normal a),
-//   and every k step taken as the six piece products q2 p0, q1 p1, q0 p2,
-//   q1 p0, q0 p1, q0 p0 in fp32 accumulation; the three left out are at most
+//   and every k step taken as the six piece products q0 p0, q1 p0, q0 p1,
+//   q1 p1, q2 p0, q0 p2 (in this order) in fp32 accumulation; the three left out are at most
 //   2^-23 of each product, so C carries the error of an fp32 dot product.
 //
 // P is the big fp32 operand (W1 for the forward product of Section 3 step 1,
@@ -35,8 +35,9 @@
 // stage k, one barrier per stage.
 //
 // In the three-piece mode each operand has three LDS planes per stage (the
-// pieces), the stage is 16 k deep (one MFMA k step), and k past K reads as
-// zero on both operands.
+// pieces), the stage is 16 k deep (one MFMA k step), global loads run two
+// stages ahead, the next stage is split into LDS between the products of
+// the current one, and k past K reads as zero on both operands.
 //
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8, and the nqt
 // q-tiles of one p-tile are consecutive workgroups of the same XCD, so the
@@ -78,7 +79,8 @@ __device__ __forceinline__ void split3x4(const f32x4& v, bf16x4& p0, bf16x4& p1,
 }
 
 template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, int EPI, bool X3 = false>
-__global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
+__global__ __launch_bounds__(64 * WP * WQ) __attribute__((amdgpu_waves_per_eu(2)))
+void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   constexpr int NT = 64 * WP * WQ;
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
   constexpr int KH = KS / 2;   // k owned by one lane half of an MFMA operand
@@ -88,7 +90,8 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   // four fp32 (half of one lane's 8-k bf16 operand entry); bf16 P (PB) and
   // Q chunks are eight bf16.
   // In the three-piece mode Q is fp32 too (four per chunk).
-  static_assert(!X3 || (!PB && KS == 16), "three-piece mode: fp32 P, one k step per stage");
+  static_assert(!X3 || (!PB && KS == 16 && DEPTH == 2),
+                "three-piece mode: fp32 P, one k step per stage, loads two stages ahead");
   constexpr int PE = PB ? 8 : 4;            // P elements per chunk
   constexpr int QE = X3 ? 4 : 8;            // Q elements per chunk
   constexpr int CP = KS / PE, CQ = KS / QE;  // chunks per row and stage
@@ -241,30 +244,6 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
   auto compute = [&](int sb) {
     const u32x4* ps = lds + sb * SS;
     const u32x4* qs = ps + PL * PS;
-    if constexpr (X3) {
-      // the six piece products, smallest first; each pass over the TQ x TP
-      // blocks issues independent MFMAs back to back
-      constexpr int QI[6] = {2, 1, 0, 1, 0, 0}, PI[6] = {0, 1, 2, 0, 1, 0};
-      bf16x8 pf[3][TP], qf[3][TQ];
-#pragma unroll
-      for (int c = 0; c < 3; ++c) {
-#pragma unroll
-        for (int j = 0; j < TP; ++j)
-          pf[c][j] = __builtin_bit_cast(bf16x8, ps[c * PS + entry(wp * TP + j, 0, lane)]);
-#pragma unroll
-        for (int i = 0; i < TQ; ++i)
-          qf[c][i] = __builtin_bit_cast(bf16x8, qs[c * QS + entry(wq * TQ + i, 0, lane)]);
-      }
-#pragma unroll
-      for (int x = 0; x < 6; ++x)
-#pragma unroll
-        for (int i = 0; i < TQ; ++i)
-#pragma unroll
-          for (int j = 0; j < TP; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[QI[x]][i], pf[PI[x]][j],
-                                                                acc[i][j], 0, 0, 0);
-      return;
-    }
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       bf16x8 pf[TP], qf[TQ];
@@ -282,7 +261,68 @@ __global__ __launch_bounds__(64 * WP * WQ) void k_gemm_bf(GemmBfArgs a, int npt,
     }
   };
 
-  if (DEPTH == 1) {
+  // Three-piece mode: the fragments of planes 0 and 1, the four piece
+  // products they make (q0 p0, q1 p0, q0 p1, q1 p1), then the fragments of
+  // plane 2 (in the registers plane 1 held) and `mid`, then q2 p0 and q0 p2.
+  // Each pass over the TQ x TP blocks issues independent MFMAs back to back.
+  auto compute_x3 = [&](int sb, auto mid) {
+    const u32x4* ps = lds + sb * SS;
+    const u32x4* qs = ps + PL * PS;
+    bf16x8 p0[TP], q0[TQ], p1[TP], q1[TQ];
+    auto frags = [&](int c, bf16x8(&pf)[TP], bf16x8(&qf)[TQ]) {
+#pragma unroll
+      for (int j = 0; j < TP; ++j)
+        pf[j] = __builtin_bit_cast(bf16x8, ps[c * PS + entry(wp * TP + j, 0, lane)]);
+#pragma unroll
+      for (int i = 0; i < TQ; ++i)
+        qf[i] = __builtin_bit_cast(bf16x8, qs[c * QS + entry(wq * TQ + i, 0, lane)]);
+    };
+    auto pass = [&](const bf16x8(&qf)[TQ], const bf16x8(&pf)[TP]) {
+#pragma unroll
+      for (int i = 0; i < TQ; ++i)
+#pragma unroll
+        for (int j = 0; j < TP; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[i], pf[j], acc[i][j], 0, 0, 0);
+    };
+    frags(0, p0, q0);
+    frags(1, p1, q1);
+    pass(q0, p0);
+    pass(q1, p0);
+    pass(q0, p1);
+    pass(q1, p1);
+    __builtin_amdgcn_sched_barrier(0);
+    frags(2, p1, q1);
+    mid();
+    __builtin_amdgcn_sched_barrier(0);
+    pass(q1, p0);
+    pass(q0, p1);
+  };
+
+  if constexpr (X3) {
+    // Stage kt+2 is loaded while stage kt is multiplied, and stage kt+1
+    // (loaded a stage earlier) is split into the other LDS buffer between
+    // the products of stage kt: one barrier per stage, and the split and
+    // LDS writes overlap the matrix work.
+    Regs r0, r1;
+    load(r0, 0);
+    store(r0, 0);
+    load(r1, 1);
+    __syncthreads();
+    for (int kt = 0;; kt += 2) {
+      load(r0, kt + 2);
+      compute_x3(0, [&] {
+        if (kt + 1 < nk) store(r1, 1);
+      });
+      if (kt + 1 >= nk) break;
+      __syncthreads();
+      load(r1, kt + 3);
+      compute_x3(1, [&] {
+        if (kt + 2 < nk) store(r0, 0);
+      });
+      if (kt + 2 >= nk) break;
+      __syncthreads();
+    }
+  } else if (DEPTH == 1) {
     // stage kt+1 is loaded while stage kt is multiplied
     Regs r;
     load(r, 0);
@@ -434,10 +474,12 @@ hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
     note_variant("k_gemm_x3", kArithX3);
     if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
     if (!gemm_bf16_args_ok(a)) return hipErrorInvalidValue;
-    // one 16-k stage of three planes per operand, loaded a stage ahead
-    if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 16, 1, false, true>(a, epi, s);
-    if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 16, 1, false, true>(a, epi, s);
-    return gemm_bf_go<4, 2, 2, 4, 16, 1, false, true>(a, epi, s);
+    // 16-k stages of three planes per operand; four-wave workgroups of at
+    // most 72 KB of LDS, two per CU, so that one's barrier waits and
+    // epilogue overlap the other's products
+    if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 16, 2, false, true>(a, epi, s);
+    if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 16, 2, false, true>(a, epi, s);
+    return gemm_bf_go<4, 2, 2, 4, 16, 2, false, true>(a, epi, s);
   }
   note_variant("k_gemm_bf", kArithBf16);
   if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
