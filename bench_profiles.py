@@ -79,7 +79,14 @@ def short(name: str) -> str:
 def role_of(name: str, precision: str):
     base = name.split("<")[0]
     if base == "k_gemm_bf" or base == "k_gemm_nt":
-        epi = name.rstrip(">").split(",")[-1].strip()
+        # the epilogue: last argument of k_gemm_nt, the one after the operand
+        # type flag of k_gemm_bf
+        args = [a.strip() for a in name.split("<", 1)[-1].rstrip(">").split(",")]
+        if base == "k_gemm_bf":
+            flags = [i for i, a in enumerate(args) if a in ("true", "false")]
+            epi = args[flags[0] + 1] if flags and flags[0] + 1 < len(args) else ""
+        else:
+            epi = args[-1]
         return {"0": "gemm_fwd", "1": "gemm_bwd", "2": "gemm_grad"}.get(epi, "gemm")
     return ROLE.get(base)
 

@@ -31,8 +31,9 @@
 // bf16 in registers), writes them to LDS in MFMA-operand order (fragment
 // (g, s) = 64 lanes x 16 bytes, g the 32-row group, s the 8-k step), and
 // every wave reads its fragments with conflict-free ds_read_b128.  Two LDS
-// stages: the global loads of stage k+1 are in flight during the MFMAs of
-// stage k, one barrier per stage.
+// stages and two register stages: the global loads of stage k+2 are in
+// flight during the MFMAs of stage k, stage k+1 is written to LDS between
+// them, and each stage ends with one barrier.
 //
 // In the three-piece mode each operand has three LDS planes per stage (the
 // pieces), the stage is 16 k deep (one MFMA k step), global loads run two
@@ -78,7 +79,7 @@ __device__ __forceinline__ void split3x4(const f32x4& v, bf16x4& p0, bf16x4& p1,
   p2 = __builtin_convertvector(r1 - __builtin_convertvector(p1, f32x4), bf16x4);
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, int EPI, bool X3 = false>
+template <int TP, int TQ, int WP, int WQ, int KS, bool PB, int EPI, bool X3 = false>
 __global__ __launch_bounds__(64 * WP * WQ) __attribute__((amdgpu_waves_per_eu(2)))
 void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   constexpr int NT = 64 * WP * WQ;
@@ -90,8 +91,7 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   // four fp32 (half of one lane's 8-k bf16 operand entry); bf16 P (PB) and
   // Q chunks are eight bf16.
   // In the three-piece mode Q is fp32 too (four per chunk).
-  static_assert(!X3 || (!PB && KS == 16 && DEPTH == 2),
-                "three-piece mode: fp32 P, one k step per stage, loads two stages ahead");
+  static_assert(!X3 || (!PB && KS == 16), "three-piece mode: fp32 P, one k step per stage");
   constexpr int PE = PB ? 8 : 4;            // P elements per chunk
   constexpr int QE = X3 ? 4 : 8;            // Q elements per chunk
   constexpr int CP = KS / PE, CQ = KS / QE;  // chunks per row and stage
@@ -129,31 +129,33 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   };
   typedef typename std::conditional<PB, unsigned short, float>::type PT;
   const PT* pbase = PB ? (const PT*)a.Pb : (const PT*)a.P;
-  const PT* pptr[LP];
-  int pk[LP], poff[LP];  // k of the chunk within the stage; LDS byte offset
-#pragma unroll
-  for (int e = 0; e < LP; ++e) {
-    const int idx = (t + e * NT) % (MP * CP), row = idx / CP, c = idx % CP;
-    int64_t p = p0 + row;
-    if (p > a.NP - 1) p = a.NP - 1;
+  // A thread's chunks e = 0 .. LP-1 lie RP rows apart at the same k (and its
+  // Q chunks RQ rows apart), so their LDS entries are a fixed distance
+  // apart; addresses are formed at each load from the first row, which
+  // keeps three values per operand in registers instead of a pointer per
+  // chunk.
+  constexpr int RP = NT / CP, RQ = NT / CQ;
+  static_assert(LP == 1 || (NT % CP == 0 && RP % 32 == 0), "loader rows");
+  static_assert(LQ == 1 || (NT % CQ == 0 && RQ % 32 == 0), "loader rows");
+  int prow, pk, poff;  // first row, k of the chunk within the stage, LDS byte offset
+  {
+    const int idx = t % (MP * CP), row = idx / CP, c = idx % CP;
     const int k = PE * c, h = k / KH, st = (k % KH) / 8;
-    pptr[e] = pbase + p * a.ldp + k;
-    pk[e] = k;
-    poff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (PB ? 0 : 8 * (c & 1));
+    prow = row;
+    pk = k;
+    poff = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (PB ? 0 : 8 * (c & 1));
   }
   typedef typename std::conditional<X3, float, unsigned short>::type QT;
   const QT* qbase = X3 ? (const QT*)a.Qf : (const QT*)a.Q;
-  const QT* qptr[LQ];
-  int qk[LQ], qoff[LQ];
-#pragma unroll
-  for (int e = 0; e < LQ; ++e) {
-    const int idx = (t + e * NT) % (MQ * CQ), row = idx / CQ, c = idx % CQ;
-    const int q = min(q0 + row, a.NQ - 1);
+  int qrow, qk, qoff;
+  {
+    const int idx = t % (MQ * CQ), row = idx / CQ, c = idx % CQ;
     const int k = QE * c, h = k / KH, st = (k % KH) / 8;
-    qptr[e] = qbase + (int64_t)q * a.ldq + k;
-    qk[e] = k;
-    qoff[e] = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (X3 ? 8 * (c & 1) : 0);
+    qrow = row;
+    qk = k;
+    qoff = entry(row >> 5, st, (row & 31) + 32 * h) * 16 + (X3 ? 8 * (c & 1) : 0);
   }
+  constexpr int PSTEP = RP / 32 * NS * 64 * 16, QSTEP = RQ / 32 * NS * 64 * 16;  // bytes
 
   // Global loads of one stage into registers, without branches so that the
   // compiler's wait counts stay exact: the stage index is clamped to the
@@ -172,17 +174,19 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
   auto load = [&](Regs& r, int kt) {
     const int k0 = min(kt, nk - 1) * KS;
     r.k0 = k0;
+    const int pkk = k0 + pk < kp ? k0 + pk : 0;
 #pragma unroll
     for (int e = 0; e < LP; ++e) {
       if (MP * CP < NT && t >= MP * CP) continue;
-      const int off = k0 + pk[e] < kp ? k0 : -pk[e];
-      r.p[e] = *(const u32x4*)(pptr[e] + off);
+      const int64_t p = min(p0 + prow + e * RP, a.NP - 1);
+      r.p[e] = *(const u32x4*)(pbase + p * a.ldp + pkk);
     }
+    const int qkk = !X3 || k0 + qk < K ? k0 + qk : 0;
 #pragma unroll
     for (int e = 0; e < LQ; ++e) {
       if (MQ * CQ < NT && t >= MQ * CQ) continue;
-      const int off = !X3 || k0 + qk[e] < K ? k0 : -qk[e];
-      r.q[e] = *(const u32x4*)(qptr[e] + off);
+      const int q = min(q0 + qrow + e * RQ, a.NQ - 1);
+      r.q[e] = *(const u32x4*)(qbase + (int64_t)q * a.ldq + qkk);
     }
   };
   auto store = [&](const Regs& r, int sb) {
@@ -192,22 +196,24 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
 #pragma unroll
       for (int e = 0; e < LP; ++e) {
         if (MP * CP < NT && t >= MP * CP) continue;
-        const f32x4 f = r.k0 + pk[e] < kp ? __builtin_bit_cast(f32x4, r.p[e]) : f32x4{0, 0, 0, 0};
+        const f32x4 f = r.k0 + pk < kp ? __builtin_bit_cast(f32x4, r.p[e]) : f32x4{0, 0, 0, 0};
         bf16x4 v0, v1, v2;
         split3x4(f, v0, v1, v2);
-        *(bf16x4*)(ps + poff[e]) = v0;
-        *(bf16x4*)(ps + PS * 16 + poff[e]) = v1;
-        *(bf16x4*)(ps + 2 * PS * 16 + poff[e]) = v2;
+        char* d = ps + poff + e * PSTEP;
+        *(bf16x4*)d = v0;
+        *(bf16x4*)(d + PS * 16) = v1;
+        *(bf16x4*)(d + 2 * PS * 16) = v2;
       }
 #pragma unroll
       for (int e = 0; e < LQ; ++e) {
         if (MQ * CQ < NT && t >= MQ * CQ) continue;
-        const f32x4 f = r.k0 + qk[e] < K ? __builtin_bit_cast(f32x4, r.q[e]) : f32x4{0, 0, 0, 0};
+        const f32x4 f = r.k0 + qk < K ? __builtin_bit_cast(f32x4, r.q[e]) : f32x4{0, 0, 0, 0};
         bf16x4 v0, v1, v2;
         split3x4(f, v0, v1, v2);
-        *(bf16x4*)(qs + qoff[e]) = v0;
-        *(bf16x4*)(qs + QS * 16 + qoff[e]) = v1;
-        *(bf16x4*)(qs + 2 * QS * 16 + qoff[e]) = v2;
+        char* d = qs + qoff + e * QSTEP;
+        *(bf16x4*)d = v0;
+        *(bf16x4*)(d + QS * 16) = v1;
+        *(bf16x4*)(d + 2 * QS * 16) = v2;
       }
       return;
     }
@@ -215,7 +221,7 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
     for (int e = 0; e < LP; ++e) {
       if (MP * CP < NT && t >= MP * CP) continue;
       if (PB) {
-        *(u32x4*)(ps + poff[e]) = r.p[e];
+        *(u32x4*)(ps + poff + e * PSTEP) = r.p[e];
       } else {
         const f32x4 f = __builtin_bit_cast(f32x4, r.p[e]);
         bf16x4 v;
@@ -223,13 +229,13 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
         v[1] = (__bf16)f[1];
         v[2] = (__bf16)f[2];
         v[3] = (__bf16)f[3];
-        *(bf16x4*)(ps + poff[e]) = v;
+        *(bf16x4*)(ps + poff + e * PSTEP) = v;
       }
     }
 #pragma unroll
     for (int e = 0; e < LQ; ++e) {
       if (MQ * CQ < NT && t >= MQ * CQ) continue;
-      *(u32x4*)(qs + qoff[e]) = r.q[e];
+      *(u32x4*)(qs + qoff + e * QSTEP) = r.q[e];
     }
   };
 
@@ -241,11 +247,18 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  auto compute = [&](int sb) {
+  // bf16 operands: NS k steps of TQ x TP products; `mid` runs after the
+  // first half of them.
+  auto compute = [&](int sb, auto mid) {
     const u32x4* ps = lds + sb * SS;
     const u32x4* qs = ps + PL * PS;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
+      if (s == NS / 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        mid();
+        __builtin_amdgcn_sched_barrier(0);
+      }
       bf16x8 pf[TP], qf[TQ];
 #pragma unroll
       for (int j = 0; j < TP; ++j)
@@ -298,11 +311,19 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
     pass(q0, p1);
   };
 
-  if constexpr (X3) {
-    // Stage kt+2 is loaded while stage kt is multiplied, and stage kt+1
-    // (loaded a stage earlier) is split into the other LDS buffer between
-    // the products of stage kt: one barrier per stage, and the split and
-    // LDS writes overlap the matrix work.
+  // Stage kt+2 is loaded while stage kt is multiplied, and stage kt+1
+  // (loaded a stage earlier) is written to the other LDS buffer (split into
+  // pieces in the three-piece mode) between the products of stage kt: one
+  // barrier per stage, and the LDS writes overlap the matrix work.  The
+  // other buffer is free then: its last reader, stage kt-1, ended before
+  // the previous barrier.
+  auto stage = [&](int sb, auto mid) {
+    if constexpr (X3)
+      compute_x3(sb, mid);
+    else
+      compute(sb, mid);
+  };
+  {
     Regs r0, r1;
     load(r0, 0);
     store(r0, 0);
@@ -310,55 +331,16 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
     __syncthreads();
     for (int kt = 0;; kt += 2) {
       load(r0, kt + 2);
-      compute_x3(0, [&] {
+      stage(0, [&] {
         if (kt + 1 < nk) store(r1, 1);
       });
       if (kt + 1 >= nk) break;
       __syncthreads();
       load(r1, kt + 3);
-      compute_x3(1, [&] {
+      stage(1, [&] {
         if (kt + 2 < nk) store(r0, 0);
       });
       if (kt + 2 >= nk) break;
-      __syncthreads();
-    }
-  } else if (DEPTH == 1) {
-    // stage kt+1 is loaded while stage kt is multiplied
-    Regs r;
-    load(r, 0);
-    store(r, 0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      load(r, kt + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(kt & 1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + 1 >= nk) break;
-      store(r, (kt + 1) & 1);
-      __syncthreads();
-    }
-  } else {
-    // stage kt+2 is loaded while stage kt is multiplied: two stages of
-    // multiplies cover the latency of every load
-    Regs r0, r1;
-    load(r0, 0);
-    store(r0, 0);
-    load(r1, 1);
-    __syncthreads();
-    for (int kt = 0;; kt += 2) {
-      load(r0, kt + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + 1 >= nk) break;
-      store(r1, 1);
-      __syncthreads();
-      load(r1, kt + 3);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + 2 >= nk) break;
-      store(r0, 0);
       __syncthreads();
     }
   }
@@ -389,45 +371,69 @@ void k_gemm_bf(GemmBfArgs a, int npt, int nqt) {
       const int64_t pb = p0 + 32 * (wp * TP + j);
       const int qb = q0 + 32 * (wq * TQ + i0);
       constexpr int LPR = 8 * QB;  // lanes per row
+      constexpr int NPASS = 32 * LPR / 64;
+      // Every global load of the round (the weights to update, per-model
+      // rates, feature-mask words) comes before its first store: a load
+      // after a store to `out` may not be moved above it, so each pass would
+      // wait a full memory round trip.  Lanes past the edge load from the
+      // last row and column and store nothing.
+      f32x4 wv[NPASS];
+      float lrv[NPASS];
+      uint32_t mbits[NPASS];
+      if constexpr (EPI != EPI_STORE) {
 #pragma unroll
-      for (int pass = 0; pass < 32 * LPR / 64; ++pass) {
+        for (int pass = 0; pass < NPASS; ++pass) {
+          const int r = pass * (64 / LPR) + lane / LPR, c4 = 4 * (lane % LPR);
+          const int64_t p = min(pb + r, a.NP - 1);
+          const int q = min(qb + c4, a.NQ - 4);
+          const int m = (a.lrm || a.fmask) ? a.mid[p] : 0;
+          // masked features: zero gradient, so their weights stay 0
+          mbits[pass] = a.fmask ? a.fmask[(int64_t)m * a.fmw + (q >> 5)] >> (q & 31) : 0xFu;
+          if constexpr (EPI == EPI_SGD) {
+            lrv[pass] = a.lrm ? a.lrm[m] : a.lr;
+            wv[pass] = *(const f32x4*)(a.out + p * a.ldo + q);
+          }
+        }
+      }
+#pragma unroll
+      for (int pass = 0; pass < NPASS; ++pass) {
         const int r = pass * (64 / LPR) + lane / LPR, c4 = 4 * (lane % LPR);
         const f32x4 v0 = *(const f32x4*)(scr + r * LDT + c4);
         const int64_t p = pb + r;
         const int q = qb + c4;
         if (p >= a.NP || q >= a.NQ) continue;
         float* o = a.out + p * a.ldo + q;
-        const float lr = (EPI == EPI_SGD && a.lrm) ? a.lrm[a.mid[p]] : a.lr;
-        // masked features: zero gradient, so their weights stay 0
-        const f32x4 v =
-            (EPI != EPI_STORE && a.fmask) ? fmask4(a.fmask, a.fmw, a.mid[p], q, v0) : v0;
-        if (EPI == EPI_STORE) {
+        if constexpr (EPI == EPI_STORE) {
           if (a.outb) {  // the bf16 storage mode keeps Z as bfloat16 (nearest even)
             const bf16x4 zb = {(__bf16)v0[0], (__bf16)v0[1], (__bf16)v0[2], (__bf16)v0[3]};
             *(bf16x4*)(a.outb + p * a.ldob + q) = zb;
           } else {
             *(f32x4*)o = v0;
           }
-        } else if (EPI == EPI_SGD) {
-          f32x4 w = *(f32x4*)o;
-          w -= lr * v;
-          *(f32x4*)o = w;
-          if (a.outb) {
-            const bf16x4 wb = {(__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};
-            *(bf16x4*)(a.outb + p * a.ldob + q) = wb;
-          }
         } else {
+          const uint32_t b = mbits[pass];
+          const f32x4 v = {(b & 1u) ? v0[0] : 0.f, (b & 2u) ? v0[1] : 0.f, (b & 4u) ? v0[2] : 0.f,
+                           (b & 8u) ? v0[3] : 0.f};
+          if constexpr (EPI == EPI_SGD) {
+            const f32x4 w = wv[pass] - lrv[pass] * v;
+            *(f32x4*)o = w;
+            if (a.outb) {
+              const bf16x4 wb = {(__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};
+              *(bf16x4*)(a.outb + p * a.ldob + q) = wb;
+            }
+          } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (q + e < a.ncols) o[e] = v[e];
-            else if (q + e == a.bcol && a.db1) a.db1[p] = v[e];
+            for (int e = 0; e < 4; ++e)
+              if (q + e < a.ncols) o[e] = v[e];
+              else if (q + e == a.bcol && a.db1) a.db1[p] = v[e];
+          }
         }
       }
       __syncthreads();
     }
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH, bool PB, bool X3 = false>
+template <int TP, int TQ, int WP, int WQ, int KS, bool PB, bool X3 = false>
 hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   constexpr int MP = 32 * TP * WP, MQ = 32 * TQ * WQ;
   const int64_t npt64 = (a.NP + MP - 1) / MP;
@@ -438,13 +444,13 @@ hipError_t gemm_bf_go(const GemmBfArgs& a, int epi, hipStream_t s) {
   const dim3 grid((unsigned)nblk), block(64 * WP * WQ);
   switch (epi) {
     case EPI_STORE:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_STORE, X3><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, PB, EPI_STORE, X3><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
     case EPI_SGD:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_SGD, X3><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, PB, EPI_SGD, X3><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
     default:
-      k_gemm_bf<TP, TQ, WP, WQ, KS, DEPTH, PB, EPI_GRAD, X3><<<grid, block, 0, s>>>(a, npt, nqt);
+      k_gemm_bf<TP, TQ, WP, WQ, KS, PB, EPI_GRAD, X3><<<grid, block, 0, s>>>(a, npt, nqt);
       break;
   }
   return hipGetLastError();
@@ -463,10 +469,10 @@ bool gemm_bf16_args_ok(const GemmBfArgs& a) {
   return a.Q != nullptr && a.ldq % 64 == 0 && a.ldq >= ((a.K + 63) / 64) * 64;
 }
 
-template <int TP, int TQ, int WP, int WQ, int KS, int DEPTH>
+template <int TP, int TQ, int WP, int WQ, int KS>
 hipError_t gemm_bf_p(const GemmBfArgs& a, int epi, hipStream_t s) {
-  if (a.Pb) return gemm_bf_go<TP, TQ, WP, WQ, KS, DEPTH, true>(a, epi, s);
-  return gemm_bf_go<TP, TQ, WP, WQ, KS, DEPTH, false>(a, epi, s);
+  if (a.Pb) return gemm_bf_go<TP, TQ, WP, WQ, KS, true>(a, epi, s);
+  return gemm_bf_go<TP, TQ, WP, WQ, KS, false>(a, epi, s);
 }
 
 hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
@@ -477,9 +483,9 @@ hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
     // 16-k stages of three planes per operand; four-wave workgroups of at
     // most 72 KB of LDS, two per CU, so that one's barrier waits and
     // epilogue overlap the other's products
-    if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 16, 2, false, true>(a, epi, s);
-    if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 16, 2, false, true>(a, epi, s);
-    return gemm_bf_go<4, 2, 2, 4, 16, 2, false, true>(a, epi, s);
+    if (a.NQ <= 64) return gemm_bf_go<4, 1, 2, 2, 16, false, true>(a, epi, s);
+    if (a.NQ <= 128) return gemm_bf_go<2, 2, 2, 2, 16, false, true>(a, epi, s);
+    return gemm_bf_go<4, 2, 2, 4, 16, false, true>(a, epi, s);
   }
   note_variant("k_gemm_bf", kArithBf16);
   if (a.NP <= 0 || a.NQ <= 0) return hipSuccess;
@@ -487,9 +493,9 @@ hipError_t launch_gemm_bf16(const GemmBfArgs& a, int epi, hipStream_t s) {
   // q tile no wider than needed for small q; 256 x 256 tiles otherwise (the
   // largest that keeps the accumulators in registers, and the least operand
   // traffic per product from L2)
-  if (a.NQ <= 64) return gemm_bf_p<4, 1, 2, 2, 32, 2>(a, epi, s);
-  if (a.NQ <= 128) return gemm_bf_p<2, 2, 2, 2, 32, 2>(a, epi, s);
-  return gemm_bf_p<4, 2, 2, 4, 32, 2>(a, epi, s);
+  if (a.NQ <= 64) return gemm_bf_p<4, 1, 2, 2, 32>(a, epi, s);
+  if (a.NQ <= 128) return gemm_bf_p<2, 2, 2, 2, 32>(a, epi, s);
+  return gemm_bf_p<4, 2, 2, 4, 32>(a, epi, s);
 }
 
 }  // namespace pmlpk
