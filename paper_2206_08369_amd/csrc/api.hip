@@ -770,6 +770,29 @@ int step_deep(pmlp* h, const float* X, const int32_t* y, int32_t B, float lr, fl
     if (int rc = run(h, KID_DEEP, [&] { return launch_sgd(d->W12, d->G12, d->K, lr, h->stream); }))
       return rc;
   }
+  if (h->lds_kernels) {  // fp32 accuracy on the bf16 matrix cores
+    GemmBfArgs g{};
+    g.P = w.Zt;
+    g.ldp = Bp;
+    g.kp = Bp;
+    g.NP = h->N;
+    g.Qf = w.Xt;
+    g.ldq = Bp;
+    g.NQ = h->F4;
+    g.K = Bp;
+    g.out = dW1 ? dW1 : h->W1;
+    g.ldo = dW1 ? h->F : h->F4;
+    g.ncols = h->F;
+    g.lr = lr;
+    g.mid = h->d_mid;
+    g.bcol = -1;
+    if (int rc = run(h, KID_GEMM_BWD, [&] {
+          return launch_gemm_bf16(g, dW1 ? EPI_GRAD : EPI_SGD, h->stream);
+        }))
+      return rc;
+    h->have_loss = true;
+    return PMLP_OK;
+  }
   GemmArgs g{};
   g.P = w.Zt;
   g.ldp = Bp;
