@@ -154,17 +154,21 @@ __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* _
                                                int Bp, int b0, const float* __restrict__ wrow,
                                                bool orow_ok, int64_t nbeg, int64_t nend, int li,
                                                int lk) {
-  // four-unit MFMA steps per pass, all loads first (loads in flight per lane:
-  // 2 kUM).  Row li of block i is sample b0 + NBB li + i, so a lane's NBB
-  // values of one unit are one vector load and the 16 lanes of a unit read
-  // 64 NBB contiguous bytes of its row (a group past the batch reads the
-  // last NBB samples instead; their outputs are not stored).
+  // kUM four-unit MFMA steps per pass, the loads of the next pass in flight
+  // while the current one is multiplied (loads in flight per lane: up to
+  // 2 kUM (NBB + 1) values).  Row li of block i is sample b0 + NBB li + i,
+  // so a lane's NBB values of one unit are one vector load and the 16 lanes
+  // of a unit read 64 NBB contiguous bytes of its row (a group past the
+  // batch reads the last NBB samples instead; their outputs are not stored).
   constexpr int kUM = NBB <= 2 ? 8 : 4;
+  constexpr int STEP = 4 * kUM;
   int bl = b0 + NBB * li;
   if (bl > Bp - NBB) bl = Bp - NBB;
-  for (int64_t n0 = nbeg; n0 < nend; n0 += 4 * kUM) {
+  struct Pass {
     float z[kUM][NBB];
     float w[kUM];
+  };
+  auto fetch = [&](Pass& P, int64_t n0) {
 #pragma unroll
     for (int u = 0; u < kUM; ++u) {
       int64_t n = n0 + 4 * u + lk;
@@ -173,27 +177,38 @@ __device__ __forceinline__ void fwd_segment_mf(f32x4 (&acc)[NBB], const float* _
       if constexpr (NBB == 4) {
         const f32x4 v = load_z4(Zt, ZB, zi);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) z[u][i] = v[i];
+        for (int i = 0; i < 4; ++i) P.z[u][i] = v[i];
       } else if constexpr (NBB == 2) {
         const f32x2 v = load_z2(Zt, ZB, zi);
-        z[u][0] = v[0];
-        z[u][1] = v[1];
+        P.z[u][0] = v[0];
+        P.z[u][1] = v[1];
       } else {
-        z[u][0] = load_z1(Zt, ZB, zi);
+        P.z[u][0] = load_z1(Zt, ZB, zi);
       }
-      w[u] = wrow[n];
+      P.w[u] = wrow[n];
     }
+  };
+  auto use = [&](const Pass& P, int64_t n0) {
 #pragma unroll
     for (int u = 0; u < kUM; ++u) {
       if (n0 + 4 * u >= nend) break;  // wave-uniform: the whole step is past the end
       const bool in = n0 + 4 * u + lk < nend;
-      const float wv = in && orow_ok ? w[u] : 0.f;
+      const float wv = in && orow_ok ? P.w[u] : 0.f;
 #pragma unroll
       for (int i = 0; i < NBB; ++i) {
-        const float h = in ? act_fwd(A, z[u][i]) : 0.f;
+        const float h = in ? act_fwd(A, P.z[u][i]) : 0.f;
         acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(h, wv, acc[i], 0, 0, 0);
       }
     }
+  };
+  Pass p0, p1;
+  if (nbeg < nend) fetch(p0, nbeg);
+  for (int64_t n0 = nbeg; n0 < nend; n0 += 2 * STEP) {
+    if (n0 + STEP < nend) fetch(p1, n0 + STEP);
+    use(p0, n0);
+    if (n0 + STEP >= nend) break;
+    if (n0 + 2 * STEP < nend) fetch(p0, n0 + 2 * STEP);
+    use(p1, n0 + STEP);
   }
 }
 
