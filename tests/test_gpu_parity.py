@@ -111,6 +111,10 @@ CASES = {
     "gx3_f1000_b64": dict(M=8, hmax=60, F=1000, O=2, B=64),
     "gx3_f1000_b120_o4": dict(M=8, hmax=60, F=1000, O=4, B=120),
     "gx3_f300_b520": dict(M=10, hmax=90, F=300, O=2, B=520),
+    # K = 4 (one stage, twelve of its sixteen k zero) in both products, the
+    # dW1 product with four q columns; widths 1 and a two-halves segment
+    "gx3_f3_b600_o3": dict(hs=[1, 700, 2, 1300, 5], F=3, O=3, B=600),
+    "gx3_f1_b300": dict(M=9, hmax=40, F=1, O=2, B=300),
 }
 
 # Kernel paths: the persistent LDS-resident kernels (default where a shape
