@@ -8,14 +8,15 @@
 //   as it is staged into bf16 pieces a = a0 + a1 + a2 (every piece the
 //   round-to-nearest of what the previous ones leave, exact for normal a),
 //   and every k step taken as the six piece products q0 p0, q1 p0, q0 p1,
-//   q1 p1, q2 p0, q0 p2 (in this order) in fp32 accumulation; the three left out are at most
-//   2^-23 of each product, so C carries the error of an fp32 dot product.
+//   q1 p1, q2 p0, q0 p2 (in this order) in fp32 accumulation; the three
+//   left out are at most 2^-23 of each product, so C carries the error of
+//   an fp32 dot product.
 //
-// P is the big fp32 operand (W1 for the forward product of Section 3 step 1,
-// dZ^T for dW1), rounded to bf16 (nearest even, v_cvt_pk_bf16_f32) as it is
-// loaded, so the fp32 master weights and activations are never copied.  Q is
-// the small operand (the batch or its transpose), already bf16.  Both are
-// k-contiguous.
+// P is the big operand (W1 for the forward product of Section 3 step 1,
+// dZ^T for dW1): bf16, or fp32 rounded to bf16 (nearest even) or split into
+// pieces as it is staged, so the fp32 master weights and activations are
+// never copied.  Q is the small operand (the batch or its transpose): bf16,
+// or fp32 in the three-piece mode.  Both are k-contiguous.
 //
 // One v_mfma_f32_32x32x16_bf16 takes a 32x16 tile of Q (lane l: row l%32,
 // eight k in half l/32) and a 16x32 tile of P^T laid out the same way, and
@@ -27,10 +28,11 @@
 //
 // A workgroup of WP x WQ waves computes an MP x MQ tile (MP = 32 TP WP,
 // MQ = 32 TQ WQ), each wave TP x TQ MFMA blocks.  Per stage, every thread
-// loads 16 consecutive k of one or more operand rows (fp32 P converted to
-// bf16 in registers), writes them to LDS in MFMA-operand order (fragment
-// (g, s) = 64 lanes x 16 bytes, g the 32-row group, s the 8-k step), and
-// every wave reads its fragments with conflict-free ds_read_b128.  Two LDS
+// loads 16-byte chunks (eight bf16 or four fp32 k values) of one or more
+// operand rows (fp32 converted or split in registers), writes them to LDS
+// in MFMA-operand order (fragment (g, s) = 64 lanes x 16 bytes, g the
+// 32-row group, s the 8-k step), and every wave reads its fragments with
+// conflict-free ds_read_b128.  Two LDS
 // stages and two register stages: the global loads of stage k+2 are in
 // flight during the MFMAs of stage k, stage k+1 is written to LDS between
 // them, and each stage ends with one barrier.
@@ -56,19 +58,6 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ u32x4 pack_bf16x8(const f32x4& a, const f32x4& b) {
-  bf16x8 r;
-  r[0] = (__bf16)a[0];
-  r[1] = (__bf16)a[1];
-  r[2] = (__bf16)a[2];
-  r[3] = (__bf16)a[3];
-  r[4] = (__bf16)b[0];
-  r[5] = (__bf16)b[1];
-  r[6] = (__bf16)b[2];
-  r[7] = (__bf16)b[3];
-  return __builtin_bit_cast(u32x4, r);
-}
 
 // Three bf16 pieces of four fp32 values: v = p0 + p1 + p2, each piece the
 // round-to-nearest-even of the remainder (exact subtractions in fp32).
