@@ -44,3 +44,33 @@ def test_epochs_end_with_their_partial_batch():
         b = bench.epoch_batches(w)
         assert b[-1][1] == last and sum(n for _, n in b) == w.S
         assert all(n == w.B for _, n in b[:-1])
+
+
+def test_every_reported_kernel_has_a_source_file():
+    """Traffic entries are tied to the source file that defines their kernel;
+    every name the library can report (its variant notes) must resolve."""
+    import re
+    csrc = os.path.join(ROOT, "paper_2206_08369_amd", "csrc")
+    names = set()
+    for f in os.listdir(csrc):
+        if f.endswith(".hip"):
+            names |= set(re.findall(r'note_variant\("(\w+)"', open(os.path.join(csrc, f)).read()))
+    assert {"k_fwd_x3", "k_bwd_x3", "k_gemm_x3", "k_gemm_bf", "k_gemm_nt"} <= names
+    for n in names:
+        src = bench.kernel_source(n)
+        assert src is not None, n
+        assert re.search(r"\bvoid\s+%s\s*\(" % bench.VARIANT_KERNEL.get(n, n),
+                         open(os.path.join(csrc, src)).read()), n
+    assert bench.kernel_source("k_gemm_x3") == bench.kernel_source("k_gemm_bf") == "k_gemm_bf16.hip"
+    assert bench.kernel_source("k_bwd_x3<6, 2, 2, 512, true>") == "k_lds.hip"
+    # the digest changes with the kernel's own file, not with other kernels' files
+    assert bench.kernel_source_digest("k_m3_fwd") != bench.kernel_source_digest("k_fwd_x3")
+
+
+def test_profile_roles_read_the_epilogue_argument():
+    import bench_profiles as bp
+    assert bp.role_of("k_gemm_bf<4, 2, 2, 4, 16, false, 0, true>", "fp32") == "gemm_fwd"
+    assert bp.role_of("k_gemm_bf<4, 2, 2, 4, 32, true, 1, false>", "bf16") == "gemm_bwd"
+    assert bp.role_of("k_gemm_bf<4, 2, 2, 4, 32, false, 2, false>", "bf16") == "gemm_grad"
+    assert bp.role_of("k_gemm_nt<4, 2, 1>", "fp32") == "gemm_bwd"
+    assert bp.role_of("k_bwd_x3<6, 2, 2, 512, true>", "fp32") == "bwd_fused"
