@@ -517,6 +517,35 @@ def test_nonfinite_losses_are_counted(pm, torch):
     net.close()
 
 
+def test_largest_batch(pm, orc, torch):
+    """The largest batch the library takes (2^20 samples, the three-piece
+    GEMMs with 4096 q tiles and a 2^20-deep k loop): logits, per-model losses
+    and the weights after one step against the oracle.  The weights are
+    compared relative to their own size, where the fp32 accumulation over
+    2^20 samples in the gradients (an update of about 1% of each weight)
+    stays far inside the bar."""
+    hs = np.array([1, 3, 2, 5, 16, 1], np.int32)
+    acts = np.array([0, 1, 2, 3, 6, 9], np.int32)
+    F, O, B, lr = 3, 2, 1 << 20, 0.05
+    X, y = wl.make_dataset(F, O, B, seed=77)
+    net = make_net(pm, F, O, hs, acts, seed=15)
+    W1, W2 = net.get_params()
+    Xd, yd = dev(torch, X), dev(torch, y)
+    got = net.forward(Xd).cpu().numpy()
+    assert err_logits(got, orc.forward(hs, acts, W1, W2, X)).max() <= TOL_STEP
+    net.train_step(Xd, yd, lr)
+    loss = net.losses()
+    T1, T2 = net.get_params()
+    O1, O2, ol = orc.train(hs, acts, W1, W2, X, y, [(0, B)], lr)
+    allow = orc.gradients(hs, acts, W1, W2, X, y)[3]
+    assert err_losses(loss, ol).max() <= TOL_STEP
+    assert err_rows(T1, O1, hs, lr * allow).max() <= TOL_STEP
+    assert err_cols(T2, O2, hs).max() <= TOL_STEP
+    v = net.kernel_variants()
+    assert v["gemm_fwd"] == ("k_gemm_x3", 2)
+    net.close()
+
+
 def test_bad_batch_arguments(pm, torch):
     net = make_net(pm, 3, 2, [2, 3], [0, 1])
     X = dev(torch, np.ones((4, 3), np.float32))
