@@ -62,6 +62,10 @@ CASES = {
     "f1": dict(M=8, hmax=9, F=1, O=2, B=17),
     "b1100": dict(M=6, hmax=20, F=20, O=2, B=1100),
     "all_width_one": dict(hs=[1] * 70, F=7, O=4, B=20),
+    # a pack of one model: wide (wider than the tile limit at this size, so
+    # two halves) and of width one
+    "one_model_wide": dict(hs=[1000], F=20, O=2, B=40),
+    "one_model_narrow": dict(hs=[1], F=5, O=3, B=9),
     # shapes of the LDS-resident kernels: batch padded to 16..256, F giving
     # 1, 2, 4, 7 and 8 sixteen-wide column tiles, K tails of 0, 4 and 12
     "f100_b250": dict(M=30, hmax=300, F=100, O=2, B=250),
